@@ -1,0 +1,181 @@
+/*
+ * svmx.h -- C ABI of libsvmx.so: kernel-SVM training by SMO on one AMD Instinct MI355X (gfx950).
+ *
+ * The problem (paper, Section III.A): samples X = {x_1..x_n}, x_i in R^d, labels y_i in {+1,-1};
+ * find the maximum-margin separator, made non-linear by a kernel.  The kernel here is the
+ * Gaussian RBF K(a,b) = exp(-gamma * |a-b|^2) (the kernel the paper names, Section III.C).
+ * Training solves the dual QP by sequential minimal optimisation: each step updates two
+ * Lagrange multipliers under the KKT conditions (Section III.B).  Multiclass training is
+ * one-against-one: m classes give m(m-1)/2 independent binary problems (Section III.A).
+ *
+ * The dual solved:  max W(a) = sum_i a_i - 1/2 sum_ij a_i a_j y_i y_j K_ij
+ *                   s.t. sum_i a_i y_i = 0,  0 <= a_i <= C.
+ * With f_i = sum_j a_j y_j K_ij - y_i the working pair of each step is the maximal violating
+ * pair u = argmin_{I_up} f, l = argmax_{I_low} f (ties to the smaller index), where
+ *   I_up  = {i : (y_i=+1 and a_i<C) or (y_i=-1 and a_i>0)},
+ *   I_low = {i : (y_i=+1 and a_i>0) or (y_i=-1 and a_i<C)};
+ * training stops when b_low - b_up <= tol (b_up = f_u, b_low = f_l) and returns
+ * b = (b_up + b_low)/2.  Decision values are d(x) = sum_{a_i>0} a_i y_i K(x_i, x) - b; the
+ * predicted label is +1 iff d(x) > 0.
+ *
+ * Conventions for every entry point:
+ *  - "device" pointers are HIP device memory of the current device; "host" pointers are
+ *    ordinary host memory.  X arrays are fp32, row-major [rows][d], rows contiguous.
+ *  - The caller owns every buffer, including the device workspace, whose size is given by
+ *    the matching *_workspace_bytes query.  The library keeps no state between calls
+ *    except the loaded code object and a thread-local error message.
+ *  - All device work is enqueued on options->stream (a hipStream_t; NULL = the null stream).
+ *    Every call returns only after its outputs are complete.
+ *  - Negative status: nothing was written to the outputs that can be relied upon, nothing
+ *    leaks; svm_last_error() explains.  SVM_NOT_CONVERGED (positive) means the iteration
+ *    limit was reached: alpha is feasible (0 <= a <= C, sum a y = 0) and b is the current
+ *    midpoint.
+ *  - Calls on one device that overlap in time must use distinct workspaces.
+ */
+#ifndef SVMX_H
+#define SVMX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SVM_OK = 0,
+  SVM_NOT_CONVERGED = 1,
+  SVM_EINVAL = -1,     /* invalid argument */
+  SVM_ENOMEM = -2,     /* problem too large for the device or for 64-bit sizes */
+  SVM_EDEVICE = -3,    /* a HIP call failed, or a device-side wait exceeded its time limit */
+  SVM_EWORKSPACE = -4  /* workspace NULL or smaller than the size query returned */
+} svm_status;
+
+/* Where kernel rows come from during the solve. */
+typedef enum {
+  SVM_GRAM_AUTO = 0, /* full Gram when it fits gram_budget_bytes, else row path */
+  SVM_GRAM_ON = 1,   /* precompute the full fp32 Gram (MFMA) and read rows from it */
+  SVM_GRAM_OFF = 2   /* row path: evaluate the two kernel rows from X at every step */
+} svm_gram_mode;
+
+typedef struct {
+  int32_t struct_size;       /* = sizeof(svm_options); set by svm_default_options */
+  int32_t gram;              /* svm_gram_mode */
+  int64_t gram_budget_bytes; /* AUTO picks the Gram when 4*n*ld <= budget (ld = n rounded up to 64);
+                                0 = 200 GiB */
+  int64_t row_cache_bytes;   /* row path: HBM bytes for cached kernel rows; 0 = none */
+  int64_t max_iter;          /* 0 = max(10^7, 100 n) SMO steps */
+  int32_t check_every;       /* SMO steps per device launch between host convergence checks
+                                (the host-side check "every set of iterations", Section III.B);
+                                0 = 65536.  Results do not depend on it. */
+  int32_t trace_len;         /* record the selection of the first trace_len steps */
+  int32_t *trace_ws;         /* host [2*trace_len]: (u, l) of each step, or NULL */
+  double *trace_b;           /* host [2*trace_len]: (b_up, b_low) of each step, or NULL */
+  double *f_out;             /* device [n]: final f, or NULL (binary training only) */
+  void *stream;              /* hipStream_t, or NULL */
+  int32_t workgroups;        /* solver workgroups per binary problem; 0 = automatic */
+  int32_t reserved;
+} svm_options;
+
+typedef struct {
+  int64_t iterations;   /* SMO steps taken */
+  int64_t n_sv;         /* samples with a_i > 0 */
+  int64_t n_bound_sv;   /* samples with a_i = C */
+  double b_up, b_low;   /* selection values of the final step */
+  double dual_obj;      /* W(a) = 1/2 sum a - 1/2 sum a y f */
+  int32_t gram_used;    /* 1 if the full Gram was precomputed */
+  int32_t launches;     /* solver launches (host convergence checks) */
+  double t_gram, t_solve, t_finalize, t_total; /* seconds */
+  double t_kernel;      /* seconds the solver kernel ran, summed over its launches (HIP events on
+                           the launch stream) */
+} svm_stats;
+
+/* Fill *o with the defaults above. */
+void svm_default_options(svm_options *o);
+
+/* Device workspace bytes svm_train needs for an n x d problem under options o (NULL =
+ * defaults); -1 if the sizes overflow or are invalid. */
+int64_t svm_train_workspace_bytes(int64_t n, int64_t d, const svm_options *o);
+
+/*
+ * Binary training (Sections III.A and III.B).
+ *   X      device fp32 [n][d]          training samples
+ *   y      device int32 [n]            labels, each +1 or -1, both present
+ *   C      > 0, finite                  box constraint
+ *   gamma  > 0, finite                  RBF width
+ *   tol    > 0, finite                  stopping tolerance on b_low - b_up
+ *   alpha  device fp64 [n], out        Lagrange multipliers
+ *   b      host double, out            bias of d(x) = sum a y K - b
+ *   workspace/workspace_bytes          device scratch of at least svm_train_workspace_bytes
+ *   o      options or NULL;  st  host stats out or NULL
+ * EINVAL: n<2, d<1, non-finite or non-positive C/gamma/tol, NULL pointers, a label not in
+ * {+1,-1} or only one class present.
+ */
+svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma, double tol,
+                     double *alpha, double *b, void *workspace, int64_t workspace_bytes, const svm_options *o,
+                     svm_stats *st);
+
+/* Device workspace bytes svm_predict needs. */
+int64_t svm_predict_workspace_bytes(int64_t n, int64_t d, int64_t m);
+
+/*
+ * Decision values d(x_q) = sum_{a_i>0} a_i y_i K(x_i, x_q) - b for m test samples.
+ *   X_train device fp32 [n][d], y device int32 [n], alpha device fp64 [n], b host value,
+ *   X_test device fp32 [m][d], dec device fp64 [m] out.  m = 0 is allowed (nothing written).
+ */
+svm_status svm_predict(const float *X_train, const int32_t *y, const double *alpha, double b, int64_t n, int64_t d,
+                       double gamma, const float *X_test, int64_t m, double *dec, void *workspace,
+                       int64_t workspace_bytes, const svm_options *o);
+
+/* Device workspace bytes svm_train_ovo needs for n samples in k classes. */
+int64_t svm_train_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, const svm_options *o);
+
+/*
+ * One-against-one training (Section III.A; the binary problems run side by side on the one
+ * device, Section III.B).  P = k(k-1)/2 pairs (a<b) in lexicographic order; in pair (a,b)
+ * class a is +1 and class b is -1, and the pair's local sample order is the class-a samples
+ * by increasing original index followed by the class-b samples likewise.
+ *   label  device int32 [n], values 0..k-1, every class present
+ *   alpha  device fp64 [(k-1)*n] out: the pairs' multipliers packed in pair order, each pair
+ *          in its local sample order (pair p occupies n_a + n_b entries)
+ *   b      host double [P] out;  st  host svm_stats [P] out or NULL
+ */
+svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k, double C,
+                         double gamma, double tol, double *alpha, double *b, void *workspace,
+                         int64_t workspace_bytes, const svm_options *o, svm_stats *st);
+
+/* Device workspace bytes svm_predict_ovo needs. */
+int64_t svm_predict_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, int64_t m);
+
+/*
+ * One-against-one prediction with the outputs of svm_train_ovo.
+ *   dec   device fp64 [m][P] out: decision value of every pair
+ *   pred  device int32 [m] out: class with most votes (pair (a,b) votes a iff d>0, else b);
+ *         ties go to the smaller class id
+ */
+svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k,
+                           const double *alpha, const double *b, double gamma, const float *X_test, int64_t m,
+                           double *dec, int32_t *pred, void *workspace, int64_t workspace_bytes,
+                           const svm_options *o);
+
+/*
+ * The kernel rows of the hot path, exposed for verification:
+ * out[q][j] = K(x_{rows[q]}, x_j) for j < n, evaluated the way the row path evaluates them.
+ *   rows device int64 [r] (each in [0,n)), out device fp32 [r][n].
+ */
+svm_status svm_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, const int64_t *rows, int64_t r,
+                           float *out, const svm_options *o);
+
+/*
+ * The full fp32 RBF Gram the Gram path precomputes (MFMA X X^T with a row-norm epilogue):
+ * G[i*ld + j] = K(x_i, x_j) for i, j < n; ld >= n.  G device fp32 [n][ld].
+ */
+svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G, int64_t ld, const svm_options *o);
+
+/* Thread-local message for the last non-OK status of this thread ("" if none). */
+const char *svm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SVMX_H */

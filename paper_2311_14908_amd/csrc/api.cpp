@@ -1,0 +1,702 @@
+// api.cpp -- the C ABI of libsvmx.so (declared in include/svmx.h): argument checks, workspace
+// planning, the host-side convergence loop and the one-vs-one orchestration.
+//
+// The paper runs the SMO iterations on the device and checks convergence on the host after
+// every set of iterations (Section III.B).  Here each solver launch advances every running
+// problem by up to check_every steps on the device; the host then reads the per-problem
+// control blocks and launches again while any problem is still running.  Because the device
+// stops a problem by itself once the stop rule holds, results do not depend on check_every.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+#include "svmx.h"
+
+using namespace svmx;
+
+namespace {
+
+thread_local std::string g_err;
+
+svm_status fail(svm_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIPCHK(expr)                                                                      \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess) return fail(SVM_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int64_t DEFAULT_GRAM_BUDGET = 200LL << 30;  // bytes of HBM the Gram may take by default
+constexpr int32_t DEFAULT_CHECK_EVERY = 65536;
+constexpr int64_t ALIGN = 256;
+constexpr int32_t CACHE_CAP_MAX = 4096;               // row-cache slots (tags live in LDS)
+constexpr double SPIN_SECONDS = 2.0;                  // longest a device-side wait may last
+constexpr int64_t LDS_BYTES = 160 * 1024;
+constexpr int32_t MAX_CLASSES = 64;
+
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
+
+struct Opts {
+  int32_t gram;
+  int64_t gram_budget;
+  int64_t row_cache_bytes;
+  int64_t max_iter;
+  int32_t check_every;
+  int32_t trace_len;
+  int32_t *trace_ws;
+  double *trace_b;
+  double *f_out;
+  hipStream_t stream;
+  int32_t workgroups;
+};
+
+bool resolve(const svm_options *o, int64_t n, Opts *r) {
+  svm_options d;
+  svm_default_options(&d);
+  if (!o) o = &d;
+  if (o->struct_size != (int32_t)sizeof(svm_options)) return false;
+  r->gram = o->gram;
+  r->gram_budget = o->gram_budget_bytes > 0 ? o->gram_budget_bytes : DEFAULT_GRAM_BUDGET;
+  r->row_cache_bytes = std::max<int64_t>(0, o->row_cache_bytes);
+  r->max_iter = o->max_iter > 0 ? o->max_iter : std::max<int64_t>(10000000, 100 * n);
+  r->check_every = o->check_every > 0 ? o->check_every : DEFAULT_CHECK_EVERY;
+  r->trace_len = std::max<int32_t>(0, o->trace_len);
+  r->trace_ws = o->trace_ws;
+  r->trace_b = o->trace_b;
+  r->f_out = o->f_out;
+  r->stream = reinterpret_cast<hipStream_t>(o->stream);
+  r->workgroups = std::max<int32_t>(0, o->workgroups);
+  return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF;
+}
+
+// How a problem of n samples is spread over workgroups.
+struct Shape {
+  int32_t nwg, per_wg, per_thread;
+};
+
+bool choose_shape(int64_t n, bool gram, int32_t requested, Shape *s) {
+  const int64_t BS = solver_block_size(), MAXP = max_per_thread();
+  int64_t nwg;
+  if (requested > 0)
+    nwg = requested;
+  else if (gram)
+    nwg = n <= 4096 ? 1 : std::min<int64_t>(256, std::max<int64_t>(8, (n + 1535) / 1536));
+  else
+    nwg = std::min<int64_t>(256, std::max<int64_t>(1, (n + 127) / 128));
+  nwg = std::max<int64_t>(1, std::min<int64_t>(nwg, n));
+  if ((n + nwg - 1) / nwg > BS * MAXP) nwg = (n + BS * MAXP - 1) / (BS * MAXP);
+  int64_t per_wg = (n + nwg - 1) / nwg;
+  nwg = (n + per_wg - 1) / per_wg;  // no empty workgroups
+  int64_t per = (per_wg + BS - 1) / BS, p = 1;
+  while (p < per) p <<= 1;
+  if (p > MAXP || nwg > 65536) return false;
+  s->nwg = (int32_t)nwg;
+  s->per_wg = (int32_t)per_wg;
+  s->per_thread = (int32_t)p;
+  return true;
+}
+
+struct Layout {
+  int64_t total = 0;
+  int64_t add(int64_t bytes) {
+    int64_t off = round_up(total, ALIGN);
+    total = off + std::max<int64_t>(bytes, 0);
+    return off;
+  }
+};
+
+// ---------------------------------------------------------------------------- binary plan
+struct TrainPlan {
+  bool gram;
+  int64_t ld;
+  Shape shape;
+  int32_t cache_cap;
+  int64_t off_f, off_gram, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_tul, off_tb, off_fin,
+      off_err;
+  int64_t total;
+};
+
+svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
+  if (n < 2 || d < 1) return fail(SVM_EINVAL, "need n >= 2 and d >= 1 (got n=%lld, d=%lld)", (long long)n, (long long)d);
+  if (n > 0x7ffffffeLL) return fail(SVM_ENOMEM, "n=%lld exceeds the 32-bit sample index", (long long)n);
+  if (d > (INT64_MAX / 8) / n) return fail(SVM_ENOMEM, "n*d overflows");
+  p->ld = round_up(n, 64);
+  const double gram_bytes = 4.0 * (double)n * (double)p->ld;
+  if (o.gram == SVM_GRAM_ON)
+    p->gram = true;
+  else if (o.gram == SVM_GRAM_OFF)
+    p->gram = false;
+  else
+    p->gram = gram_bytes <= (double)o.gram_budget;
+  if (p->gram && gram_bytes > 9.0e18) return fail(SVM_ENOMEM, "Gram size overflows");
+  if (!choose_shape(n, p->gram, o.workgroups, &p->shape)) return fail(SVM_ENOMEM, "problem too large to place");
+  p->cache_cap = 0;
+  if (!p->gram) {
+    if (o.row_cache_bytes > 0)
+      p->cache_cap = (int32_t)std::min<int64_t>(CACHE_CAP_MAX, std::min<int64_t>(n, o.row_cache_bytes / (4 * p->ld)));
+    const int64_t lds = (2 * d + 2 * (int64_t)solver_block_size() * p->shape.per_thread) * 4 + 4LL * p->cache_cap + 64 +
+                        1024;
+    if (lds > LDS_BYTES)
+      return fail(SVM_EINVAL, "row path: d=%lld does not fit the 160 KiB LDS of a workgroup; use the Gram path",
+                  (long long)d);
+  }
+  Layout L;
+  p->off_f = L.add(8 * n);
+  p->off_gram = p->gram ? L.add((int64_t)gram_bytes) : -1;
+  p->off_cache = p->cache_cap ? L.add(4LL * p->cache_cap * p->ld) : -1;
+  p->off_tags = p->cache_cap ? L.add(4LL * p->cache_cap * p->shape.nwg) : -1;
+  p->off_ctl = L.add(sizeof(Ctl));
+  p->off_prob = L.add(sizeof(Prob));
+  p->off_wgp = L.add(4LL * p->shape.nwg);
+  p->off_slots = L.add(8LL * 2 * p->shape.nwg * SLOT_WORDS);
+  p->off_tul = L.add(4LL * 2 * o.trace_len);
+  p->off_tb = L.add(8LL * 2 * o.trace_len);
+  p->off_fin = L.add(8 * 4);
+  p->off_err = L.add(16);
+  p->total = round_up(L.total, ALIGN);
+  return SVM_OK;
+}
+
+uint64_t spin_ticks() {
+  int dev = 0, khz = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+      khz <= 0)
+    khz = 100000;
+  return (uint64_t)(SPIN_SECONDS * 1000.0 * (double)khz);
+}
+
+struct Timer {
+  hipEvent_t a = nullptr, b = nullptr;
+  ~Timer() {
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+  }
+  hipError_t init() {
+    hipError_t e = hipEventCreate(&a);
+    if (e != hipSuccess) return e;
+    return hipEventCreate(&b);
+  }
+  double seconds() {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, a, b) != hipSuccess) return 0.0;
+    return ms * 1e-3;
+  }
+};
+
+// Launch the solver until no problem is running.  Returns SVM_OK or a negative status.
+svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t per_thread, bool gram, Ctl *d_ctl,
+                      hipStream_t stream, int32_t *launches, std::vector<Ctl> &h, double *t_kernel) {
+  int32_t herr = 0;
+  Timer tk;
+  HIPCHK(tk.init());
+  *t_kernel = 0.0;
+  h.assign(nprob, Ctl{});
+  std::vector<int64_t> prev(nprob, -1);
+  for (;;) {
+    int32_t maxres = 0;
+    HIPCHK(hipEventRecord(tk.a, stream));
+    hipError_t e = launch_solver(sp, total_wg, per_thread, gram, stream, &maxres);
+    if (e == hipErrorCooperativeLaunchTooLarge)
+      return fail(SVM_ENOMEM, "%d solver workgroups do not fit on the device at once (at most %d)", total_wg, maxres);
+    if (e != hipSuccess) return fail(SVM_EDEVICE, "solver launch: %s", hipGetErrorString(e));
+    ++*launches;
+    HIPCHK(hipEventRecord(tk.b, stream));
+    HIPCHK(hipMemcpyAsync(h.data(), d_ctl, sizeof(Ctl) * nprob, hipMemcpyDeviceToHost, stream));
+    HIPCHK(hipMemcpyAsync(&herr, sp.error, sizeof(herr), hipMemcpyDeviceToHost, stream));
+    HIPCHK(hipStreamSynchronize(stream));
+    if (herr) return fail(SVM_EDEVICE, "a device-side wait exceeded its %.1f s limit", SPIN_SECONDS);
+    *t_kernel += tk.seconds();
+    bool running = false, progress = false;
+    for (int32_t q = 0; q < nprob; ++q) {
+      if (h[q].status == ST_TIMEOUT)
+        return fail(SVM_EDEVICE, "a device-side wait exceeded its %.1f s limit (problem %d, step %lld)", SPIN_SECONDS, q,
+                    (long long)h[q].t);
+      if (h[q].status == ST_RUNNING) running = true;
+      if (h[q].t != prev[q]) progress = true;
+      prev[q] = h[q].t;
+    }
+    if (!running) return SVM_OK;
+    if (!progress) return fail(SVM_EDEVICE, "solver made no progress");
+  }
+}
+
+svm_status check_labels_pm1(const int32_t *y, int64_t n, hipStream_t stream) {
+  std::vector<int32_t> h(n);
+  HIPCHK(hipMemcpyAsync(h.data(), y, 4 * n, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  int64_t pos = 0, neg = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (h[i] == 1)
+      ++pos;
+    else if (h[i] == -1)
+      ++neg;
+    else
+      return fail(SVM_EINVAL, "label y[%lld] = %d is not +1 or -1", (long long)i, h[i]);
+  }
+  if (!pos || !neg) return fail(SVM_EINVAL, "both classes must be present (%lld positive, %lld negative)", (long long)pos,
+                                (long long)neg);
+  return SVM_OK;
+}
+
+// ---------------------------------------------------------------------------- one-vs-one
+struct OvoPlan {
+  bool gram;
+  int64_t ld;
+  int32_t P;
+  int64_t off_perm, off_xs, off_f, off_gram, off_ctl, off_prob, off_wgp, off_slots, off_fin, off_err;
+  int64_t total;
+};
+
+constexpr int32_t OVO_MAX_WG_PER_PAIR = 256;
+
+svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) {
+  if (n < 2 || d < 1) return fail(SVM_EINVAL, "need n >= 2 and d >= 1");
+  if (k < 2 || k > MAX_CLASSES) return fail(SVM_EINVAL, "k=%d must be in [2, %d]", k, MAX_CLASSES);
+  if (n > 0x7ffffffeLL) return fail(SVM_ENOMEM, "n too large");
+  if (d > (INT64_MAX / 8) / n) return fail(SVM_ENOMEM, "n*d overflows");
+  p->P = k * (k - 1) / 2;
+  p->ld = round_up(n, 64);
+  const double gram_bytes = 4.0 * (double)n * (double)p->ld;
+  p->gram = o.gram == SVM_GRAM_ON || (o.gram == SVM_GRAM_AUTO && gram_bytes <= (double)o.gram_budget);
+  if (!p->gram) {
+    const int64_t lds = (2 * d + 2 * (int64_t)solver_block_size() * max_per_thread()) * 4 + 1024;
+    if (lds > LDS_BYTES) return fail(SVM_EINVAL, "row path: d=%lld does not fit LDS", (long long)d);
+  }
+  Layout L;
+  p->off_perm = L.add(4 * n);
+  p->off_xs = L.add(4 * n * d);
+  p->off_f = L.add(8 * (int64_t)(k - 1) * n);
+  p->off_gram = p->gram ? L.add((int64_t)gram_bytes) : -1;
+  p->off_ctl = L.add((int64_t)sizeof(Ctl) * p->P);
+  p->off_prob = L.add((int64_t)sizeof(Prob) * p->P);
+  p->off_wgp = L.add(4LL * p->P * OVO_MAX_WG_PER_PAIR);
+  p->off_slots = L.add(8LL * 2 * SLOT_WORDS * p->P * OVO_MAX_WG_PER_PAIR);
+  p->off_fin = L.add(8LL * 4 * p->P);
+  p->off_err = L.add(16);
+  p->total = round_up(L.total, ALIGN);
+  return SVM_OK;
+}
+
+// Class counts and the stable class-sorted order of the labels (host copy).
+svm_status class_sort(const int32_t *label, int64_t n, int32_t k, hipStream_t stream, std::vector<int32_t> &perm,
+                      std::vector<int64_t> &start, std::vector<int64_t> &cnt) {
+  std::vector<int32_t> h(n);
+  HIPCHK(hipMemcpyAsync(h.data(), label, 4 * n, hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  cnt.assign(k, 0);
+  for (int64_t i = 0; i < n; ++i) {
+    if (h[i] < 0 || h[i] >= k) return fail(SVM_EINVAL, "label[%lld] = %d is outside 0..%d", (long long)i, h[i], k - 1);
+    cnt[h[i]]++;
+  }
+  for (int32_t c = 0; c < k; ++c)
+    if (!cnt[c]) return fail(SVM_EINVAL, "class %d has no samples", c);
+  start.assign(k, 0);
+  for (int32_t c = 1; c < k; ++c) start[c] = start[c - 1] + cnt[c - 1];
+  perm.assign(n, 0);
+  std::vector<int64_t> pos(start);
+  for (int64_t i = 0; i < n; ++i) perm[pos[h[i]]++] = (int32_t)i;
+  return SVM_OK;
+}
+
+}  // namespace
+
+// ============================================================================ C ABI
+extern "C" {
+
+void svm_default_options(svm_options *o) {
+  if (!o) return;
+  std::memset(o, 0, sizeof(*o));
+  o->struct_size = (int32_t)sizeof(svm_options);
+  o->gram = SVM_GRAM_AUTO;
+  o->check_every = DEFAULT_CHECK_EVERY;
+}
+
+const char *svm_last_error(void) { return g_err.c_str(); }
+
+int64_t svm_train_workspace_bytes(int64_t n, int64_t d, const svm_options *o) {
+  Opts r;
+  if (!resolve(o, n, &r)) return -1;
+  TrainPlan p;
+  if (plan_train(n, d, r, &p) != SVM_OK) return -1;
+  return p.total;
+}
+
+svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma, double tol,
+                     double *alpha, double *b, void *workspace, int64_t workspace_bytes, const svm_options *o,
+                     svm_stats *st) {
+  const auto t_start = std::chrono::steady_clock::now();
+  g_err.clear();
+  if (!X || !y || !alpha || !b) return fail(SVM_EINVAL, "NULL pointer argument");
+  if (!finite_pos(C) || !finite_pos(gamma) || !finite_pos(tol))
+    return fail(SVM_EINVAL, "C, gamma and tol must be finite and > 0");
+  Opts r;
+  if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options (struct_size or gram mode)");
+  if (r.trace_len > 0 && (int64_t)r.trace_len > r.max_iter + 1) r.trace_len = (int32_t)(r.max_iter + 1);
+  TrainPlan p;
+  svm_status s0 = plan_train(n, d, r, &p);
+  if (s0 != SVM_OK) return s0;
+  if (!workspace || workspace_bytes < p.total)
+    return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)p.total,
+                (long long)workspace_bytes);
+  hipStream_t stream = r.stream;
+  s0 = check_labels_pm1(y, n, stream);
+  if (s0 != SVM_OK) return s0;
+
+  char *ws = static_cast<char *>(workspace);
+  double *f = reinterpret_cast<double *>(ws + p.off_f);
+  float *G = p.gram ? reinterpret_cast<float *>(ws + p.off_gram) : nullptr;
+  Ctl *ctl = reinterpret_cast<Ctl *>(ws + p.off_ctl);
+  Prob *dprob = reinterpret_cast<Prob *>(ws + p.off_prob);
+  int32_t *wgp = reinterpret_cast<int32_t *>(ws + p.off_wgp);
+  u64 *slots = reinterpret_cast<u64 *>(ws + p.off_slots);
+  int32_t *tul = reinterpret_cast<int32_t *>(ws + p.off_tul);
+  double *tb = reinterpret_cast<double *>(ws + p.off_tb);
+  double *fin = reinterpret_cast<double *>(ws + p.off_fin);
+  int32_t *err = reinterpret_cast<int32_t *>(ws + p.off_err);
+
+  Prob hp{};
+  hp.n = n;
+  hp.off0 = 0;
+  hp.len0 = n;
+  hp.off1 = n;
+  hp.y = y;
+  hp.alpha = alpha;
+  hp.f = f;
+  hp.ctl = ctl;
+  hp.slots = slots;
+  hp.trace_ul = r.trace_len ? tul : nullptr;
+  hp.trace_b = r.trace_len ? tb : nullptr;
+  hp.trace_len = r.trace_len;
+  hp.wg0 = 0;
+  hp.nwg = p.shape.nwg;
+  hp.per_wg = p.shape.per_wg;
+  std::vector<int32_t> hwgp(p.shape.nwg, 0);
+  HIPCHK(hipMemcpyAsync(dprob, &hp, sizeof(Prob), hipMemcpyHostToDevice, stream));
+  HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
+  HIPCHK(hipMemsetAsync(err, 0, 16, stream));
+  if (p.cache_cap)
+    HIPCHK(hipMemsetAsync(ws + p.off_tags, 0xff, 4LL * p.cache_cap * p.shape.nwg, stream));
+
+  Timer tg, ts, tf;
+  HIPCHK(tg.init());
+  HIPCHK(ts.init());
+  HIPCHK(tf.init());
+  HIPCHK(hipEventRecord(tg.a, stream));
+  if (p.gram) HIPCHK(launch_gram(X, n, d, (float)gamma, G, p.ld, stream));
+  HIPCHK(hipEventRecord(tg.b, stream));
+
+  HIPCHK(hipEventRecord(ts.a, stream));
+  HIPCHK(launch_solver_init(dprob, 1, n, stream));
+  SolveParams sp{};
+  sp.probs = dprob;
+  sp.wg_prob = wgp;
+  sp.C = C;
+  sp.tol = tol;
+  sp.gamma = gamma;
+  sp.max_iter = r.max_iter;
+  sp.steps = r.check_every;
+  sp.gram = G;
+  sp.ld = p.ld;
+  sp.X = X;
+  sp.d = d;
+  sp.cache = p.cache_cap ? reinterpret_cast<float *>(ws + p.off_cache) : nullptr;
+  sp.cache_tags = p.cache_cap ? reinterpret_cast<int32_t *>(ws + p.off_tags) : nullptr;
+  sp.cache_cap = p.cache_cap;
+  sp.spin_limit = spin_ticks();
+  sp.error = err;
+  int32_t launches = 0;
+  std::vector<Ctl> hc;
+  double t_kernel = 0.0;
+  svm_status s1 = run_solver(sp, 1, p.shape.nwg, p.shape.per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel);
+  if (s1 != SVM_OK) return s1;
+  HIPCHK(hipEventRecord(ts.b, stream));
+
+  HIPCHK(hipEventRecord(tf.a, stream));
+  HIPCHK(launch_finalize(dprob, 1, C, fin, stream));
+  double hfin[4];
+  HIPCHK(hipMemcpyAsync(hfin, fin, sizeof(hfin), hipMemcpyDeviceToHost, stream));
+  if (r.trace_len) {
+    const int64_t steps = std::min<int64_t>(r.trace_len, hc[0].t + 1);
+    if (r.trace_ws) HIPCHK(hipMemcpyAsync(r.trace_ws, tul, 4 * 2 * steps, hipMemcpyDeviceToHost, stream));
+    if (r.trace_b) HIPCHK(hipMemcpyAsync(r.trace_b, tb, 8 * 2 * steps, hipMemcpyDeviceToHost, stream));
+  }
+  if (r.f_out) HIPCHK(hipMemcpyAsync(r.f_out, f, 8 * n, hipMemcpyDeviceToDevice, stream));
+  HIPCHK(hipEventRecord(tf.b, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+
+  const Ctl &c = hc[0];
+  *b = 0.5 * (c.b_up + c.b_low);
+  if (st) {
+    st->iterations = c.t;
+    st->n_sv = (int64_t)hfin[2];
+    st->n_bound_sv = (int64_t)hfin[3];
+    st->b_up = c.b_up;
+    st->b_low = c.b_low;
+    st->dual_obj = 0.5 * hfin[0] - 0.5 * hfin[1];
+    st->gram_used = p.gram ? 1 : 0;
+    st->launches = launches;
+    st->t_gram = p.gram ? tg.seconds() : 0.0;
+    st->t_solve = ts.seconds();
+    st->t_finalize = tf.seconds();
+    st->t_total = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
+    st->t_kernel = t_kernel;
+  }
+  return c.status == ST_MAXITER ? SVM_NOT_CONVERGED : SVM_OK;
+}
+
+int64_t svm_predict_workspace_bytes(int64_t n, int64_t d, int64_t m) {
+  if (n < 1 || d < 1 || m < 0) return -1;
+  return ALIGN;
+}
+
+svm_status svm_predict(const float *X_train, const int32_t *y, const double *alpha, double b, int64_t n, int64_t d,
+                       double gamma, const float *X_test, int64_t m, double *dec, void *workspace,
+                       int64_t workspace_bytes, const svm_options *o) {
+  g_err.clear();
+  (void)workspace;
+  (void)workspace_bytes;
+  if (n < 1 || d < 1 || m < 0) return fail(SVM_EINVAL, "need n >= 1, d >= 1, m >= 0");
+  if (!X_train || !y || !alpha || (m > 0 && (!X_test || !dec))) return fail(SVM_EINVAL, "NULL pointer argument");
+  if (!finite_pos(gamma) || !std::isfinite(b)) return fail(SVM_EINVAL, "gamma must be finite and > 0, b finite");
+  if (d > (INT64_MAX / 8) / std::max<int64_t>(n, m)) return fail(SVM_ENOMEM, "sizes overflow");
+  if ((int64_t)8 * 4 * d > LDS_BYTES) return fail(SVM_EINVAL, "d=%lld too large for the staged test tile", (long long)d);
+  Opts r;
+  if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options");
+  if (m == 0) return SVM_OK;
+  HIPCHK(launch_predict_map(X_train, d, 0, n, n, y, nullptr, alpha, n, gamma, X_test, m, b, dec, 1, r.stream));
+  HIPCHK(hipStreamSynchronize(r.stream));
+  return SVM_OK;
+}
+
+int64_t svm_train_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, const svm_options *o) {
+  Opts r;
+  if (!resolve(o, n, &r)) return -1;
+  OvoPlan p;
+  if (plan_ovo(n, d, k, r, &p) != SVM_OK) return -1;
+  return p.total;
+}
+
+svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k, double C,
+                         double gamma, double tol, double *alpha, double *b, void *workspace,
+                         int64_t workspace_bytes, const svm_options *o, svm_stats *st) {
+  const auto t_start = std::chrono::steady_clock::now();
+  g_err.clear();
+  if (!X || !label || !alpha || !b) return fail(SVM_EINVAL, "NULL pointer argument");
+  if (!finite_pos(C) || !finite_pos(gamma) || !finite_pos(tol))
+    return fail(SVM_EINVAL, "C, gamma and tol must be finite and > 0");
+  Opts r;
+  if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options");
+  OvoPlan p;
+  svm_status s0 = plan_ovo(n, d, k, r, &p);
+  if (s0 != SVM_OK) return s0;
+  if (!workspace || workspace_bytes < p.total)
+    return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)p.total,
+                (long long)workspace_bytes);
+  hipStream_t stream = r.stream;
+  std::vector<int32_t> perm;
+  std::vector<int64_t> start, cnt;
+  s0 = class_sort(label, n, k, stream, perm, start, cnt);
+  if (s0 != SVM_OK) return s0;
+
+  char *ws = static_cast<char *>(workspace);
+  int32_t *dperm = reinterpret_cast<int32_t *>(ws + p.off_perm);
+  float *Xs = reinterpret_cast<float *>(ws + p.off_xs);
+  double *f = reinterpret_cast<double *>(ws + p.off_f);
+  float *G = p.gram ? reinterpret_cast<float *>(ws + p.off_gram) : nullptr;
+  Ctl *ctl = reinterpret_cast<Ctl *>(ws + p.off_ctl);
+  Prob *dprob = reinterpret_cast<Prob *>(ws + p.off_prob);
+  int32_t *wgp = reinterpret_cast<int32_t *>(ws + p.off_wgp);
+  u64 *slots = reinterpret_cast<u64 *>(ws + p.off_slots);
+  double *fin = reinterpret_cast<double *>(ws + p.off_fin);
+  int32_t *err = reinterpret_cast<int32_t *>(ws + p.off_err);
+
+  std::vector<Prob> hp(p.P);
+  std::vector<int32_t> hwgp;
+  int64_t pack = 0, max_n = 0;
+  int32_t per_thread = 1, wg = 0, q = 0;
+  for (int32_t a = 0; a < k; ++a)
+    for (int32_t bb = a + 1; bb < k; ++bb, ++q) {
+      Prob &P = hp[q];
+      P = Prob{};
+      P.n = cnt[a] + cnt[bb];
+      P.off0 = start[a];
+      P.len0 = cnt[a];
+      P.off1 = start[bb];
+      P.y = nullptr;
+      P.alpha = alpha + pack;
+      P.f = f + pack;
+      P.ctl = ctl + q;
+      Shape sh;
+      if (!choose_shape(P.n, p.gram, r.workgroups, &sh) || sh.nwg > OVO_MAX_WG_PER_PAIR)
+        return fail(SVM_ENOMEM, "pair (%d,%d) too large to place", a, bb);
+      P.slots = slots + (size_t)q * 2 * OVO_MAX_WG_PER_PAIR * SLOT_WORDS;
+      P.wg0 = wg;
+      P.nwg = sh.nwg;
+      P.per_wg = sh.per_wg;
+      per_thread = std::max(per_thread, sh.per_thread);
+      for (int32_t w = 0; w < sh.nwg; ++w) hwgp.push_back(q);
+      wg += sh.nwg;
+      pack += P.n;
+      max_n = std::max(max_n, P.n);
+    }
+  HIPCHK(hipMemcpyAsync(dperm, perm.data(), 4 * n, hipMemcpyHostToDevice, stream));
+  HIPCHK(hipMemcpyAsync(dprob, hp.data(), sizeof(Prob) * hp.size(), hipMemcpyHostToDevice, stream));
+  HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
+  HIPCHK(hipMemsetAsync(err, 0, 16, stream));
+  HIPCHK(launch_gather_rows(X, d, dperm, n, Xs, stream));
+
+  Timer tg, ts, tf;
+  HIPCHK(tg.init());
+  HIPCHK(ts.init());
+  HIPCHK(tf.init());
+  HIPCHK(hipEventRecord(tg.a, stream));
+  if (p.gram) HIPCHK(launch_gram(Xs, n, d, (float)gamma, G, p.ld, stream));
+  HIPCHK(hipEventRecord(tg.b, stream));
+  HIPCHK(hipEventRecord(ts.a, stream));
+  HIPCHK(launch_solver_init(dprob, p.P, max_n, stream));
+  SolveParams sp{};
+  sp.probs = dprob;
+  sp.wg_prob = wgp;
+  sp.C = C;
+  sp.tol = tol;
+  sp.gamma = gamma;
+  sp.max_iter = r.max_iter;
+  sp.steps = r.check_every;
+  sp.gram = G;
+  sp.ld = p.ld;
+  sp.X = Xs;
+  sp.d = d;
+  sp.spin_limit = spin_ticks();
+  sp.error = err;
+  int32_t launches = 0;
+  std::vector<Ctl> hc;
+  double t_kernel = 0.0;
+  svm_status s1 = run_solver(sp, p.P, wg, per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel);
+  if (s1 != SVM_OK) return s1;
+  HIPCHK(hipEventRecord(ts.b, stream));
+  HIPCHK(hipEventRecord(tf.a, stream));
+  HIPCHK(launch_finalize(dprob, p.P, C, fin, stream));
+  std::vector<double> hfin(4 * (size_t)p.P);
+  HIPCHK(hipMemcpyAsync(hfin.data(), fin, 8 * hfin.size(), hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipEventRecord(tf.b, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  bool maxed = false;
+  const double t_total = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
+  for (int32_t q2 = 0; q2 < p.P; ++q2) {
+    b[q2] = 0.5 * (hc[q2].b_up + hc[q2].b_low);
+    maxed = maxed || hc[q2].status == ST_MAXITER;
+    if (st) {
+      svm_stats &S = st[q2];
+      S.iterations = hc[q2].t;
+      S.n_sv = (int64_t)hfin[4 * q2 + 2];
+      S.n_bound_sv = (int64_t)hfin[4 * q2 + 3];
+      S.b_up = hc[q2].b_up;
+      S.b_low = hc[q2].b_low;
+      S.dual_obj = 0.5 * hfin[4 * q2] - 0.5 * hfin[4 * q2 + 1];
+      S.gram_used = p.gram ? 1 : 0;
+      S.launches = launches;
+      S.t_gram = p.gram ? tg.seconds() : 0.0;
+      S.t_solve = ts.seconds();
+      S.t_finalize = tf.seconds();
+      S.t_total = t_total;
+      S.t_kernel = t_kernel;
+    }
+  }
+  return maxed ? SVM_NOT_CONVERGED : SVM_OK;
+}
+
+int64_t svm_predict_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, int64_t m) {
+  if (n < 2 || d < 1 || k < 2 || k > MAX_CLASSES || m < 0) return -1;
+  return round_up(4 * n, ALIGN);
+}
+
+svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k,
+                           const double *alpha, const double *b, double gamma, const float *X_test, int64_t m,
+                           double *dec, int32_t *pred, void *workspace, int64_t workspace_bytes,
+                           const svm_options *o) {
+  g_err.clear();
+  if (n < 2 || d < 1 || m < 0) return fail(SVM_EINVAL, "need n >= 2, d >= 1, m >= 0");
+  if (k < 2 || k > MAX_CLASSES) return fail(SVM_EINVAL, "k=%d must be in [2, %d]", k, MAX_CLASSES);
+  if (!X || !label || !alpha || !b || (m > 0 && (!X_test || !dec || !pred))) return fail(SVM_EINVAL, "NULL pointer");
+  if (!finite_pos(gamma)) return fail(SVM_EINVAL, "gamma must be finite and > 0");
+  if ((int64_t)8 * 4 * d > LDS_BYTES) return fail(SVM_EINVAL, "d too large for the staged test tile");
+  Opts r;
+  if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options");
+  const int64_t need = svm_predict_ovo_workspace_bytes(n, d, k, m);
+  if (!workspace || workspace_bytes < need) return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed", (long long)need);
+  const int32_t P = k * (k - 1) / 2;
+  for (int32_t q = 0; q < P; ++q)
+    if (!std::isfinite(b[q])) return fail(SVM_EINVAL, "b[%d] is not finite", q);
+  std::vector<int32_t> perm;
+  std::vector<int64_t> start, cnt;
+  svm_status s0 = class_sort(label, n, k, r.stream, perm, start, cnt);
+  if (s0 != SVM_OK) return s0;
+  if (m == 0) return SVM_OK;
+  int32_t *dperm = static_cast<int32_t *>(workspace);
+  HIPCHK(hipMemcpyAsync(dperm, perm.data(), 4 * n, hipMemcpyHostToDevice, r.stream));
+  int64_t pack = 0;
+  int32_t q = 0;
+  for (int32_t a = 0; a < k; ++a)
+    for (int32_t bb = a + 1; bb < k; ++bb, ++q) {
+      const int64_t np = cnt[a] + cnt[bb];
+      HIPCHK(launch_predict_map(X, d, start[a], cnt[a], start[bb], nullptr, dperm, alpha + pack, np, gamma, X_test, m,
+                                b[q], dec + q, P, r.stream));
+      pack += np;
+    }
+  HIPCHK(launch_ovo_vote(dec, m, k, pred, r.stream));
+  HIPCHK(hipStreamSynchronize(r.stream));
+  return SVM_OK;
+}
+
+svm_status svm_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, const int64_t *rows, int64_t r,
+                           float *out, const svm_options *o) {
+  g_err.clear();
+  if (!X || !rows || !out) return fail(SVM_EINVAL, "NULL pointer argument");
+  if (n < 1 || d < 1 || r < 1) return fail(SVM_EINVAL, "need n, d, r >= 1");
+  if (!finite_pos(gamma)) return fail(SVM_EINVAL, "gamma must be finite and > 0");
+  if (d > (INT64_MAX / 8) / n || r > INT64_MAX / 8 / n) return fail(SVM_ENOMEM, "sizes overflow");
+  if (2 * 4 * d > LDS_BYTES) return fail(SVM_EINVAL, "d too large for the staged rows");
+  Opts op;
+  if (!resolve(o, n, &op)) return fail(SVM_EINVAL, "bad options");
+  std::vector<int64_t> h(r);
+  HIPCHK(hipMemcpyAsync(h.data(), rows, 8 * r, hipMemcpyDeviceToHost, op.stream));
+  HIPCHK(hipStreamSynchronize(op.stream));
+  for (int64_t q = 0; q < r; ++q)
+    if (h[q] < 0 || h[q] >= n) return fail(SVM_EINVAL, "rows[%lld] = %lld out of range", (long long)q, (long long)h[q]);
+  HIPCHK(launch_kernel_rows(X, n, d, gamma, rows, r, out, op.stream));
+  HIPCHK(hipStreamSynchronize(op.stream));
+  return SVM_OK;
+}
+
+svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G, int64_t ld, const svm_options *o) {
+  g_err.clear();
+  if (!X || !G) return fail(SVM_EINVAL, "NULL pointer argument");
+  if (n < 1 || d < 1 || ld < n) return fail(SVM_EINVAL, "need n, d >= 1 and ld >= n");
+  if (!finite_pos(gamma)) return fail(SVM_EINVAL, "gamma must be finite and > 0");
+  if (d > (INT64_MAX / 8) / n || ld > (INT64_MAX / 8) / n) return fail(SVM_ENOMEM, "sizes overflow");
+  Opts op;
+  if (!resolve(o, n, &op)) return fail(SVM_EINVAL, "bad options");
+  HIPCHK(launch_gram(X, n, d, (float)gamma, G, ld, op.stream));
+  HIPCHK(hipStreamSynchronize(op.stream));
+  return SVM_OK;
+}
+
+}  // extern "C"

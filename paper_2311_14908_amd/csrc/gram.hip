@@ -1,0 +1,206 @@
+// gram.hip -- RBF Gram precompute on MFMA, kernel rows from X, and row gathers (gfx950).
+//
+// G_ij = exp(-gamma * max(0, |x_i|^2 + |x_j|^2 - 2 x_i.x_j)): the dot products form the
+// contraction X X^T, run on v_mfma_f32_16x16x4f32 with fp32 inputs and accumulation; the
+// row norms are accumulated from the same LDS tiles and the RBF map is the epilogue.  The
+// kernel is the Gaussian RBF the paper names (Section III.C).
+#include "common.hpp"
+#include "rbf_rows.hpp"
+
+#include <math.h>
+
+namespace svmx {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int GT = 128;       // tile edge (rows and columns)
+constexpr int GKC = 16;       // k per LDS stage
+constexpr int GPAD = GT + 16; // LDS row pitch in floats (keeps the MFMA operand reads conflict-free)
+constexpr int GBS = 256;      // 4 waves, 2x2 over the tile, 64x64 each
+
+// Load a 128 x 16 slab of X (rows r0.., columns k0..) into LDS transposed to [k][row], and
+// add the slab's squares into this thread's norm partials.  Thread t covers rows t/4 and
+// 64 + t/4, columns k0 + 4*(t%4) .. +3, so the partials of a row always meet in the same
+// order and a sample's norm does not depend on which tile role loaded it.
+template <bool VEC4>
+__device__ __forceinline__ void load_slab(const float *__restrict__ X, int64_t n, int64_t d, int64_t r0, int64_t k0,
+                                          float (*S)[GPAD], float nacc[2]) {
+  const int t = threadIdx.x;
+  const int kq = (t & 3) * 4;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int row = h * 64 + (t >> 2);
+    const int64_t gr = r0 + row;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (gr < n) {
+      const float *src = X + gr * d + k0 + kq;
+      if (VEC4 && k0 + kq + 3 < d) {
+        const float4 q = *reinterpret_cast<const float4 *>(src);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (k0 + kq + e < d) v[e] = src[e];
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      S[kq + e][row] = v[e];
+      nacc[h] += v[e] * v[e];
+    }
+  }
+}
+
+template <bool VEC4>
+__global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X, int64_t n, int64_t d, float gamma,
+                                                     float *__restrict__ G, int64_t ld) {
+  __shared__ float As[GKC][GPAD];
+  __shared__ float Bs[GKC][GPAD];
+  __shared__ float nA[GT], nB[GT];
+  const int64_t i0 = (int64_t)blockIdx.y * GT, j0 = (int64_t)blockIdx.x * GT;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  v4f acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) acc[a][b] = (v4f){0.f, 0.f, 0.f, 0.f};
+  float na[2] = {0.f, 0.f}, nb[2] = {0.f, 0.f};
+
+  for (int64_t k0 = 0; k0 < d; k0 += GKC) {
+    load_slab<VEC4>(X, n, d, i0, k0, As, na);
+    load_slab<VEC4>(X, n, d, j0, k0, Bs, nb);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < GKC; kk += 4) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) av[m] = As[kk + (lane >> 4)][wm * 64 + m * 16 + (lane & 15)];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) bv[m] = Bs[kk + (lane >> 4)][wn * 64 + m * 16 + (lane & 15)];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  // norms: combine the four partials of each row (lanes 4r..4r+3 of a wave)
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    na[h] += __shfl_xor(na[h], 1);
+    na[h] += __shfl_xor(na[h], 2);
+    nb[h] += __shfl_xor(nb[h], 1);
+    nb[h] += __shfl_xor(nb[h], 2);
+  }
+  if ((threadIdx.x & 3) == 0) {
+    nA[threadIdx.x >> 2] = na[0];
+    nA[64 + (threadIdx.x >> 2)] = na[1];
+    nB[threadIdx.x >> 2] = nb[0];
+    nB[64 + (threadIdx.x >> 2)] = nb[1];
+  }
+  __syncthreads();
+  // epilogue: lane holds D[4*(lane/16)+e][lane%16] of each 16x16 block
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int lc = wn * 64 + b * 16 + (lane & 15);
+      const int64_t gc = j0 + lc;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int lr = wm * 64 + a * 16 + 4 * (lane >> 4) + e;
+        const int64_t gr = i0 + lr;
+        if (gr < n && gc < n) {
+          float t = nA[lr] + nB[lc] - 2.0f * acc[a][b][e];
+          t = t > 0.f ? t : 0.f;
+          G[gr * ld + gc] = (gr == gc) ? 1.0f : expf(-gamma * t);
+        }
+      }
+    }
+  }
+}
+
+hipError_t launch_gram(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, hipStream_t s) {
+  const int64_t tiles = (n + GT - 1) / GT;
+  if (tiles > 65535) return hipErrorInvalidValue;
+  dim3 grid((unsigned)tiles, (unsigned)tiles);
+  const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);
+  if (vec4)
+    hipLaunchKernelGGL(gram_rbf_mfma<true>, grid, dim3(GBS), 0, s, X, n, d, gamma, G, ld);
+  else
+    hipLaunchKernelGGL(gram_rbf_mfma<false>, grid, dim3(GBS), 0, s, X, n, d, gamma, G, ld);
+  return hipGetLastError();
+}
+
+// out[q][j] = K(x_rows[q], x_j), evaluated with the row path's routine (pairs of rows).
+template <bool VEC4>
+__global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X, int64_t n, int64_t d, double gamma,
+                                                      const int64_t *__restrict__ rows, int64_t r,
+                                                      float *__restrict__ out) {
+  extern __shared__ float4 sx4[];  // two staged rows
+  float *sx = reinterpret_cast<float *>(sx4);
+  const int64_t q0 = 2 * (int64_t)blockIdx.y;
+  const int64_t q1 = q0 + 1 < r ? q0 + 1 : q0;
+  const int64_t ru = rows[q0], rl = rows[q1];
+  for (int64_t k = threadIdx.x; k < d; k += 256) {
+    sx[k] = X[ru * d + k];
+    sx[d + k] = X[rl * d + k];
+  }
+  __syncthreads();
+  const int gs = group_size_for(d, VEC4);
+  const int lig = threadIdx.x & (gs - 1);
+  const int ngroups = 256 / gs;
+  const int grp = threadIdx.x / gs;
+  for (int64_t j = (int64_t)blockIdx.x * ngroups + grp; j < n; j += (int64_t)gridDim.x * ngroups) {
+    double du, dl;
+    dist2_group<VEC4>(X + j * d, sx, sx + d, d, lig, gs, du, dl);
+    if (lig == 0) {
+      out[q0 * n + j] = (float)exp(-gamma * du);
+      if (q1 != q0) out[q1 * n + j] = (float)exp(-gamma * dl);
+    }
+  }
+}
+
+hipError_t launch_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, const int64_t *rows, int64_t r,
+                              float *out, hipStream_t s) {
+  const int64_t pairs = (r + 1) / 2;
+  if (pairs > 65535) return hipErrorInvalidValue;
+  int64_t bx = (n + 63) / 64;
+  if (bx > 1024) bx = 1024;
+  const size_t shmem = 2 * (size_t)d * sizeof(float);
+  const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);
+  const void *fn = vec4 ? reinterpret_cast<const void *>(&kernel_rows_k<true>)
+                        : reinterpret_cast<const void *>(&kernel_rows_k<false>);
+  if (shmem > 48 * 1024) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
+    if (e != hipSuccess) return e;
+  }
+  if (vec4)
+    hipLaunchKernelGGL(kernel_rows_k<true>, dim3((unsigned)bx, (unsigned)pairs), dim3(256), shmem, s, X, n, d, gamma,
+                       rows, r, out);
+  else
+    hipLaunchKernelGGL(kernel_rows_k<false>, dim3((unsigned)bx, (unsigned)pairs), dim3(256), shmem, s, X, n, d,
+                       gamma, rows, r, out);
+  return hipGetLastError();
+}
+
+// Xs[r] = X[perm[r]] (row gather, e.g. into class-sorted order).
+__global__ void gather_rows_k(const float *__restrict__ X, int64_t d, const int32_t *__restrict__ perm, int64_t n,
+                              float *__restrict__ Xs) {
+  const int64_t total = n * d;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = e / d, k = e - r * d;
+    Xs[e] = X[(int64_t)perm[r] * d + k];
+  }
+}
+
+hipError_t launch_gather_rows(const float *X, int64_t d, const int32_t *perm, int64_t n, float *Xs, hipStream_t s) {
+  int64_t blocks = (n * d + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(gather_rows_k, dim3((unsigned)blocks), dim3(256), 0, s, X, d, perm, n, Xs);
+  return hipGetLastError();
+}
+
+}  // namespace svmx

@@ -1,0 +1,486 @@
+// smo.hip -- persistent SMO solver for gfx950 (paper, Section III.B: SMO with two Lagrange
+// multipliers per step; the data-parallel work runs one thread per training sample).
+//
+// One cooperative launch advances every running problem by up to `steps` SMO steps.  A
+// problem is served by nwg workgroups; workgroup r owns local samples [r*per_wg,
+// (r+1)*per_wg) and keeps their f, alpha and label in registers for the whole launch.
+// Each step:
+//   1. every workgroup selects its own candidates  u_r = argmin_{I_up} f,  l_r = argmax_{I_low} f
+//      (ties to the smaller index) with wave shuffles and LDS;
+//   2. the nwg partial results are exchanged through global memory as self-stamped 64-bit
+//      words (payload | step stamp), so no fence or cache flush is needed: a reader simply
+//      waits until every word it needs carries the current stamp;
+//   3. every workgroup reduces the same nwg records to the same pair (u, l), tests the stop
+//      rule, and solves the 2x2 sub-problem redundantly (identical fp64 arithmetic);
+//   4. every workgroup fetches K(u, j) and K(l, j) for its own samples -- from the Gram or
+//      computed from X -- and applies f_j += da_u y_u K_uj + da_l y_l K_lj.
+// Every wait is bounded by a wall-clock limit; on expiry the kernel records an error and
+// all waits end, so a launch always drains.
+#include "common.hpp"
+#include "rbf_rows.hpp"
+
+#include <math.h>
+
+namespace svmx {
+
+constexpr int BS = 256;
+constexpr int NWAVE = BS / 64;
+constexpr int IBIG = 0x7fffffff;
+constexpr int MAX_PER = 16;
+
+int solver_block_size() { return BS; }
+int max_per_thread() { return MAX_PER; }
+
+__device__ __forceinline__ bool lt_min(double v2, int i2, double v, int i) { return v2 < v || (v2 == v && i2 < i); }
+__device__ __forceinline__ bool gt_max(double v2, int i2, double v, int i) { return v2 > v || (v2 == v && i2 < i); }
+
+struct Sel {
+  double vu, au;  // min f over I_up and the alpha there
+  double vl, al;  // max f over I_low and the alpha there
+  int iu, il;
+};
+
+__device__ __forceinline__ void sel_init(Sel &s) {
+  s.vu = INFINITY; s.au = 0.0; s.iu = IBIG;
+  s.vl = -INFINITY; s.al = 0.0; s.il = IBIG;
+}
+
+__device__ __forceinline__ void sel_merge(Sel &s, double vu, int iu, double au, double vl, int il, double al) {
+  if (lt_min(vu, iu, s.vu, s.iu)) { s.vu = vu; s.iu = iu; s.au = au; }
+  if (gt_max(vl, il, s.vl, s.il)) { s.vl = vl; s.il = il; s.al = al; }
+}
+
+__device__ __forceinline__ void sel_wave(Sel &s) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    double vu = __shfl_xor(s.vu, o), au = __shfl_xor(s.au, o);
+    int iu = __shfl_xor(s.iu, o);
+    double vl = __shfl_xor(s.vl, o), al = __shfl_xor(s.al, o);
+    int il = __shfl_xor(s.il, o);
+    sel_merge(s, vu, iu, au, vl, il, al);
+  }
+}
+
+struct SelShared {
+  double vu[NWAVE], au[NWAVE], vl[NWAVE], al[NWAVE];
+  int iu[NWAVE], il[NWAVE];
+  Sel out;
+};
+
+// Block-wide reduction; the result is returned to every thread.
+__device__ __forceinline__ Sel sel_block(Sel s, SelShared &sh) {
+  sel_wave(s);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sh.vu[w] = s.vu; sh.au[w] = s.au; sh.iu[w] = s.iu;
+    sh.vl[w] = s.vl; sh.al[w] = s.al; sh.il[w] = s.il;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < NWAVE; ++q) sel_merge(s, sh.vu[q], sh.iu[q], sh.au[q], sh.vl[q], sh.il[q], sh.al[q]);
+    sh.out = s;
+  }
+  __syncthreads();
+  Sel r = sh.out;
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ void st_word(u64 *p, u64 v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ u64 ld_word(const u64 *p) {
+  return __hip_atomic_load(const_cast<u64 *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ u64 stamp_word(unsigned stamp, unsigned payload) { return ((u64)stamp << 32) | payload; }
+__device__ __forceinline__ double join_double(u64 hi, u64 lo) {
+  return __longlong_as_double((long long)(((hi & 0xffffffffull) << 32) | (lo & 0xffffffffull)));
+}
+
+// Exchange of the workgroup selections of one problem (see file comment, item 2).
+// Record layout (10 words): vu hi, vu lo, iu, au hi, au lo, vl hi, vl lo, il, al hi, al lo.
+__device__ Sel exchange(const Prob &P, int rank, unsigned stamp, Sel mine, SelShared &sh, uint64_t spin_limit,
+                        int32_t *err, int *abort_flag) {
+  u64 *base = P.slots + (size_t)(stamp & 1u) * P.nwg * SLOT_WORDS;
+  if (threadIdx.x < 10) {
+    const u64 bvu = (u64)__double_as_longlong(mine.vu), bau = (u64)__double_as_longlong(mine.au);
+    const u64 bvl = (u64)__double_as_longlong(mine.vl), bal = (u64)__double_as_longlong(mine.al);
+    unsigned pl;
+    switch (threadIdx.x) {
+      case 0: pl = (unsigned)(bvu >> 32); break;
+      case 1: pl = (unsigned)bvu; break;
+      case 2: pl = (unsigned)mine.iu; break;
+      case 3: pl = (unsigned)(bau >> 32); break;
+      case 4: pl = (unsigned)bau; break;
+      case 5: pl = (unsigned)(bvl >> 32); break;
+      case 6: pl = (unsigned)bvl; break;
+      case 7: pl = (unsigned)mine.il; break;
+      case 8: pl = (unsigned)(bal >> 32); break;
+      default: pl = (unsigned)bal; break;
+    }
+    st_word(base + (size_t)rank * SLOT_WORDS + threadIdx.x, stamp_word(stamp, pl));
+  }
+  Sel s;
+  sel_init(s);
+  for (int q = threadIdx.x; q < P.nwg; q += BS) {
+    const u64 *rec = base + (size_t)q * SLOT_WORDS;
+    u64 w[10];
+    const uint64_t t0 = wall_clock64();
+    for (;;) {
+      bool ok = true;
+#pragma unroll
+      for (int k = 0; k < 10; ++k) {
+        w[k] = ld_word(rec + k);
+        ok = ok && ((unsigned)(w[k] >> 32) == stamp);
+      }
+      if (ok) break;
+      if (wall_clock64() - t0 > spin_limit) {
+        __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *abort_flag = 1;
+        break;
+      }
+    }
+    sel_merge(s, join_double(w[0], w[1]), (int)(unsigned)w[2], join_double(w[3], w[4]), join_double(w[5], w[6]),
+              (int)(unsigned)w[7], join_double(w[8], w[9]));
+  }
+  return sel_block(s, sh);
+}
+
+// 2x2 sub-problem on (u, l): eta = K_uu + K_ll - 2 K_ul with K_uu = K_ll = 1 for the RBF
+// kernel, the box [L, H] on a_l, the partner clamped to [0, C], values within 1e-12 C of a
+// bound snapped onto it.  Written without contraction so the fp64 rounding is that of the
+// plain expression.
+struct PairStep {
+  double au, al;  // new multipliers of u and l
+};
+
+__device__ __forceinline__ PairStep solve_pair(double C, double bu, double bl, double au, double al, double yu,
+                                               double yl, double kul) {
+#pragma clang fp contract(off)
+  double eta = (1.0 + 1.0) - 2.0 * kul;
+  if (eta <= 0.0) eta = 1e-12;
+  const double s = yu * yl;
+  double L, H;
+  if (s < 0) {
+    L = fmax(0.0, al - au);
+    H = fmin(C, C + al - au);
+  } else {
+    L = fmax(0.0, au + al - C);
+    H = fmin(C, au + al);
+  }
+  double aln = al + yl * (bu - bl) / eta;
+  aln = aln < L ? L : (aln > H ? H : aln);
+  double aun = au + s * (al - aln);
+  aun = aun < 0.0 ? 0.0 : (aun > C ? C : aun);
+  const double snap = 1e-12 * C;
+  if (fabs(aln) <= snap) aln = 0.0;
+  if (fabs(aln - C) <= snap) aln = C;
+  if (fabs(aun) <= snap) aun = 0.0;
+  if (fabs(aun - C) <= snap) aun = C;
+  return PairStep{aun, aln};
+}
+
+__device__ __forceinline__ int64_t gmap(const Prob &P, int64_t j) { return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0); }
+__device__ __forceinline__ int label_of(const Prob &P, int64_t j) {
+  return P.y ? P.y[gmap(P, j)] : (j < P.len0 ? 1 : -1);
+}
+
+// ---------------------------------------------------------------------------------------
+template <int PER, bool GRAM, bool VEC4>
+__global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
+  extern __shared__ float4 dyn4[];  // row path: x_u[d], x_l[d], krow[2][per_wg], tags[cap]
+  float *dyn = reinterpret_cast<float *>(dyn4);
+  __shared__ SelShared sh;
+  __shared__ int s_abort;
+
+  const int32_t pid = p.wg_prob[blockIdx.x];
+  const Prob P = p.probs[pid];
+  const int rank = (int)blockIdx.x - P.wg0;
+  Ctl *ctl = P.ctl;
+  if (ctl->status != ST_RUNNING) return;
+  int64_t t = ctl->t;
+  if (threadIdx.x == 0) s_abort = 0;
+
+  const int64_t base = (int64_t)rank * P.per_wg;
+  const int64_t lim = min(base + (int64_t)P.per_wg, P.n);
+  double f[PER], a[PER];
+  int yv[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+    if (j < lim) {
+      f[k] = P.f[j];
+      a[k] = P.alpha[j];
+      yv[k] = label_of(P, j);
+    } else {
+      f[k] = 0.0;
+      a[k] = 0.0;
+      yv[k] = 0;
+    }
+  }
+
+  float *sxu = dyn, *sxl = dyn + p.d;
+  float *krow = dyn + 2 * p.d;  // [2][per_wg]
+  int *tags = reinterpret_cast<int *>(krow + 2 * (int64_t)P.per_wg);
+  const bool use_cache = !GRAM && p.cache != nullptr && p.cache_cap > 0;
+  if (use_cache) {
+    for (int s = threadIdx.x; s < p.cache_cap; s += BS) tags[s] = p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s];
+  }
+  __syncthreads();
+
+  const double C = p.C;
+  const int64_t t_end = min(t + p.steps, p.max_iter);
+  for (;;) {
+    // 1. local candidates
+    Sel s;
+    sel_init(s);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+      if (j < lim) {
+        const bool up = (yv[k] > 0 && a[k] < C) || (yv[k] < 0 && a[k] > 0.0);
+        const bool lo = (yv[k] > 0 && a[k] > 0.0) || (yv[k] < 0 && a[k] < C);
+        if (up && lt_min(f[k], (int)j, s.vu, s.iu)) { s.vu = f[k]; s.iu = (int)j; s.au = a[k]; }
+        if (lo && gt_max(f[k], (int)j, s.vl, s.il)) { s.vl = f[k]; s.il = (int)j; s.al = a[k]; }
+      }
+    }
+    s = sel_block(s, sh);
+    // 2. exchange across the problem's workgroups
+    if (P.nwg > 1) s = exchange(P, rank, (unsigned)(t + 1), s, sh, p.spin_limit, p.error, &s_abort);
+    __syncthreads();
+    const bool aborted = s_abort != 0;
+    // 3. stop rule
+    if (rank == 0 && threadIdx.x == 0 && t < P.trace_len) {
+      if (P.trace_ul) { P.trace_ul[2 * t] = s.iu; P.trace_ul[2 * t + 1] = s.il; }
+      if (P.trace_b) { P.trace_b[2 * t] = s.vu; P.trace_b[2 * t + 1] = s.vl; }
+    }
+    int status = ST_RUNNING;
+    if (aborted) status = ST_TIMEOUT;
+    else if (s.iu == IBIG || s.il == IBIG || s.vl - s.vu <= p.tol) status = ST_CONVERGED;
+    else if (t >= p.max_iter) status = ST_MAXITER;
+    if (status != ST_RUNNING || t >= t_end) {
+      if (rank == 0 && threadIdx.x == 0) {
+        ctl->t = t;
+        ctl->status = status;
+        ctl->b_up = s.vu;
+        ctl->b_low = s.vl;
+        ctl->u = s.iu;
+        ctl->l = s.il;
+      }
+      break;
+    }
+    const int64_t u = s.iu, l = s.il;
+    const int64_t gu = gmap(P, u), gl = gmap(P, l);
+    const double yu = (double)label_of(P, u), yl = (double)label_of(P, l);
+
+    // 4. kernel rows of u and l for the own samples, K_ul, 2x2 solve, f update
+    float ku[PER], kl[PER];
+    double kul;
+    if (GRAM) {
+      const float *Ru = p.gram + gu * p.ld;
+      const float *Rl = p.gram + gl * p.ld;
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+        if (j < lim) {
+          const int64_t g = gmap(P, j);
+          ku[k] = Ru[g];
+          kl[k] = Rl[g];
+        }
+      }
+      kul = (double)Ru[gl];
+    } else {
+      const int64_t d = p.d;
+      const int gs = group_size_for(d, VEC4);
+      const int lane_in_group = threadIdx.x & (gs - 1);
+      const int ngroups = BS / gs;
+      const int grp = threadIdx.x / gs;
+      const float *xu = p.X + gu * d, *xl = p.X + gl * d;
+      for (int64_t k = threadIdx.x; k < d; k += BS) {
+        sxu[k] = xu[k];
+        sxl[k] = xl[k];
+      }
+      int su = -1, sl = -1;
+      bool hit_u = false, hit_l = false;
+      if (use_cache) {
+        su = (int)(gu % p.cache_cap);
+        sl = (int)(gl % p.cache_cap);
+        hit_u = tags[su] == (int)gu;
+        hit_l = tags[sl] == (int)gl;
+      }
+      __syncthreads();
+      // K_ul from the staged rows (group 0)
+      __shared__ double s_kul;
+      if (grp == 0) {
+        double du, dl;
+        dist2_group<VEC4>(sxl, sxu, sxu, d, lane_in_group, gs, du, dl);
+        if (lane_in_group == 0) s_kul = (double)(float)exp(-p.gamma * du);
+      }
+      const bool need = !(hit_u && hit_l);
+      if (need) {
+        const int64_t cnt = lim - base;
+        for (int64_t q = grp; q < cnt; q += ngroups) {
+          double du, dl;
+          dist2_group<VEC4>(p.X + gmap(P, base + q) * d, sxu, sxl, d, lane_in_group, gs, du, dl);
+          if (lane_in_group == 0) {
+            krow[q] = (float)exp(-p.gamma * du);
+            krow[P.per_wg + q] = (float)exp(-p.gamma * dl);
+          }
+        }
+      }
+      __syncthreads();
+      kul = s_kul;
+      const bool store_u = use_cache && !hit_u;
+      const bool store_l = use_cache && !hit_l && !(sl == su && store_u);
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+        if (j < lim) {
+          const int64_t q = j - base;
+          ku[k] = hit_u ? p.cache[(size_t)su * p.ld + j] : krow[q];
+          kl[k] = hit_l ? p.cache[(size_t)sl * p.ld + j] : krow[P.per_wg + q];
+          if (store_u) p.cache[(size_t)su * p.ld + j] = ku[k];
+          if (store_l) p.cache[(size_t)sl * p.ld + j] = kl[k];
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        if (store_u) tags[su] = (int)gu;
+        if (store_l) tags[sl] = (int)gl;
+      }
+    }
+    const PairStep ps = solve_pair(C, s.vu, s.vl, s.au, s.al, yu, yl, kul);
+    const double au_new = ps.au, al_new = ps.al;
+    const double cu = (au_new - s.au) * yu, cl = (al_new - s.al) * yl;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+      if (j < lim) {
+        f[k] += cu * (double)ku[k] + cl * (double)kl[k];
+        if (j == u) a[k] = au_new;
+        if (j == l) a[k] = al_new;
+      }
+    }
+    ++t;
+  }
+
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+    if (j < lim) {
+      P.f[j] = f[k];
+      P.alpha[j] = a[k];
+    }
+  }
+  if (use_cache) {
+    __syncthreads();
+    for (int s = threadIdx.x; s < p.cache_cap; s += BS) p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s] = tags[s];
+  }
+}
+
+// a = 0, f = -y for every problem; exchange words and control blocks cleared.
+__global__ void smo_init(const Prob *probs, int32_t nprob) {
+  const int32_t pid = blockIdx.y;
+  const Prob P = probs[pid];
+  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < P.n; j += (int64_t)gridDim.x * blockDim.x) {
+    P.alpha[j] = 0.0;
+    P.f[j] = -(double)label_of(P, j);
+  }
+  const int64_t nw = 2 * (int64_t)P.nwg * SLOT_WORDS;
+  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nw; q += (int64_t)gridDim.x * blockDim.x)
+    P.slots[q] = 0ull;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    P.ctl->t = 0;
+    P.ctl->status = ST_RUNNING;
+    P.ctl->b_up = 0.0;
+    P.ctl->b_low = 0.0;
+    P.ctl->u = -1;
+    P.ctl->l = -1;
+  }
+}
+
+// Per problem: out[4p+0] = sum a, out[4p+1] = sum a y f, out[4p+2] = #(a>0), out[4p+3] = #(a>=C).
+__global__ void __launch_bounds__(BS) smo_finalize(const Prob *probs, double C, double *out) {
+  const Prob P = probs[blockIdx.x];
+  double sa = 0.0, saf = 0.0, nsv = 0.0, nb = 0.0;
+  for (int64_t j = threadIdx.x; j < P.n; j += BS) {
+    const double aj = P.alpha[j];
+    sa += aj;
+    saf += aj * (double)label_of(P, j) * P.f[j];
+    nsv += aj > 0.0 ? 1.0 : 0.0;
+    nb += aj >= C ? 1.0 : 0.0;
+  }
+  __shared__ double red[4][NWAVE];
+  for (int o = 32; o > 0; o >>= 1) {
+    sa += __shfl_xor(sa, o);
+    saf += __shfl_xor(saf, o);
+    nsv += __shfl_xor(nsv, o);
+    nb += __shfl_xor(nb, o);
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { red[0][w] = sa; red[1][w] = saf; red[2][w] = nsv; red[3][w] = nb; }
+  __syncthreads();
+  if (threadIdx.x < 4) {
+    double v = 0.0;
+    for (int q = 0; q < NWAVE; ++q) v += red[threadIdx.x][q];
+    out[4 * (int64_t)blockIdx.x + threadIdx.x] = v;
+  }
+}
+
+hipError_t launch_solver_init(const Prob *probs, int32_t nprob, int64_t max_n, hipStream_t s) {
+  int64_t bx = (max_n + 255) / 256;
+  if (bx < 1) bx = 1;
+  if (bx > 4096) bx = 4096;
+  hipLaunchKernelGGL(smo_init, dim3((unsigned)bx, (unsigned)nprob), dim3(256), 0, s, probs, nprob);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const Prob *probs, int32_t nprob, double C, double *out, hipStream_t s) {
+  hipLaunchKernelGGL(smo_finalize, dim3((unsigned)nprob), dim3(BS), 0, s, probs, C, out);
+  return hipGetLastError();
+}
+
+template <int PER, bool GRAM, bool VEC4>
+static hipError_t launch_one(const SolveParams &p, int32_t total_wg, size_t shmem, hipStream_t s, int32_t *maxres) {
+  const void *fn = reinterpret_cast<const void *>(&smo_solve<PER, GRAM, VEC4>);
+  if (shmem > 48 * 1024) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
+    if (e != hipSuccess) return e;
+  }
+  int dev = 0, cus = 0, per_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, BS, shmem);
+  if (e != hipSuccess) return e;
+  if (maxres) *maxres = per_cu * cus;
+  if ((int64_t)total_wg > (int64_t)per_cu * cus) return hipErrorCooperativeLaunchTooLarge;
+  SolveParams pp = p;
+  void *args[] = {&pp};
+  return hipLaunchCooperativeKernel(fn, dim3((unsigned)total_wg), dim3(BS), args, (unsigned)shmem, s);
+}
+
+template <bool GRAM, bool VEC4>
+static hipError_t launch_per(const SolveParams &p, int32_t total_wg, int32_t per, size_t shmem, hipStream_t s,
+                             int32_t *maxres) {
+  switch (per) {
+    case 1: return launch_one<1, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
+    case 2: return launch_one<2, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
+    case 4: return launch_one<4, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
+    case 8: return launch_one<8, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
+    case 16: return launch_one<16, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
+                         int32_t *max_coresident) {
+  if (gram) return launch_per<true, false>(p, total_wg, per_thread, 0, s, max_coresident);
+  // row path: x_u, x_l, two row slices of per_wg floats, tags
+  const size_t per_wg = (size_t)BS * per_thread;
+  const size_t shmem = (2 * (size_t)p.d + 2 * per_wg) * sizeof(float) + (size_t)p.cache_cap * sizeof(int) + 16;
+  const bool vec4 = (p.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(p.X) & 15) == 0);
+  if (vec4) return launch_per<false, true>(p, total_wg, per_thread, shmem, s, max_coresident);
+  return launch_per<false, false>(p, total_wg, per_thread, shmem, s, max_coresident);
+}
+
+}  // namespace svmx

@@ -1,0 +1,131 @@
+"""Host-side checks of libsvmx.so (no GPU needed): exports, defaults, workspace planning and
+argument validation, which all run before any device access."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2311_14908_amd import svmx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "svmx.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(svm_[a-z_]+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(svmx.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = svmx.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    # and as dynamic symbols of the shared object
+    out = os.popen(f"nm -D --defined-only {svmx.lib_path()}").read()
+    for name in declared_functions():
+        assert re.search(rf"\bT {name}$", out, flags=re.M), name
+
+
+def test_struct_layouts_match_header():
+    lib = svmx.load()
+    o = svmx.svm_options()
+    lib.svm_default_options(C.byref(o))
+    assert o.struct_size == C.sizeof(svmx.svm_options) == 80
+    assert o.check_every == 65536 and o.gram == svmx.GRAM_AUTO
+    assert C.sizeof(svmx.svm_stats) == 96
+
+
+def _opts(**kw):
+    lib = svmx.load()
+    o = svmx.svm_options()
+    lib.svm_default_options(C.byref(o))
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def test_workspace_sizes():
+    lib = svmx.load()
+    ws = lambda n, d, **kw: lib.svm_train_workspace_bytes(n, d, C.byref(_opts(**kw)))
+    # full Gram of the 100k x 32 workload: 100000 * ld(100032) * 4 bytes, plus small state
+    w3 = ws(100_000, 32)
+    assert 4 * 100_000 * 100_032 <= w3 < 4 * 100_000 * 100_032 + (8 << 20)
+    # row path: no Gram
+    assert ws(100_000, 32, gram=svmx.GRAM_OFF) < (16 << 20)
+    # a Gram budget below the Gram size selects the row path under AUTO
+    assert ws(20_000, 784, gram_budget_bytes=1 << 20) < (8 << 20)
+    assert ws(20_000, 784, gram=svmx.GRAM_ON, gram_budget_bytes=1 << 20) > 4 * 20_000 ** 2
+    # row cache adds cap * ld floats
+    base = ws(5000, 16, gram=svmx.GRAM_OFF)
+    withc = ws(5000, 16, gram=svmx.GRAM_OFF, row_cache_bytes=100 * 4 * 5056)
+    assert withc - base >= 100 * 4 * 5056
+    assert ws(1, 16) == -1 and ws(10, 0) == -1
+    assert lib.svm_train_ovo_workspace_bytes(60_000, 784, 10, C.byref(_opts())) > 4 * 60_000 ** 2
+    assert lib.svm_train_ovo_workspace_bytes(60_000, 784, 1, C.byref(_opts())) == -1
+    bad = _opts()
+    bad.struct_size = 12
+    assert lib.svm_train_workspace_bytes(100, 4, C.byref(bad)) == -1
+
+
+FAKE = C.c_void_p(0x1000)  # never dereferenced: every case below fails validation first
+
+
+@pytest.mark.parametrize("case,expect", [
+    (dict(X=None), svmx.SVM_EINVAL),
+    (dict(y=None), svmx.SVM_EINVAL),
+    (dict(n=1), svmx.SVM_EINVAL),
+    (dict(d=0), svmx.SVM_EINVAL),
+    (dict(Cv=0.0), svmx.SVM_EINVAL),
+    (dict(Cv=float("inf")), svmx.SVM_EINVAL),
+    (dict(gamma=-1.0), svmx.SVM_EINVAL),
+    (dict(tol=float("nan")), svmx.SVM_EINVAL),
+    (dict(wsb=16), svmx.SVM_EWORKSPACE),
+    (dict(ws=None), svmx.SVM_EWORKSPACE),
+    (dict(n=1 << 40, d=1 << 30), svmx.SVM_ENOMEM),
+])
+def test_train_rejects(case, expect):
+    lib = svmx.load()
+    a = dict(X=FAKE, y=FAKE, n=100, d=4, Cv=1.0, gamma=0.5, tol=1e-3, alpha=FAKE, ws=FAKE, wsb=16)
+    a.update(case)
+    b = C.c_double(0)
+    o = _opts()
+    st = lib.svm_train(a["X"], a["y"], a["n"], a["d"], a["Cv"], a["gamma"], a["tol"], a["alpha"], C.byref(b),
+                       a["ws"], a["wsb"], C.byref(o), None)
+    assert st == expect
+    assert lib.svm_last_error().decode() != ""
+
+
+def test_ovo_rejects():
+    lib = svmx.load()
+    b = np.zeros(100)
+    o = _opts()
+    bp = b.ctypes.data_as(C.c_void_p)
+    assert lib.svm_train_ovo(FAKE, FAKE, 100, 4, 1, 1.0, 0.5, 1e-3, FAKE, bp, FAKE, 1 << 30, C.byref(o), None) == -1
+    assert lib.svm_train_ovo(FAKE, FAKE, 100, 4, 65, 1.0, 0.5, 1e-3, FAKE, bp, FAKE, 1 << 30, C.byref(o), None) == -1
+    assert lib.svm_train_ovo(FAKE, FAKE, 100, 4, 3, 1.0, 0.5, 1e-3, FAKE, bp, FAKE, 8, C.byref(o), None) == -4
+    assert lib.svm_predict_ovo(FAKE, FAKE, 100, 4, 3, FAKE, None, 0.5, FAKE, 10, FAKE, FAKE, FAKE, 1 << 20,
+                               C.byref(o)) == -1
+
+
+def test_predict_and_rows_reject():
+    lib = svmx.load()
+    o = _opts()
+    assert lib.svm_predict(FAKE, FAKE, FAKE, 0.0, 0, 4, 0.5, FAKE, 10, FAKE, FAKE, 256, C.byref(o)) == -1
+    assert lib.svm_predict(FAKE, FAKE, FAKE, 0.0, 10, 4, 0.0, FAKE, 10, FAKE, FAKE, 256, C.byref(o)) == -1
+    assert lib.svm_predict(FAKE, FAKE, FAKE, float("nan"), 10, 4, 0.5, FAKE, 10, FAKE, FAKE, 256, C.byref(o)) == -1
+    assert lib.svm_kernel_rows(FAKE, 10, 4, 0.5, None, 2, FAKE, C.byref(o)) == -1
+    assert lib.svm_gram(FAKE, 10, 4, 0.5, FAKE, 9, C.byref(o)) == -1
+    assert lib.svm_gram(FAKE, 10, 4, -0.5, FAKE, 10, C.byref(o)) == -1
+
+
+def test_predict_m0_is_noop():
+    lib = svmx.load()
+    o = _opts()
+    assert lib.svm_predict(FAKE, FAKE, FAKE, 0.0, 10, 4, 0.5, None, 0, None, FAKE, 256, C.byref(o)) == 0

@@ -1,0 +1,280 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on identical seeded inputs.
+
+Gates (fp64 oracle vs fp32-kernel GPU path):
+  kernel rows     relative error <= 1e-5 where K >= 1e-30
+  f               max |f_gpu - f_oracle| <= 1e-4 after 1, 10, 100 and 1000 steps
+  working set     identical (u, l) for every step of the workload-0 solve (first 1000)
+  dual objective  relative error <= 1e-4
+  decisions       max abs error <= 1e-3; identical labels where |d_oracle| >= 1e-3
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2311_14908_amd import svmx, synth
+
+pytestmark = pytest.mark.gpu
+
+ROW_RTOL = 1e-5
+F_ATOL = 1e-4
+W_RTOL = 1e-4
+DEC_ATOL = 1e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    svmx.load()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def row_rel_err(got, ref):
+    got = np.asarray(got, np.float64)
+    mask = ref >= 1e-30
+    return float(np.max(np.abs(got[mask] - ref[mask]) / ref[mask])) if mask.any() else 0.0
+
+
+def check_decisions(d_gpu, d_ref):
+    assert np.max(np.abs(d_gpu - d_ref)) <= DEC_ATOL
+    sure = np.abs(d_ref) >= DEC_ATOL
+    assert np.array_equal(d_gpu[sure] > 0, d_ref[sure] > 0)
+
+
+# --- kernel rows and the Gram ------------------------------------------------------------
+
+@pytest.mark.parametrize("cid", [0, 1, 2, 3, 4])
+def test_kernel_rows_full_size(cid):
+    wl = synth.workload(cid)
+    X, _, _, _ = synth.generate(cid, m=1)
+    rng = np.random.default_rng(100 + cid)
+    rows = np.concatenate([[0, X.shape[0] - 1], rng.integers(0, X.shape[0], 5)])
+    got = svmx.svm_kernel_rows(dev(X), wl.gamma, rows).cpu().numpy()
+    ref = oracle.kernel_rows(X, rows, wl.gamma)
+    assert row_rel_err(got, ref) <= ROW_RTOL
+    assert np.all(got[np.arange(len(rows)), rows] == 1.0)
+
+
+@pytest.mark.parametrize("cid,n,d", [(0, 1000, 16), (2, 1300, 128), (1, 700, 784), (3, 3001, 32), (0, 333, 13),
+                                     (0, 129, 5)])
+def test_gram_small(cid, n, d):
+    wl = synth.workload(cid)
+    X, _, _, _ = synth.generate(cid, n=n, m=1, d=d)
+    G = svmx.svm_gram(dev(X), wl.gamma, ld=n + 3).cpu().numpy()[:, :n]
+    ref = oracle.kernel_rows(X, np.arange(n), wl.gamma)
+    assert row_rel_err(G, ref) <= ROW_RTOL
+    assert np.all(np.diag(G) == 1.0)
+
+
+@pytest.mark.parametrize("cid", [1, 2])
+def test_gram_sampled_full_size(cid):
+    wl = synth.workload(cid)
+    X, _, _, _ = synth.generate(cid, m=1)
+    Gd = svmx.svm_gram(dev(X), wl.gamma)
+    rows = np.random.default_rng(7).integers(0, X.shape[0], 6)
+    got = Gd[torch.from_numpy(rows).cuda()].cpu().numpy()
+    del Gd
+    torch.cuda.empty_cache()
+    ref = oracle.kernel_rows(X, rows, wl.gamma)
+    assert row_rel_err(got, ref) <= ROW_RTOL
+
+
+# --- binary training on workload 0 -------------------------------------------------------
+
+C0 = synth.workload(0)
+
+
+@pytest.fixture(scope="module")
+def c0():
+    X, y, Xt, yt = synth.generate(0)
+    ref = oracle.train(X, y, C0.C, C0.gamma, C0.tol, trace_len=5000, want_f=True)
+    return X, y, Xt, ref
+
+
+@pytest.mark.parametrize("gram,wgs", [(svmx.GRAM_ON, 0), (svmx.GRAM_ON, 3), (svmx.GRAM_ON, 8), (svmx.GRAM_OFF, 0),
+                                      (svmx.GRAM_OFF, 1)])
+def test_train_c0_trace_and_result(c0, gram, wgs):
+    X, y, Xt, ref = c0
+    out = svmx.svm_train(dev(X), dev(y), C0.C, C0.gamma, C0.tol, gram=gram, workgroups=wgs, trace_len=1001)
+    assert out.status == svmx.SVM_OK
+    st = out.stats
+    assert st["iterations"] == ref.iterations
+    steps = min(1000, ref.iterations + 1)
+    np.testing.assert_array_equal(out.trace_ul[:steps], ref.trace_ul[:steps])
+    np.testing.assert_allclose(out.trace_b[:steps], ref.trace_b[:steps], atol=F_ATOL, rtol=0)
+    assert abs(st["dual_obj"] - ref.dual_obj) <= W_RTOL * abs(ref.dual_obj)
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= C0.C) and abs(a @ y) <= 1e-9 * C0.C * len(y)
+    d_gpu = svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, C0.gamma, dev(Xt)).cpu().numpy()
+    d_ref = oracle.decision(X, y, ref.alpha, ref.b, Xt, C0.gamma)
+    check_decisions(d_gpu, d_ref)
+
+
+@pytest.mark.parametrize("steps", [1, 10, 100, 1000])
+def test_gradient_snapshots_c0(c0, steps):
+    X, y, _, _ = c0
+    r = oracle.train(X, y, C0.C, C0.gamma, C0.tol, max_iter=steps, want_f=True)
+    for gram in (svmx.GRAM_ON, svmx.GRAM_OFF):
+        f = torch.empty(X.shape[0], dtype=torch.float64, device="cuda")
+        out = svmx.svm_train(dev(X), dev(y), C0.C, C0.gamma, C0.tol, gram=gram, max_iter=steps, f_out=f)
+        expect = svmx.SVM_OK if r.status == 0 else svmx.SVM_NOT_CONVERGED
+        assert out.status == expect
+        assert np.max(np.abs(f.cpu().numpy() - r.f)) <= F_ATOL
+        np.testing.assert_allclose(out.alpha.cpu().numpy(), r.alpha, atol=1e-5, rtol=0)
+
+
+# --- edge cases --------------------------------------------------------------------------
+
+def test_two_point_rbf_gpu():
+    X = np.array([[1.0, 2.0, 0.5], [-0.5, 1.0, 2.0]], np.float32)
+    y = np.array([1, -1], np.int32)
+    for C_, a_exp in ((10.0, 1.2377002127605519), (0.5, 0.5)):
+        out = svmx.svm_train(dev(X), dev(y), C_, 0.3, 1e-9)
+        assert out.stats["iterations"] == 1
+        np.testing.assert_allclose(out.alpha.cpu().numpy(), [a_exp, a_exp], rtol=1e-6)
+        assert abs(out.b) <= 1e-7
+
+
+@pytest.mark.parametrize("n,wgs,gram", [(3, 0, 1), (255, 0, 1), (257, 2, 1), (1001, 5, 2), (4097, 0, 1), (5000, 0, 1),
+                                        (5000, 0, 2), (6001, 13, 1)])
+def test_ragged_sizes(n, wgs, gram):
+    X, y = synth.two_blobs(n, 6, seed=n)
+    if n == 3:
+        y = np.array([1, -1, 1], np.int32)
+    r = oracle.train(X, y, 1.0, 0.3, 1e-3, trace_len=100)
+    out = svmx.svm_train(dev(X), dev(y), 1.0, 0.3, 1e-3, gram=gram, workgroups=wgs, trace_len=100)
+    k = min(100, r.iterations + 1)
+    np.testing.assert_array_equal(out.trace_ul[:k], r.trace_ul[:k])
+    assert abs(out.stats["dual_obj"] - r.dual_obj) <= W_RTOL * abs(r.dual_obj)
+    d_gpu = svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, 0.3, dev(X[:500])).cpu().numpy()
+    check_decisions(d_gpu, oracle.decision(X, y, r.alpha, r.b, X[:500], 0.3))
+
+
+def test_duplicate_samples_eta_floor():
+    X, y = synth.two_blobs(200, 4, seed=1)
+    X = np.concatenate([X, X[:20]])
+    y = np.concatenate([y, -y[:20]])  # identical points with opposite labels: eta = 0
+    r = oracle.train(X, y, 1.0, 0.5, 1e-3)
+    out = svmx.svm_train(dev(X), dev(y), 1.0, 0.5, 1e-3)
+    assert abs(out.stats["dual_obj"] - r.dual_obj) <= W_RTOL * abs(r.dual_obj)
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= 1.0) and abs(a @ y) <= 1e-9 * len(y)
+
+
+def test_max_iter_not_converged_feasible():
+    X, y = synth.two_blobs(500, 5, seed=4)
+    out = svmx.svm_train(dev(X), dev(y), 1.0, 0.2, 1e-6, max_iter=7)
+    assert out.status == svmx.SVM_NOT_CONVERGED
+    assert out.stats["iterations"] == 7
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= 1.0) and abs(a @ y) <= 1e-12 * len(y)
+    r = oracle.train(X, y, 1.0, 0.2, 1e-6, max_iter=7)
+    assert abs(out.b - r.b) <= F_ATOL
+
+
+def test_results_independent_of_check_cadence():
+    X, y = synth.two_blobs(3000, 8, seed=8)
+    ref = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3)
+    for ce in (1, 7, 256):
+        out = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3, check_every=ce)
+        assert torch.equal(out.alpha, ref.alpha) and out.b == ref.b
+        assert out.stats["iterations"] == ref.stats["iterations"]
+
+
+def test_row_cache_does_not_change_results():
+    X, y = synth.two_blobs(3000, 8, seed=9)
+    ld = 3008
+    base = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3, gram=svmx.GRAM_OFF)
+    for slots in (1, 3, 64, 3000):
+        out = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3, gram=svmx.GRAM_OFF, row_cache_bytes=slots * 4 * ld)
+        assert torch.equal(out.alpha, base.alpha) and out.b == base.b
+
+
+def test_deterministic_repeat():
+    X, y = synth.two_blobs(4000, 8, seed=12)
+    a = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3)
+    b = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3)
+    assert torch.equal(a.alpha, b.alpha) and a.b == b.b
+
+
+# --- predict ----------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cid", [0, 2])
+def test_predict_matches_oracle_given_alpha(cid):
+    wl = synth.workload(cid)
+    X, y, Xt, _ = synth.generate(cid, n=1500, m=777)
+    r = oracle.train(X, y, wl.C, wl.gamma, wl.tol)
+    d_ref = oracle.decision(X, y, r.alpha, r.b, Xt, wl.gamma)
+    d_gpu = svmx.svm_predict(dev(X), dev(y), dev(r.alpha), r.b, wl.gamma, dev(Xt)).cpu().numpy()
+    assert np.max(np.abs(d_gpu - d_ref)) <= 1e-9 * max(1.0, np.max(np.abs(d_ref)))
+
+
+# --- one-vs-one ---------------------------------------------------------------------------------
+
+def kkt_ok(X, y, a, b, C_, gamma, tol, slack=1e-4):
+    """tol-KKT of (a, b) checked in fp64 from scratch (validity when trajectories may differ)."""
+    from scipy.spatial.distance import cdist
+    K = np.exp(-gamma * cdist(X.astype(np.float64), X.astype(np.float64), "sqeuclidean"))
+    f = K @ (a * y) - y
+    up = ((y > 0) & (a < C_)) | ((y < 0) & (a > 0))
+    low = ((y > 0) & (a > 0)) | ((y < 0) & (a < C_))
+    feas = np.all(a >= 0) and np.all(a <= C_) and abs(a @ y) <= 1e-9 * C_ * len(y)
+    return feas and np.all(f[up] >= b - tol / 2 - slack) and np.all(f[low] <= b + tol / 2 + slack)
+
+
+@pytest.mark.parametrize("gram", [svmx.GRAM_ON, svmx.GRAM_OFF])
+def test_ovo_pairs_equal_standalone_binary_solves(gram):
+    """Every pair of the batched one-launch solve is bit-identical to a binary solve of that pair."""
+    k = 4
+    X, lab, _, _ = synth.generate(4, n=800, m=1, d=24, classes=k)
+    out = svmx.svm_train_ovo(dev(X), dev(lab), k, 10.0, 0.05, 1e-3, gram=gram)
+    offs, sizes = svmx.ovo_offsets(lab, k)
+    for p, (a, b) in enumerate(oracle.ovo_pairs(k)):
+        idx, y = oracle.ovo_local(lab, a, b)
+        r = svmx.svm_train(dev(X[idx]), dev(y), 10.0, 0.05, 1e-3, gram=gram)
+        assert torch.equal(out.alpha[offs[p]:offs[p] + sizes[p]], r.alpha)
+        assert out.b[p] == r.b
+        assert out.stats[p]["iterations"] == r.stats["iterations"]
+
+
+@pytest.mark.parametrize("gram", [svmx.GRAM_ON, svmx.GRAM_OFF])
+def test_ovo_small(gram):
+    """Against the oracle.  The SMO step leaves f_u = f_l in exact arithmetic, so later
+    selections can tie exactly and fp32 kernel values may break such ties the other way; what
+    is unique is the optimum, so both sides solve to tol 1e-5 and W, tol-KKT validity,
+    decisions and labels are compared."""
+    k, tol = 4, 1e-5
+    X, lab, Xt, _ = synth.generate(4, n=600, m=300, d=20, classes=k)
+    models = oracle.train_ovo(X, lab, k, 10.0, 0.05, tol)
+    out = svmx.svm_train_ovo(dev(X), dev(lab), k, 10.0, 0.05, tol, gram=gram)
+    assert out.status == svmx.SVM_OK
+    offs, sizes = svmx.ovo_offsets(lab, k)
+    a = out.alpha.cpu().numpy()
+    for p, (idx, y, r) in enumerate(models):
+        assert sizes[p] == len(idx)
+        ap = a[offs[p]:offs[p] + sizes[p]]
+        assert abs(out.stats[p]["dual_obj"] - r.dual_obj) <= W_RTOL * abs(r.dual_obj)
+        assert kkt_ok(X[idx], y, ap, out.b[p], 10.0, 0.05, tol, slack=1e-5)
+    dec_ref, pred_ref = oracle.predict_ovo(X, lab, k, models, Xt, 0.05)
+    dec, pred = svmx.svm_predict_ovo(dev(X), dev(lab), k, out.alpha, out.b, 0.05, dev(Xt))
+    dec = dec.cpu().numpy()
+    assert np.max(np.abs(dec - dec_ref)) <= DEC_ATOL
+    sure = np.all(np.abs(dec_ref) >= DEC_ATOL, axis=1)
+    assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
+
+
+def test_ovo_predict_matches_oracle_given_alpha():
+    k = 5
+    X, lab, Xt, _ = synth.generate(4, n=500, m=200, d=12, classes=k)
+    models = oracle.train_ovo(X, lab, k, 1.0, 0.1, 1e-3)
+    alpha = np.concatenate([r.alpha for (_, _, r) in models])
+    b = np.array([r.b for (_, _, r) in models])
+    dec_ref, pred_ref = oracle.predict_ovo(X, lab, k, models, Xt, 0.1)
+    dec, pred = svmx.svm_predict_ovo(dev(X), dev(lab), k, dev(alpha), b, 0.1, dev(Xt))
+    assert np.max(np.abs(dec.cpu().numpy() - dec_ref)) <= 1e-9
+    sure = np.all(np.abs(dec_ref) >= 1e-9, axis=1)
+    assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
