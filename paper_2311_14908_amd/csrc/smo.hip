@@ -34,55 +34,94 @@ int max_per_thread() { return MAX_PER; }
 __device__ __forceinline__ bool lt_min(double v2, int i2, double v, int i) { return v2 < v || (v2 == v && i2 < i); }
 __device__ __forceinline__ bool gt_max(double v2, int i2, double v, int i) { return v2 > v || (v2 == v && i2 < i); }
 
+// Candidates of one selection: min f over I_up (vu at index iu) and max f over I_low (vl at
+// il), each with the multiplier and label of its sample.
 struct Sel {
-  double vu, au;  // min f over I_up and the alpha there
-  double vl, al;  // max f over I_low and the alpha there
-  int iu, il;
+  double vu, au, vl, al;
+  int iu, yu, il, yl;
 };
 
 __device__ __forceinline__ void sel_init(Sel &s) {
-  s.vu = INFINITY; s.au = 0.0; s.iu = IBIG;
-  s.vl = -INFINITY; s.al = 0.0; s.il = IBIG;
+  s.vu = INFINITY; s.au = 0.0; s.iu = IBIG; s.yu = 0;
+  s.vl = -INFINITY; s.al = 0.0; s.il = IBIG; s.yl = 0;
 }
 
-__device__ __forceinline__ void sel_merge(Sel &s, double vu, int iu, double au, double vl, int il, double al) {
-  if (lt_min(vu, iu, s.vu, s.iu)) { s.vu = vu; s.iu = iu; s.au = au; }
-  if (gt_max(vl, il, s.vl, s.il)) { s.vl = vl; s.il = il; s.al = al; }
+__device__ __forceinline__ void sel_merge(Sel &s, const Sel &o) {
+  if (lt_min(o.vu, o.iu, s.vu, s.iu)) { s.vu = o.vu; s.iu = o.iu; s.au = o.au; s.yu = o.yu; }
+  if (gt_max(o.vl, o.il, s.vl, s.il)) { s.vl = o.vl; s.il = o.il; s.al = o.al; s.yl = o.yl; }
 }
 
-__device__ __forceinline__ void sel_wave(Sel &s) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    double vu = __shfl_xor(s.vu, o), au = __shfl_xor(s.au, o);
-    int iu = __shfl_xor(s.iu, o);
-    double vl = __shfl_xor(s.vl, o), al = __shfl_xor(s.al, o);
-    int il = __shfl_xor(s.il, o);
-    sel_merge(s, vu, iu, au, vl, il, al);
-  }
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+  const long long b = __double_as_longlong(v);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(b >> 32), lane);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)b, lane);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-struct SelShared {
-  double vu[NWAVE], au[NWAVE], vl[NWAVE], al[NWAVE];
-  int iu[NWAVE], il[NWAVE];
-  Sel out;
+// One DPP round of the (value, index) reduction of both sides.  Lanes outside ROW_MASK keep
+// their own values (update_dpp with old = src), which the idempotent merge leaves unchanged.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_mov(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, CTRL, ROW_MASK, 0xf, false);
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void dpp_round(double &vu, int &iu, double &vl, int &il) {
+  const long long bu = __double_as_longlong(vu), bl = __double_as_longlong(vl);
+  const unsigned uh = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)(bu >> 32));
+  const unsigned ul = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)bu);
+  const unsigned lh = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)(bl >> 32));
+  const unsigned ll = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)bl);
+  const int oiu = dpp_mov<CTRL, ROW_MASK>(iu), oil = dpp_mov<CTRL, ROW_MASK>(il);
+  const double ou = __longlong_as_double((long long)(((unsigned long long)uh << 32) | ul));
+  const double ol = __longlong_as_double((long long)(((unsigned long long)lh << 32) | ll));
+  if (lt_min(ou, oiu, vu, iu)) { vu = ou; iu = oiu; }
+  if (gt_max(ol, oil, vl, il)) { vl = ol; il = oil; }
+}
+
+// Wave-wide selection, returned to every lane.  The (value, index) pairs are reduced with
+// DPP row operations (xor 1 and 2 inside quads, rotations by 4 and 8 inside rows of 16, then
+// the row-15 and row-31 broadcasts), which leaves the result in lane 63; the multiplier and
+// label of the winner are then read from the lane that holds it.  Must be called by all 64
+// lanes of the wave.
+__device__ __forceinline__ Sel sel_wave(const Sel &mine) {
+  double vu = mine.vu, vl = mine.vl;
+  int iu = mine.iu, il = mine.il;
+  dpp_round<0xB1, 0xF>(vu, iu, vl, il);   // quad_perm [1,0,3,2]
+  dpp_round<0x4E, 0xF>(vu, iu, vl, il);   // quad_perm [2,3,0,1]
+  dpp_round<0x124, 0xF>(vu, iu, vl, il);  // row_ror:4
+  dpp_round<0x128, 0xF>(vu, iu, vl, il);  // row_ror:8
+  dpp_round<0x142, 0xA>(vu, iu, vl, il);  // row_bcast:15 -> rows 1, 3
+  dpp_round<0x143, 0xC>(vu, iu, vl, il);  // row_bcast:31 -> rows 2, 3
+  Sel r;
+  r.vu = readlane_d(vu, 63);
+  r.iu = __builtin_amdgcn_readlane(iu, 63);
+  r.vl = readlane_d(vl, 63);
+  r.il = __builtin_amdgcn_readlane(il, 63);
+  const int lu = __ffsll((unsigned long long)__ballot(mine.iu == r.iu)) - 1;
+  const int ll = __ffsll((unsigned long long)__ballot(mine.il == r.il)) - 1;
+  r.au = readlane_d(mine.au, lu);
+  r.yu = __builtin_amdgcn_readlane(mine.yu, lu);
+  r.al = readlane_d(mine.al, ll);
+  r.yl = __builtin_amdgcn_readlane(mine.yl, ll);
+  return r;
+}
+
+// LDS hand-off between the waves of a workgroup.  Two buffers used alternately, so one
+// barrier per hand-off suffices: a buffer is rewritten only after another hand-off's barrier.
+struct SelLds {
+  Sel slot[2][NWAVE];
+  int flip;
 };
 
-// Block-wide reduction; the result is returned to every thread.
-__device__ __forceinline__ Sel sel_block(Sel s, SelShared &sh) {
-  sel_wave(s);
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    sh.vu[w] = s.vu; sh.au[w] = s.au; sh.iu[w] = s.iu;
-    sh.vl[w] = s.vl; sh.al[w] = s.al; sh.il[w] = s.il;
-  }
+// Combine the wave results of all waves; every thread returns the same workgroup result.
+__device__ __forceinline__ Sel sel_block(const Sel &wave_res, SelLds &L, int &buf) {
+  if ((threadIdx.x & 63) == 0) L.slot[buf][threadIdx.x >> 6] = wave_res;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int q = 1; q < NWAVE; ++q) sel_merge(s, sh.vu[q], sh.iu[q], sh.au[q], sh.vl[q], sh.il[q], sh.al[q]);
-    sh.out = s;
-  }
-  __syncthreads();
-  Sel r = sh.out;
-  __syncthreads();
+  Sel r = L.slot[buf][0];
+#pragma unroll
+  for (int q = 1; q < NWAVE; ++q) sel_merge(r, L.slot[buf][q]);
+  buf ^= 1;
   return r;
 }
 
@@ -94,11 +133,14 @@ __device__ __forceinline__ u64 stamp_word(unsigned stamp, unsigned payload) { re
 __device__ __forceinline__ double join_double(u64 hi, u64 lo) {
   return __longlong_as_double((long long)(((hi & 0xffffffffull) << 32) | (lo & 0xffffffffull)));
 }
+__device__ __forceinline__ unsigned pack_index(int i, int y) { return (unsigned)i | (y < 0 ? 0x80000000u : 0u); }
 
 // Exchange of the workgroup selections of one problem (see file comment, item 2).
-// Record layout (10 words): vu hi, vu lo, iu, au hi, au lo, vl hi, vl lo, il, al hi, al lo.
-__device__ Sel exchange(const Prob &P, int rank, unsigned stamp, Sel mine, SelShared &sh, uint64_t spin_limit,
-                        int32_t *err, int *abort_flag) {
+// Record layout (10 words): vu hi, vu lo, iu|yu, au hi, au lo, vl hi, vl lo, il|yl, al hi, al lo
+// (the label travels in bit 31 of the index word).  Wave 0 polls the records and reduces them;
+// the result reaches the other waves through LDS.
+__device__ Sel exchange(const Prob &P, int rank, unsigned stamp, const Sel &mine, SelLds &L, int &buf,
+                        uint64_t spin_limit, int32_t *err, int *abort_flag) {
   u64 *base = P.slots + (size_t)(stamp & 1u) * P.nwg * SLOT_WORDS;
   if (threadIdx.x < 10) {
     const u64 bvu = (u64)__double_as_longlong(mine.vu), bau = (u64)__double_as_longlong(mine.au);
@@ -107,41 +149,56 @@ __device__ Sel exchange(const Prob &P, int rank, unsigned stamp, Sel mine, SelSh
     switch (threadIdx.x) {
       case 0: pl = (unsigned)(bvu >> 32); break;
       case 1: pl = (unsigned)bvu; break;
-      case 2: pl = (unsigned)mine.iu; break;
+      case 2: pl = pack_index(mine.iu, mine.yu); break;
       case 3: pl = (unsigned)(bau >> 32); break;
       case 4: pl = (unsigned)bau; break;
       case 5: pl = (unsigned)(bvl >> 32); break;
       case 6: pl = (unsigned)bvl; break;
-      case 7: pl = (unsigned)mine.il; break;
+      case 7: pl = pack_index(mine.il, mine.yl); break;
       case 8: pl = (unsigned)(bal >> 32); break;
       default: pl = (unsigned)bal; break;
     }
     st_word(base + (size_t)rank * SLOT_WORDS + threadIdx.x, stamp_word(stamp, pl));
   }
-  Sel s;
-  sel_init(s);
-  for (int q = threadIdx.x; q < P.nwg; q += BS) {
-    const u64 *rec = base + (size_t)q * SLOT_WORDS;
-    u64 w[10];
-    const uint64_t t0 = wall_clock64();
-    for (;;) {
-      bool ok = true;
+  if (threadIdx.x < 64) {
+    Sel s;
+    sel_init(s);
+    for (int q = threadIdx.x; q < P.nwg; q += 64) {
+      const u64 *rec = base + (size_t)q * SLOT_WORDS;
+      u64 w[10];
+      const uint64_t t0 = wall_clock64();
+      for (;;) {
+        bool ok = true;
 #pragma unroll
-      for (int k = 0; k < 10; ++k) {
-        w[k] = ld_word(rec + k);
-        ok = ok && ((unsigned)(w[k] >> 32) == stamp);
+        for (int k = 0; k < 10; ++k) {
+          w[k] = ld_word(rec + k);
+          ok = ok && ((unsigned)(w[k] >> 32) == stamp);
+        }
+        if (ok) break;
+        if (wall_clock64() - t0 > spin_limit) {
+          __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          *abort_flag = 1;
+          break;
+        }
       }
-      if (ok) break;
-      if (wall_clock64() - t0 > spin_limit) {
-        __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *abort_flag = 1;
-        break;
-      }
+      Sel o;
+      o.vu = join_double(w[0], w[1]);
+      o.iu = (int)((unsigned)w[2] & 0x7fffffffu);
+      o.yu = ((unsigned)w[2] >> 31) ? -1 : 1;
+      o.au = join_double(w[3], w[4]);
+      o.vl = join_double(w[5], w[6]);
+      o.il = (int)((unsigned)w[7] & 0x7fffffffu);
+      o.yl = ((unsigned)w[7] >> 31) ? -1 : 1;
+      o.al = join_double(w[8], w[9]);
+      sel_merge(s, o);
     }
-    sel_merge(s, join_double(w[0], w[1]), (int)(unsigned)w[2], join_double(w[3], w[4]), join_double(w[5], w[6]),
-              (int)(unsigned)w[7], join_double(w[8], w[9]));
+    s = sel_wave(s);
+    if (threadIdx.x == 0) L.slot[buf][0] = s;
   }
-  return sel_block(s, sh);
+  __syncthreads();
+  const Sel r = L.slot[buf][0];
+  buf ^= 1;
+  return r;
 }
 
 // 2x2 sub-problem on (u, l): eta = K_uu + K_ll - 2 K_ul with K_uu = K_ll = 1 for the RBF
@@ -183,13 +240,22 @@ __device__ __forceinline__ int label_of(const Prob &P, int64_t j) {
   return P.y ? P.y[gmap(P, j)] : (j < P.len0 ? 1 : -1);
 }
 
+// Offer sample j (value f, multiplier a, label y) to this thread's candidates.
+__device__ __forceinline__ void consider(Sel &s, double f, double a, int y, int j, double C) {
+  const bool up = (y > 0 && a < C) || (y < 0 && a > 0.0);
+  const bool lo = (y > 0 && a > 0.0) || (y < 0 && a < C);
+  if (up && lt_min(f, j, s.vu, s.iu)) { s.vu = f; s.iu = j; s.au = a; s.yu = y; }
+  if (lo && gt_max(f, j, s.vl, s.il)) { s.vl = f; s.il = j; s.al = a; s.yl = y; }
+}
+
 // ---------------------------------------------------------------------------------------
 template <int PER, bool GRAM, bool VEC4>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   extern __shared__ float4 dyn4[];  // row path: x_u[d], x_l[d], krow[2][per_wg], tags[cap]
   float *dyn = reinterpret_cast<float *>(dyn4);
-  __shared__ SelShared sh;
+  __shared__ SelLds sh;
   __shared__ int s_abort;
+  int buf = 0;
 
   const int32_t pid = p.wg_prob[blockIdx.x];
   const Prob P = p.probs[pid];
@@ -228,24 +294,20 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
 
   const double C = p.C;
   const int64_t t_end = min(t + p.steps, p.max_iter);
-  for (;;) {
-    // 1. local candidates
-    Sel s;
-    sel_init(s);
+  // Candidates of this thread's samples; after the first scan they are gathered in the same
+  // pass as the f update of the previous step.
+  Sel s;
+  sel_init(s);
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int64_t j = base + threadIdx.x + (int64_t)k * BS;
-      if (j < lim) {
-        const bool up = (yv[k] > 0 && a[k] < C) || (yv[k] < 0 && a[k] > 0.0);
-        const bool lo = (yv[k] > 0 && a[k] > 0.0) || (yv[k] < 0 && a[k] < C);
-        if (up && lt_min(f[k], (int)j, s.vu, s.iu)) { s.vu = f[k]; s.iu = (int)j; s.au = a[k]; }
-        if (lo && gt_max(f[k], (int)j, s.vl, s.il)) { s.vl = f[k]; s.il = (int)j; s.al = a[k]; }
-      }
-    }
-    s = sel_block(s, sh);
+  for (int k = 0; k < PER; ++k) {
+    const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+    if (j < lim) consider(s, f[k], a[k], yv[k], (int)j, C);
+  }
+  for (;;) {
+    // 1. workgroup candidates
+    s = sel_block(sel_wave(s), sh, buf);
     // 2. exchange across the problem's workgroups
-    if (P.nwg > 1) s = exchange(P, rank, (unsigned)(t + 1), s, sh, p.spin_limit, p.error, &s_abort);
-    __syncthreads();
+    if (P.nwg > 1) s = exchange(P, rank, (unsigned)(t + 1), s, sh, buf, p.spin_limit, p.error, &s_abort);
     const bool aborted = s_abort != 0;
     // 3. stop rule
     if (rank == 0 && threadIdx.x == 0 && t < P.trace_len) {
@@ -269,7 +331,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
     }
     const int64_t u = s.iu, l = s.il;
     const int64_t gu = gmap(P, u), gl = gmap(P, l);
-    const double yu = (double)label_of(P, u), yl = (double)label_of(P, l);
+    const double yu = (double)s.yu, yl = (double)s.yl;
 
     // 4. kernel rows of u and l for the own samples, K_ul, 2x2 solve, f update
     float ku[PER], kl[PER];
@@ -350,6 +412,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
     const PairStep ps = solve_pair(C, s.vu, s.vl, s.au, s.al, yu, yl, kul);
     const double au_new = ps.au, al_new = ps.al;
     const double cu = (au_new - s.au) * yu, cl = (al_new - s.al) * yl;
+    sel_init(s);
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int64_t j = base + threadIdx.x + (int64_t)k * BS;
@@ -357,6 +420,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         f[k] += cu * (double)ku[k] + cl * (double)kl[k];
         if (j == u) a[k] = au_new;
         if (j == l) a[k] = al_new;
+        consider(s, f[k], a[k], yv[k], (int)j, C);
       }
     }
     ++t;
