@@ -89,22 +89,25 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
 
 // How a problem of n samples is spread over workgroups.
 struct Shape {
-  int32_t nwg, per_wg, per_thread;
+  int32_t nwg, per_wg, per_thread, g1, ng;
 };
+
+constexpr int32_t TWO_LEVEL_ABOVE = 64;  // workgroups per problem above which the exchange has two levels
 
 // Gram path: one workgroup up to 4096 samples (no exchange at all), else about sqrt(n)/3.5
 // workgroups -- the measured optimum between per-workgroup work and exchange cost on MI355X
-// (40 at n = 20,000, 64 at 50,000, 90 at 100,000).  `cap` bounds the count (one-vs-one runs
-// all pairs in one launch, so their workgroups must fit on the device together).
+// (40 at n = 20,000, 64 at 50,000, 90 at 100,000).  Row path: up to 256 workgroups of 512
+// threads (at least 64 samples each), so that the streaming of X keeps every CU busy.  `cap` bounds the count
+// (one-vs-one runs all pairs in one launch, so their workgroups must fit together).
 bool choose_shape(int64_t n, bool gram, int32_t requested, Shape *s, int64_t cap = 256) {
-  const int64_t BS = solver_block_size(), MAXP = max_per_thread();
+  const int64_t BS = solver_block_size(gram), MAXP = max_per_thread(gram);
   int64_t nwg;
   if (requested > 0)
     nwg = requested;
   else if (gram)
     nwg = n <= 4096 ? 1 : std::min<int64_t>(cap, std::max<int64_t>(8, (int64_t)std::ceil(std::sqrt((double)n) / 3.5)));
   else
-    nwg = std::min<int64_t>(cap, std::max<int64_t>(1, (n + 127) / 128));
+    nwg = std::min<int64_t>(cap, std::max<int64_t>(1, (n + 63) / 64));
   nwg = std::max<int64_t>(1, std::min<int64_t>(nwg, n));
   if ((n + nwg - 1) / nwg > BS * MAXP) nwg = (n + BS * MAXP - 1) / (BS * MAXP);
   int64_t per_wg = (n + nwg - 1) / nwg;
@@ -115,6 +118,13 @@ bool choose_shape(int64_t n, bool gram, int32_t requested, Shape *s, int64_t cap
   s->nwg = (int32_t)nwg;
   s->per_wg = (int32_t)per_wg;
   s->per_thread = (int32_t)p;
+  if (nwg > TWO_LEVEL_ABOVE) {
+    s->g1 = (int32_t)std::ceil(std::sqrt((double)nwg));
+    s->ng = (int32_t)((nwg + s->g1 - 1) / s->g1);
+  } else {
+    s->g1 = 0;
+    s->ng = 0;
+  }
   return true;
 }
 
@@ -133,8 +143,8 @@ struct TrainPlan {
   int64_t ld;
   Shape shape;
   int32_t cache_cap;
-  int64_t off_f, off_gram, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_tul, off_tb, off_fin,
-      off_err;
+  int64_t off_f, off_gram, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_tul, off_tb,
+      off_fin, off_err;
   int64_t total;
 };
 
@@ -156,8 +166,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   if (!p->gram) {
     if (o.row_cache_bytes > 0)
       p->cache_cap = (int32_t)std::min<int64_t>(CACHE_CAP_MAX, std::min<int64_t>(n, o.row_cache_bytes / (4 * p->ld)));
-    const int64_t lds = (2 * d + 2 * (int64_t)solver_block_size() * p->shape.per_thread) * 4 + 4LL * p->cache_cap + 64 +
-                        1024;
+    const int64_t lds = (2 * d + 2 * (int64_t)p->shape.per_wg) * 4 + 4LL * p->cache_cap + 64 + 4096;
     if (lds > LDS_BYTES)
       return fail(SVM_EINVAL, "row path: d=%lld does not fit the 160 KiB LDS of a workgroup; use the Gram path",
                   (long long)d);
@@ -171,6 +180,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   p->off_prob = L.add(sizeof(Prob));
   p->off_wgp = L.add(4LL * p->shape.nwg);
   p->off_slots = L.add(8LL * 2 * p->shape.nwg * SLOT_WORDS);
+  p->off_slots2 = L.add(8LL * 2 * std::max(1, p->shape.ng) * SLOT_WORDS);
   p->off_tul = L.add(4LL * 2 * o.trace_len);
   p->off_tb = L.add(8LL * 2 * o.trace_len);
   p->off_fin = L.add(8 * 4);
@@ -265,11 +275,12 @@ struct OvoPlan {
   bool gram;
   int64_t ld;
   int32_t P;
-  int64_t off_perm, off_xs, off_f, off_gram, off_ctl, off_prob, off_wgp, off_slots, off_fin, off_err;
+  int64_t off_perm, off_xs, off_f, off_gram, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_fin, off_err;
   int64_t total;
 };
 
 constexpr int32_t OVO_MAX_WG_PER_PAIR = 256;
+constexpr int32_t OVO_MAX_GROUPS = 16;  // second-level groups of a pair: ceil(256 / ceil(sqrt(256)))
 constexpr int64_t OVO_TOTAL_WG = 512;  // default workgroup budget shared by all pairs of one launch
 
 svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) {
@@ -282,7 +293,7 @@ svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) 
   const double gram_bytes = 4.0 * (double)n * (double)p->ld;
   p->gram = o.gram == SVM_GRAM_ON || (o.gram == SVM_GRAM_AUTO && gram_bytes <= (double)o.gram_budget);
   if (!p->gram) {
-    const int64_t lds = (2 * d + 2 * (int64_t)solver_block_size() * max_per_thread()) * 4 + 1024;
+    const int64_t lds = (2 * d + 2 * (int64_t)solver_block_size(false) * max_per_thread(false)) * 4 + 4096;
     if (lds > LDS_BYTES) return fail(SVM_EINVAL, "row path: d=%lld does not fit LDS", (long long)d);
   }
   Layout L;
@@ -294,6 +305,7 @@ svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) 
   p->off_prob = L.add((int64_t)sizeof(Prob) * p->P);
   p->off_wgp = L.add(4LL * p->P * OVO_MAX_WG_PER_PAIR);
   p->off_slots = L.add(8LL * 2 * SLOT_WORDS * p->P * OVO_MAX_WG_PER_PAIR);
+  p->off_slots2 = L.add(8LL * 2 * SLOT_WORDS * p->P * OVO_MAX_GROUPS);
   p->off_fin = L.add(8LL * 4 * p->P);
   p->off_err = L.add(16);
   p->total = round_up(L.total, ALIGN);
@@ -393,6 +405,9 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   hp.wg0 = 0;
   hp.nwg = p.shape.nwg;
   hp.per_wg = p.shape.per_wg;
+  hp.g1 = p.shape.g1;
+  hp.ng = p.shape.ng;
+  hp.slots2 = p.shape.g1 ? reinterpret_cast<u64 *>(ws + p.off_slots2) : nullptr;
   std::vector<int32_t> hwgp(p.shape.nwg, 0);
   HIPCHK(hipMemcpyAsync(dprob, &hp, sizeof(Prob), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
@@ -530,6 +545,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   Prob *dprob = reinterpret_cast<Prob *>(ws + p.off_prob);
   int32_t *wgp = reinterpret_cast<int32_t *>(ws + p.off_wgp);
   u64 *slots = reinterpret_cast<u64 *>(ws + p.off_slots);
+  u64 *slots2 = reinterpret_cast<u64 *>(ws + p.off_slots2);
   double *fin = reinterpret_cast<double *>(ws + p.off_fin);
   int32_t *err = reinterpret_cast<int32_t *>(ws + p.off_err);
 
@@ -554,6 +570,9 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
       if (!choose_shape(P.n, p.gram, r.workgroups, &sh, cap) || sh.nwg > OVO_MAX_WG_PER_PAIR)
         return fail(SVM_ENOMEM, "pair (%d,%d) too large to place", a, bb);
       P.slots = slots + (size_t)q * 2 * OVO_MAX_WG_PER_PAIR * SLOT_WORDS;
+      P.g1 = sh.g1;
+      P.ng = sh.ng;
+      P.slots2 = sh.g1 ? slots2 + (size_t)q * 2 * OVO_MAX_GROUPS * SLOT_WORDS : nullptr;
       P.wg0 = wg;
       P.nwg = sh.nwg;
       P.per_wg = sh.per_wg;

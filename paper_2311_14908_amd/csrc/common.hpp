@@ -31,11 +31,14 @@ struct Prob {
   double *f;          // [n]
   Ctl *ctl;
   u64 *slots;         // exchange words [2][nwg][SLOT_WORDS]
+  u64 *slots2;        // second exchange level [2][ng][SLOT_WORDS], or NULL
   int32_t *trace_ul;  // [2*trace_len] or NULL
   double *trace_b;    // [2*trace_len] or NULL
   int64_t trace_len;
   int32_t wg0, nwg;   // workgroups [wg0, wg0+nwg) of the launch serve this problem
   int32_t per_wg;     // local samples per workgroup
+  int32_t g1;         // workgroups per first-level exchange group (0 = one level)
+  int32_t ng;         // number of first-level groups
   int32_t pad;
 };
 
@@ -78,7 +81,7 @@ hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t
                               const float *T, int64_t m, double b, double *dec, int64_t dec_stride, hipStream_t s);
 hipError_t launch_ovo_vote(const double *dec, int64_t m, int32_t k, int32_t *pred, hipStream_t s);
 
-int solver_block_size();
-int max_per_thread();
+int solver_block_size(bool gram);
+int max_per_thread(bool gram);
 
 }  // namespace svmx

@@ -1,8 +1,9 @@
 // gram.hip -- RBF Gram precompute on MFMA, kernel rows from X, and row gathers (gfx950).
 //
 // G_ij = exp(-gamma * max(0, |x_i|^2 + |x_j|^2 - 2 x_i.x_j)): the dot products form the
-// contraction X X^T, run on v_mfma_f32_16x16x4f32 with fp32 inputs and accumulation; the
-// row norms are accumulated from the same LDS tiles and the RBF map is the epilogue.  The
+// contraction X X^T, run on v_mfma_f32_16x16x4f32 with fp32 inputs and accumulation over the
+// upper-triangle tiles only (G is symmetric); the row norms are accumulated from the same LDS
+// tiles and the RBF map is the epilogue.  The
 // kernel is the Gaussian RBF the paper names (Section III.C).
 #include "common.hpp"
 #include "rbf_rows.hpp"
@@ -51,20 +52,39 @@ __device__ __forceinline__ void load_slab(const float *__restrict__ X, int64_t n
   }
 }
 
-template <bool VEC4>
-__global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X, int64_t n, int64_t d, float gamma,
-                                                     float *__restrict__ G, int64_t ld) {
+// One 128x128 tile (rows i0.., columns j0..) of the Gram for each tile with ti <= tj (the
+// upper triangle); a tile off the diagonal is stored twice, as itself and mirrored.  Tiles are
+// handed out XCD-major: consecutive workgroups of one XCD take consecutive tiles of one tile
+// row, so they share its row slab in that XCD's L2.  The RBF map is exp2(c * t) with
+// c = -gamma * log2(e) and t = |x_i|^2 + |x_j|^2 - 2 x_i.x_j clamped at 0 (v_exp_f32).
+template <bool VEC4, bool STORE4>
+__global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X, int64_t n, int64_t d, float c,
+                                                     float *__restrict__ G, int64_t ld, int64_t nt, int64_t ntiles) {
   __shared__ float As[GKC][GPAD];
   __shared__ float Bs[GKC][GPAD];
   __shared__ float nA[GT], nB[GT];
-  const int64_t i0 = (int64_t)blockIdx.y * GT, j0 = (int64_t)blockIdx.x * GT;
+  // XCD-major swizzle of the linear tile index, then (ti, tj) of the upper triangle
+  const int64_t per_xcd = (ntiles + 7) / 8;
+  const int64_t b = (int64_t)blockIdx.x;
+  const int64_t lin = (b % 8) * per_xcd + b / 8;
+  if (lin >= ntiles) return;
+  // row ti starts at s(ti) = ti*nt - ti*(ti-1)/2; invert with a square root and fix up
+  const double tw = 2.0 * (double)nt + 1.0;
+  int64_t ti = (int64_t)((tw - sqrt(tw * tw - 8.0 * (double)lin)) * 0.5);
+  if (ti < 0) ti = 0;
+  if (ti >= nt) ti = nt - 1;
+  while (ti > 0 && ti * nt - ti * (ti - 1) / 2 > lin) --ti;
+  while ((ti + 1) * nt - (ti + 1) * ti / 2 <= lin) ++ti;
+  const int64_t tj = ti + (lin - (ti * nt - ti * (ti - 1) / 2));
+  const int64_t i0 = ti * GT, j0 = tj * GT;
+
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w >> 1, wn = w & 1;
   v4f acc[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = (v4f){0.f, 0.f, 0.f, 0.f};
+    for (int bb = 0; bb < 4; ++bb) acc[a][bb] = (v4f){0.f, 0.f, 0.f, 0.f};
   float na[2] = {0.f, 0.f}, nb[2] = {0.f, 0.f};
 
   for (int64_t k0 = 0; k0 < d; k0 += GKC) {
@@ -81,7 +101,8 @@ __global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
+        for (int bb = 0; bb < 4; ++bb)
+          acc[a][bb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[bb], acc[a][bb], 0, 0, 0);
     }
     __syncthreads();
   }
@@ -101,20 +122,35 @@ __global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X
   }
   __syncthreads();
   // epilogue: lane holds D[4*(lane/16)+e][lane%16] of each 16x16 block
+  const bool mirror = ti != tj;
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
+    const int lr0 = wm * 64 + a * 16 + 4 * (lane >> 4);
+    const int64_t gr0 = i0 + lr0;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int lc = wn * 64 + b * 16 + (lane & 15);
+    for (int bb = 0; bb < 4; ++bb) {
+      const int lc = wn * 64 + bb * 16 + (lane & 15);
       const int64_t gc = j0 + lc;
+      float kv[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int lr = wm * 64 + a * 16 + 4 * (lane >> 4) + e;
-        const int64_t gr = i0 + lr;
-        if (gr < n && gc < n) {
-          float t = nA[lr] + nB[lc] - 2.0f * acc[a][b][e];
-          t = t > 0.f ? t : 0.f;
-          G[gr * ld + gc] = (gr == gc) ? 1.0f : expf(-gamma * t);
+        float t = nA[lr0 + e] + nB[lc] - 2.0f * acc[a][bb][e];
+        t = t > 0.f ? t : 0.f;
+        kv[e] = (gr0 + e == gc) ? 1.0f : __builtin_amdgcn_exp2f(c * t);
+      }
+      if (gc < n) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (gr0 + e < n) G[(gr0 + e) * ld + gc] = kv[e];
+        if (mirror) {
+          float *dst = G + gc * ld + gr0;
+          if (STORE4 && gr0 + 3 < n) {
+            *reinterpret_cast<float4 *>(dst) = make_float4(kv[0], kv[1], kv[2], kv[3]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (gr0 + e < n) dst[e] = kv[e];
+          }
         }
       }
     }
@@ -122,14 +158,21 @@ __global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X
 }
 
 hipError_t launch_gram(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, hipStream_t s) {
-  const int64_t tiles = (n + GT - 1) / GT;
-  if (tiles > 65535) return hipErrorInvalidValue;
-  dim3 grid((unsigned)tiles, (unsigned)tiles);
+  const int64_t nt = (n + GT - 1) / GT;
+  const int64_t ntiles = nt * (nt + 1) / 2;
+  const int64_t grid = ((ntiles + 7) / 8) * 8;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
+  const float c = -gamma * 1.4426950408889634f;
   const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);
-  if (vec4)
-    hipLaunchKernelGGL(gram_rbf_mfma<true>, grid, dim3(GBS), 0, s, X, n, d, gamma, G, ld);
+  const bool st4 = (ld % 4 == 0) && ((reinterpret_cast<uintptr_t>(G) & 15) == 0);
+  if (vec4 && st4)
+    hipLaunchKernelGGL((gram_rbf_mfma<true, true>), dim3((unsigned)grid), dim3(GBS), 0, s, X, n, d, c, G, ld, nt, ntiles);
+  else if (vec4)
+    hipLaunchKernelGGL((gram_rbf_mfma<true, false>), dim3((unsigned)grid), dim3(GBS), 0, s, X, n, d, c, G, ld, nt, ntiles);
+  else if (st4)
+    hipLaunchKernelGGL((gram_rbf_mfma<false, true>), dim3((unsigned)grid), dim3(GBS), 0, s, X, n, d, c, G, ld, nt, ntiles);
   else
-    hipLaunchKernelGGL(gram_rbf_mfma<false>, grid, dim3(GBS), 0, s, X, n, d, gamma, G, ld);
+    hipLaunchKernelGGL((gram_rbf_mfma<false, false>), dim3((unsigned)grid), dim3(GBS), 0, s, X, n, d, c, G, ld, nt, ntiles);
   return hipGetLastError();
 }
 
@@ -138,6 +181,7 @@ template <bool VEC4>
 __global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X, int64_t n, int64_t d, double gamma,
                                                       const int64_t *__restrict__ rows, int64_t r,
                                                       float *__restrict__ out) {
+  constexpr int SB = 4;
   extern __shared__ float4 sx4[];  // two staged rows
   float *sx = reinterpret_cast<float *>(sx4);
   const int64_t q0 = 2 * (int64_t)blockIdx.y;
@@ -152,12 +196,22 @@ __global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X
   const int lig = threadIdx.x & (gs - 1);
   const int ngroups = 256 / gs;
   const int grp = threadIdx.x / gs;
-  for (int64_t j = (int64_t)blockIdx.x * ngroups + grp; j < n; j += (int64_t)gridDim.x * ngroups) {
-    double du, dl;
-    dist2_group<VEC4>(X + j * d, sx, sx + d, d, lig, gs, du, dl);
-    if (lig == 0) {
-      out[q0 * n + j] = (float)exp(-gamma * du);
-      if (q1 != q0) out[q1 * n + j] = (float)exp(-gamma * dl);
+  const int64_t chunk = (int64_t)ngroups * SB;
+  for (int64_t j0 = (int64_t)blockIdx.x * chunk + (int64_t)grp * SB; j0 < n; j0 += (int64_t)gridDim.x * chunk) {
+    const int nb = (int)(n - j0 < SB ? n - j0 : SB);
+    const float *xs[SB];
+#pragma unroll
+    for (int b = 0; b < SB; ++b) xs[b] = X + (j0 + (b < nb ? b : nb - 1)) * d;
+    double du[SB], dl[SB];
+    dist2_batch<VEC4, SB>(xs, nb, sx, sx + d, d, lig, gs, du, dl);
+    for (int v = lig; v < 2 * SB; v += gs) {
+      const int b = v < SB ? v : v - SB;
+      if (b >= nb) continue;
+      const float kv = rbf_of(batch_value<SB>(du, dl, v), gamma);
+      if (v < SB)
+        out[q0 * n + j0 + b] = kv;
+      else if (q1 != q0)
+        out[q1 * n + j0 + b] = kv;
     }
   }
 }
@@ -166,7 +220,7 @@ hipError_t launch_kernel_rows(const float *X, int64_t n, int64_t d, double gamma
                               float *out, hipStream_t s) {
   const int64_t pairs = (r + 1) / 2;
   if (pairs > 65535) return hipErrorInvalidValue;
-  int64_t bx = (n + 63) / 64;
+  int64_t bx = (n + 255) / 256;
   if (bx > 1024) bx = 1024;
   const size_t shmem = 2 * (size_t)d * sizeof(float);
   const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);

@@ -6,10 +6,12 @@
 // (r+1)*per_wg) and keeps their f, alpha and label in registers for the whole launch.
 // Each step:
 //   1. every workgroup selects its own candidates  u_r = argmin_{I_up} f,  l_r = argmax_{I_low} f
-//      (ties to the smaller index) with wave shuffles and LDS;
+//      (ties to the smaller index) with DPP wave reductions and one LDS hand-off;
 //   2. the nwg partial results are exchanged through global memory as self-stamped 64-bit
 //      words (payload | step stamp), so no fence or cache flush is needed: a reader simply
-//      waits until every word it needs carries the current stamp;
+//      waits until every word it needs carries the current stamp.  Above 64 workgroups the
+//      exchange has two levels (group leaders reduce about sqrt(nwg) records each and publish
+//      a group record; every workgroup then reads the group records);
 //   3. every workgroup reduces the same nwg records to the same pair (u, l), tests the stop
 //      rule, and solves the 2x2 sub-problem redundantly (identical fp64 arithmetic);
 //   4. every workgroup fetches K(u, j) and K(l, j) for its own samples -- from the Gram or
@@ -23,13 +25,16 @@
 
 namespace svmx {
 
-constexpr int BS = 256;
-constexpr int NWAVE = BS / 64;
+// Gram path: 256-thread workgroups, up to 16 samples per thread.  Row path: 512-thread
+// workgroups (8 waves per CU, each with 4 samples x the lane's float4 loads in flight, keep
+// the streaming of X busy without spilling), up to 8 samples per thread.
+constexpr int BS_GRAM = 256, MAXP_GRAM = 16;
+constexpr int BS_ROWS = 512, MAXP_ROWS = 8;
+constexpr int ROW_BATCH = 4;  // samples per lane group and batch in the row evaluation
 constexpr int IBIG = 0x7fffffff;
-constexpr int MAX_PER = 16;
 
-int solver_block_size() { return BS; }
-int max_per_thread() { return MAX_PER; }
+int solver_block_size(bool gram) { return gram ? BS_GRAM : BS_ROWS; }
+int max_per_thread(bool gram) { return gram ? MAXP_GRAM : MAXP_ROWS; }
 
 __device__ __forceinline__ bool lt_min(double v2, int i2, double v, int i) { return v2 < v || (v2 == v && i2 < i); }
 __device__ __forceinline__ bool gt_max(double v2, int i2, double v, int i) { return v2 > v || (v2 == v && i2 < i); }
@@ -109,18 +114,19 @@ __device__ __forceinline__ Sel sel_wave(const Sel &mine) {
 
 // LDS hand-off between the waves of a workgroup.  Two buffers used alternately, so one
 // barrier per hand-off suffices: a buffer is rewritten only after another hand-off's barrier.
+template <int NW>
 struct SelLds {
-  Sel slot[2][NWAVE];
-  int flip;
+  Sel slot[2][NW];
 };
 
 // Combine the wave results of all waves; every thread returns the same workgroup result.
-__device__ __forceinline__ Sel sel_block(const Sel &wave_res, SelLds &L, int &buf) {
+template <int NW>
+__device__ __forceinline__ Sel sel_block(const Sel &wave_res, SelLds<NW> &L, int &buf) {
   if ((threadIdx.x & 63) == 0) L.slot[buf][threadIdx.x >> 6] = wave_res;
   __syncthreads();
   Sel r = L.slot[buf][0];
 #pragma unroll
-  for (int q = 1; q < NWAVE; ++q) sel_merge(r, L.slot[buf][q]);
+  for (int q = 1; q < NW; ++q) sel_merge(r, L.slot[buf][q]);
   buf ^= 1;
   return r;
 }
@@ -135,64 +141,91 @@ __device__ __forceinline__ double join_double(u64 hi, u64 lo) {
 }
 __device__ __forceinline__ unsigned pack_index(int i, int y) { return (unsigned)i | (y < 0 ? 0x80000000u : 0u); }
 
-// Exchange of the workgroup selections of one problem (see file comment, item 2).
-// Record layout (10 words): vu hi, vu lo, iu|yu, au hi, au lo, vl hi, vl lo, il|yl, al hi, al lo
-// (the label travels in bit 31 of the index word).  Wave 0 polls the records and reduces them;
-// the result reaches the other waves through LDS.
-__device__ Sel exchange(const Prob &P, int rank, unsigned stamp, const Sel &mine, SelLds &L, int &buf,
-                        uint64_t spin_limit, int32_t *err, int *abort_flag) {
-  u64 *base = P.slots + (size_t)(stamp & 1u) * P.nwg * SLOT_WORDS;
-  if (threadIdx.x < 10) {
-    const u64 bvu = (u64)__double_as_longlong(mine.vu), bau = (u64)__double_as_longlong(mine.au);
-    const u64 bvl = (u64)__double_as_longlong(mine.vl), bal = (u64)__double_as_longlong(mine.al);
+// Exchange record (10 words): vu hi, vu lo, iu|yu, au hi, au lo, vl hi, vl lo, il|yl, al hi,
+// al lo; the label travels in bit 31 of the index word.  Lanes 0..9 of the calling wave each
+// write one word.
+__device__ __forceinline__ void put_record(u64 *rec, unsigned stamp, const Sel &s) {
+  const int t = threadIdx.x & 63;
+  if (t < 10) {
+    const u64 bvu = (u64)__double_as_longlong(s.vu), bau = (u64)__double_as_longlong(s.au);
+    const u64 bvl = (u64)__double_as_longlong(s.vl), bal = (u64)__double_as_longlong(s.al);
     unsigned pl;
-    switch (threadIdx.x) {
+    switch (t) {
       case 0: pl = (unsigned)(bvu >> 32); break;
       case 1: pl = (unsigned)bvu; break;
-      case 2: pl = pack_index(mine.iu, mine.yu); break;
+      case 2: pl = pack_index(s.iu, s.yu); break;
       case 3: pl = (unsigned)(bau >> 32); break;
       case 4: pl = (unsigned)bau; break;
       case 5: pl = (unsigned)(bvl >> 32); break;
       case 6: pl = (unsigned)bvl; break;
-      case 7: pl = pack_index(mine.il, mine.yl); break;
+      case 7: pl = pack_index(s.il, s.yl); break;
       case 8: pl = (unsigned)(bal >> 32); break;
       default: pl = (unsigned)bal; break;
     }
-    st_word(base + (size_t)rank * SLOT_WORDS + threadIdx.x, stamp_word(stamp, pl));
+    st_word(rec + t, stamp_word(stamp, pl));
   }
-  if (threadIdx.x < 64) {
-    Sel s;
-    sel_init(s);
-    for (int q = threadIdx.x; q < P.nwg; q += 64) {
-      const u64 *rec = base + (size_t)q * SLOT_WORDS;
-      u64 w[10];
-      const uint64_t t0 = wall_clock64();
-      for (;;) {
-        bool ok = true;
+}
+
+// Wave-level: wait for records [q0, q1) of `words` to carry `stamp`, reduce them, and return
+// the result to every lane of the wave (all 64 lanes must call).
+__device__ Sel poll_reduce(const u64 *words, int q0, int q1, unsigned stamp, uint64_t spin_limit, int32_t *err,
+                           int *abort_flag) {
+  Sel s;
+  sel_init(s);
+  for (int q = q0 + (int)(threadIdx.x & 63); q < q1; q += 64) {
+    const u64 *rec = words + (size_t)q * SLOT_WORDS;
+    u64 w[10];
+    const uint64_t t0 = wall_clock64();
+    for (;;) {
+      bool ok = true;
 #pragma unroll
-        for (int k = 0; k < 10; ++k) {
-          w[k] = ld_word(rec + k);
-          ok = ok && ((unsigned)(w[k] >> 32) == stamp);
-        }
-        if (ok) break;
-        if (wall_clock64() - t0 > spin_limit) {
-          __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          *abort_flag = 1;
-          break;
-        }
+      for (int k = 0; k < 10; ++k) {
+        w[k] = ld_word(rec + k);
+        ok = ok && ((unsigned)(w[k] >> 32) == stamp);
       }
-      Sel o;
-      o.vu = join_double(w[0], w[1]);
-      o.iu = (int)((unsigned)w[2] & 0x7fffffffu);
-      o.yu = ((unsigned)w[2] >> 31) ? -1 : 1;
-      o.au = join_double(w[3], w[4]);
-      o.vl = join_double(w[5], w[6]);
-      o.il = (int)((unsigned)w[7] & 0x7fffffffu);
-      o.yl = ((unsigned)w[7] >> 31) ? -1 : 1;
-      o.al = join_double(w[8], w[9]);
-      sel_merge(s, o);
+      if (ok) break;
+      if (wall_clock64() - t0 > spin_limit) {
+        __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *abort_flag = 1;
+        break;
+      }
     }
-    s = sel_wave(s);
+    Sel o;
+    o.vu = join_double(w[0], w[1]);
+    o.iu = (int)((unsigned)w[2] & 0x7fffffffu);
+    o.yu = ((unsigned)w[2] >> 31) ? -1 : 1;
+    o.au = join_double(w[3], w[4]);
+    o.vl = join_double(w[5], w[6]);
+    o.il = (int)((unsigned)w[7] & 0x7fffffffu);
+    o.yl = ((unsigned)w[7] >> 31) ? -1 : 1;
+    o.al = join_double(w[8], w[9]);
+    sel_merge(s, o);
+  }
+  return sel_wave(s);
+}
+
+// Exchange of the workgroup selections of one problem (see file comment, item 2).  Wave 0
+// does the global-memory work; the result reaches the other waves through LDS.
+template <int NW>
+__device__ Sel exchange(const Prob &P, int rank, unsigned stamp, const Sel &mine, SelLds<NW> &L, int &buf,
+                        uint64_t spin_limit, int32_t *err, int *abort_flag) {
+  const size_t par = stamp & 1u;
+  u64 *lv1 = P.slots + par * (size_t)P.nwg * SLOT_WORDS;
+  if (threadIdx.x < 64) {
+    put_record(lv1 + (size_t)rank * SLOT_WORDS, stamp, mine);
+    Sel s;
+    if (P.g1 > 0) {
+      u64 *lv2 = P.slots2 + par * (size_t)P.ng * SLOT_WORDS;
+      const int g = rank / P.g1;
+      if (rank % P.g1 == 0) {
+        const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
+        const Sel gs = poll_reduce(lv1, q0, q1, stamp, spin_limit, err, abort_flag);
+        put_record(lv2 + (size_t)g * SLOT_WORDS, stamp, gs);
+      }
+      s = poll_reduce(lv2, 0, P.ng, stamp, spin_limit, err, abort_flag);
+    } else {
+      s = poll_reduce(lv1, 0, P.nwg, stamp, spin_limit, err, abort_flag);
+    }
     if (threadIdx.x == 0) L.slot[buf][0] = s;
   }
   __syncthreads();
@@ -249,12 +282,15 @@ __device__ __forceinline__ void consider(Sel &s, double f, double a, int y, int 
 }
 
 // ---------------------------------------------------------------------------------------
-template <int PER, bool GRAM, bool VEC4>
+template <int BS, int PER, bool GRAM, bool VEC4>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
+  constexpr int NW = BS / 64;
+  constexpr int SB = ROW_BATCH;
   extern __shared__ float4 dyn4[];  // row path: x_u[d], x_l[d], krow[2][per_wg], tags[cap]
   float *dyn = reinterpret_cast<float *>(dyn4);
-  __shared__ SelLds sh;
+  __shared__ SelLds<NW> sh;
   __shared__ int s_abort;
+  __shared__ double s_kul;
   int buf = 0;
 
   const int32_t pid = p.wg_prob[blockIdx.x];
@@ -305,9 +341,9 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   }
   for (;;) {
     // 1. workgroup candidates
-    s = sel_block(sel_wave(s), sh, buf);
+    s = sel_block<NW>(sel_wave(s), sh, buf);
     // 2. exchange across the problem's workgroups
-    if (P.nwg > 1) s = exchange(P, rank, (unsigned)(t + 1), s, sh, buf, p.spin_limit, p.error, &s_abort);
+    if (P.nwg > 1) s = exchange<NW>(P, rank, (unsigned)(t + 1), s, sh, buf, p.spin_limit, p.error, &s_abort);
     const bool aborted = s_abort != 0;
     // 3. stop rule
     if (rank == 0 && threadIdx.x == 0 && t < P.trace_len) {
@@ -352,7 +388,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
     } else {
       const int64_t d = p.d;
       const int gs = group_size_for(d, VEC4);
-      const int lane_in_group = threadIdx.x & (gs - 1);
+      const int lig = threadIdx.x & (gs - 1);
       const int ngroups = BS / gs;
       const int grp = threadIdx.x / gs;
       const float *xu = p.X + gu * d, *xl = p.X + gl * d;
@@ -369,22 +405,25 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         hit_l = tags[sl] == (int)gl;
       }
       __syncthreads();
-      // K_ul from the staged rows (group 0)
-      __shared__ double s_kul;
+      // K_ul: x_l as the sample against the staged x_u, exactly as the row of u evaluates it
       if (grp == 0) {
-        double du, dl;
-        dist2_group<VEC4>(sxl, sxu, sxu, d, lane_in_group, gs, du, dl);
-        if (lane_in_group == 0) s_kul = (double)(float)exp(-p.gamma * du);
+        const float *xs1[1] = {sxl};
+        double du1[1], dl1[1];
+        dist2_batch<VEC4, 1>(xs1, 1, sxu, sxu, d, lig, gs, du1, dl1);
+        if (lig == 0) s_kul = (double)rbf_of(du1[0], p.gamma);
       }
-      const bool need = !(hit_u && hit_l);
-      if (need) {
+      if (!(hit_u && hit_l)) {
         const int64_t cnt = lim - base;
-        for (int64_t q = grp; q < cnt; q += ngroups) {
-          double du, dl;
-          dist2_group<VEC4>(p.X + gmap(P, base + q) * d, sxu, sxl, d, lane_in_group, gs, du, dl);
-          if (lane_in_group == 0) {
-            krow[q] = (float)exp(-p.gamma * du);
-            krow[P.per_wg + q] = (float)exp(-p.gamma * dl);
+        for (int64_t q0 = (int64_t)grp * SB; q0 < cnt; q0 += (int64_t)ngroups * SB) {
+          const int nb = (int)min<int64_t>(SB, cnt - q0);
+          const float *xs[SB];
+#pragma unroll
+          for (int b = 0; b < SB; ++b) xs[b] = p.X + gmap(P, base + q0 + min(b, nb - 1)) * d;
+          double du[SB], dl[SB];
+          dist2_batch<VEC4, SB>(xs, nb, sxu, sxl, d, lig, gs, du, dl);
+          for (int v = lig; v < 2 * SB; v += gs) {
+            const int b = v < SB ? v : v - SB;
+            if (b < nb) krow[(v < SB ? 0 : P.per_wg) + q0 + b] = rbf_of(batch_value<SB>(du, dl, v), p.gamma);
           }
         }
       }
@@ -436,7 +475,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   }
   if (use_cache) {
     __syncthreads();
-    for (int s = threadIdx.x; s < p.cache_cap; s += BS) p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s] = tags[s];
+    for (int s2 = threadIdx.x; s2 < p.cache_cap; s2 += BS) p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s2] = tags[s2];
   }
 }
 
@@ -444,13 +483,15 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
 __global__ void smo_init(const Prob *probs, int32_t nprob) {
   const int32_t pid = blockIdx.y;
   const Prob P = probs[pid];
-  for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < P.n; j += (int64_t)gridDim.x * blockDim.x) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  for (int64_t j = i0; j < P.n; j += stride) {
     P.alpha[j] = 0.0;
     P.f[j] = -(double)label_of(P, j);
   }
-  const int64_t nw = 2 * (int64_t)P.nwg * SLOT_WORDS;
-  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < nw; q += (int64_t)gridDim.x * blockDim.x)
-    P.slots[q] = 0ull;
+  for (int64_t q = i0; q < 2 * (int64_t)P.nwg * SLOT_WORDS; q += stride) P.slots[q] = 0ull;
+  if (P.slots2)
+    for (int64_t q = i0; q < 2 * (int64_t)P.ng * SLOT_WORDS; q += stride) P.slots2[q] = 0ull;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     P.ctl->t = 0;
     P.ctl->status = ST_RUNNING;
@@ -461,18 +502,20 @@ __global__ void smo_init(const Prob *probs, int32_t nprob) {
   }
 }
 
+constexpr int FBS = 256;
+
 // Per problem: out[4p+0] = sum a, out[4p+1] = sum a y f, out[4p+2] = #(a>0), out[4p+3] = #(a>=C).
-__global__ void __launch_bounds__(BS) smo_finalize(const Prob *probs, double C, double *out) {
+__global__ void __launch_bounds__(FBS) smo_finalize(const Prob *probs, double C, double *out) {
   const Prob P = probs[blockIdx.x];
   double sa = 0.0, saf = 0.0, nsv = 0.0, nb = 0.0;
-  for (int64_t j = threadIdx.x; j < P.n; j += BS) {
+  for (int64_t j = threadIdx.x; j < P.n; j += FBS) {
     const double aj = P.alpha[j];
     sa += aj;
     saf += aj * (double)label_of(P, j) * P.f[j];
     nsv += aj > 0.0 ? 1.0 : 0.0;
     nb += aj >= C ? 1.0 : 0.0;
   }
-  __shared__ double red[4][NWAVE];
+  __shared__ double red[4][FBS / 64];
   for (int o = 32; o > 0; o >>= 1) {
     sa += __shfl_xor(sa, o);
     saf += __shfl_xor(saf, o);
@@ -484,7 +527,7 @@ __global__ void __launch_bounds__(BS) smo_finalize(const Prob *probs, double C, 
   __syncthreads();
   if (threadIdx.x < 4) {
     double v = 0.0;
-    for (int q = 0; q < NWAVE; ++q) v += red[threadIdx.x][q];
+    for (int q = 0; q < FBS / 64; ++q) v += red[threadIdx.x][q];
     out[4 * (int64_t)blockIdx.x + threadIdx.x] = v;
   }
 }
@@ -498,13 +541,13 @@ hipError_t launch_solver_init(const Prob *probs, int32_t nprob, int64_t max_n, h
 }
 
 hipError_t launch_finalize(const Prob *probs, int32_t nprob, double C, double *out, hipStream_t s) {
-  hipLaunchKernelGGL(smo_finalize, dim3((unsigned)nprob), dim3(BS), 0, s, probs, C, out);
+  hipLaunchKernelGGL(smo_finalize, dim3((unsigned)nprob), dim3(FBS), 0, s, probs, C, out);
   return hipGetLastError();
 }
 
-template <int PER, bool GRAM, bool VEC4>
+template <int BS, int PER, bool GRAM, bool VEC4>
 static hipError_t launch_one(const SolveParams &p, int32_t total_wg, size_t shmem, hipStream_t s, int32_t *maxres) {
-  const void *fn = reinterpret_cast<const void *>(&smo_solve<PER, GRAM, VEC4>);
+  const void *fn = reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4>);
   if (shmem > 48 * 1024) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return e;
@@ -523,28 +566,33 @@ static hipError_t launch_one(const SolveParams &p, int32_t total_wg, size_t shme
   return hipLaunchCooperativeKernel(fn, dim3((unsigned)total_wg), dim3(BS), args, (unsigned)shmem, s);
 }
 
-template <bool GRAM, bool VEC4>
-static hipError_t launch_per(const SolveParams &p, int32_t total_wg, int32_t per, size_t shmem, hipStream_t s,
-                             int32_t *maxres) {
-  switch (per) {
-    case 1: return launch_one<1, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
-    case 2: return launch_one<2, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
-    case 4: return launch_one<4, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
-    case 8: return launch_one<8, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
-    case 16: return launch_one<16, GRAM, VEC4>(p, total_wg, shmem, s, maxres);
-    default: return hipErrorInvalidValue;
-  }
-}
-
 hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
                          int32_t *max_coresident) {
-  if (gram) return launch_per<true, false>(p, total_wg, per_thread, 0, s, max_coresident);
+  if (gram) {
+    switch (per_thread) {
+      case 1: return launch_one<BS_GRAM, 1, true, false>(p, total_wg, 0, s, max_coresident);
+      case 2: return launch_one<BS_GRAM, 2, true, false>(p, total_wg, 0, s, max_coresident);
+      case 4: return launch_one<BS_GRAM, 4, true, false>(p, total_wg, 0, s, max_coresident);
+      case 8: return launch_one<BS_GRAM, 8, true, false>(p, total_wg, 0, s, max_coresident);
+      case 16: return launch_one<BS_GRAM, 16, true, false>(p, total_wg, 0, s, max_coresident);
+      default: return hipErrorInvalidValue;
+    }
+  }
   // row path: x_u, x_l, two row slices of per_wg floats, tags
-  const size_t per_wg = (size_t)BS * per_thread;
+  const size_t per_wg = (size_t)BS_ROWS * per_thread;
   const size_t shmem = (2 * (size_t)p.d + 2 * per_wg) * sizeof(float) + (size_t)p.cache_cap * sizeof(int) + 16;
   const bool vec4 = (p.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(p.X) & 15) == 0);
-  if (vec4) return launch_per<false, true>(p, total_wg, per_thread, shmem, s, max_coresident);
-  return launch_per<false, false>(p, total_wg, per_thread, shmem, s, max_coresident);
+  switch (per_thread * 2 + (vec4 ? 1 : 0)) {
+    case 2: return launch_one<BS_ROWS, 1, false, false>(p, total_wg, shmem, s, max_coresident);
+    case 3: return launch_one<BS_ROWS, 1, false, true>(p, total_wg, shmem, s, max_coresident);
+    case 4: return launch_one<BS_ROWS, 2, false, false>(p, total_wg, shmem, s, max_coresident);
+    case 5: return launch_one<BS_ROWS, 2, false, true>(p, total_wg, shmem, s, max_coresident);
+    case 8: return launch_one<BS_ROWS, 4, false, false>(p, total_wg, shmem, s, max_coresident);
+    case 9: return launch_one<BS_ROWS, 4, false, true>(p, total_wg, shmem, s, max_coresident);
+    case 16: return launch_one<BS_ROWS, 8, false, false>(p, total_wg, shmem, s, max_coresident);
+    case 17: return launch_one<BS_ROWS, 8, false, true>(p, total_wg, shmem, s, max_coresident);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace svmx

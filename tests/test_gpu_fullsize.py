@@ -1,0 +1,121 @@
+"""GPU vs oracle at the full sizes of the synthetic workloads, through the C ABI.
+
+The oracle's full-size results are stored in tests/golden/oracle_full_w*.json, written by
+tests/golden/make_oracle_refs.py (which calls only oracle/).  The inputs are regenerated here
+and their digest must equal the one stored with the reference.
+
+Gates (as for the small cases):
+  working set   identical (u, l) for the first 1000 steps, up to the first step whose oracle
+                runner-up gap is below 1e-6 (a tie within the fp32-kernel error of f, where
+                either choice is a maximal violating pair)
+  objective     relative 1e-4
+  decisions     max abs 1e-3 on the stored test points; identical labels where |d| >= 1e-3
+  validity      0 <= a <= C, sum a y = 0, and tol-KKT on sampled rows with f recomputed by the
+                oracle from the GPU's alpha (slack 1e-4 for the fp32 kernel values)
+"""
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2311_14908_amd import svmx, synth
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TIE_GAP = 1e-6
+
+
+def ref(cid):
+    path = os.path.join(GOLDEN, f"oracle_full_w{cid}.json")
+    if not os.path.exists(path):
+        pytest.skip(f"{path} not generated")
+    return json.load(open(path))
+
+
+def digest(*arrays):
+    h = hashlib.sha256()
+    for a in arrays:
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h.hexdigest()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    svmx.load()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_binary_full_size(cid):
+    R = ref(cid)
+    wl = synth.workload(cid)
+    X, y, Xt, _ = synth.generate(cid)
+    nt = len(R["test_decisions"])
+    assert digest(X, y, Xt[:nt]) == R["inputs_sha256"], "inputs differ from the stored reference"
+    Xd, yd = dev(X), dev(y)
+    out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, trace_len=1000)
+    assert out.status == svmx.SVM_OK
+    st = out.stats
+    print(f"\nworkload {cid}: gpu {st['iterations']} steps W={st['dual_obj']:.9f} b={out.b:.6f}; "
+          f"oracle {R['iterations']} steps W={R['dual_obj']:.9f} b={R['b']:.6f}")
+
+    # working-set sequence
+    gaps = np.array(R["trace_gap_min"])
+    tied = np.flatnonzero(gaps[1:] < TIE_GAP)
+    k = min(len(R["trace_ul"]), 1000, (int(tied[0]) + 1) if tied.size else 1000)
+    np.testing.assert_array_equal(out.trace_ul[:k], np.array(R["trace_ul"])[:k])
+
+    # objective and decisions
+    assert abs(st["dual_obj"] - R["dual_obj"]) <= 1e-4 * abs(R["dual_obj"])
+    d_gpu = svmx.svm_predict(Xd, yd, out.alpha, out.b, wl.gamma, dev(Xt[:nt])).cpu().numpy()
+    d_ref = np.array(R["test_decisions"])
+    err = np.max(np.abs(d_gpu - d_ref))
+    print(f"max |d_gpu - d_oracle| = {err:.2e}")
+    assert err <= 1e-3
+    sure = np.abs(d_ref) >= 1e-3
+    assert np.array_equal(d_gpu[sure] > 0, d_ref[sure] > 0)
+
+    # validity of the GPU solution, checked by the oracle
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= wl.C)
+    assert abs(float(a @ y)) <= 1e-9 * wl.C * len(y)
+    rows = np.random.default_rng(cid).choice(len(y), 128, replace=False)
+    f = oracle.f_from_alpha(X, y, a, wl.gamma, rows=rows)
+    ar, yr = a[rows], y[rows]
+    up = ((yr > 0) & (ar < wl.C)) | ((yr < 0) & (ar > 0))
+    low = ((yr > 0) & (ar > 0)) | ((yr < 0) & (ar < wl.C))
+    slack = 1e-4
+    assert np.all(f[up] >= out.b - wl.tol / 2 - slack)
+    assert np.all(f[low] <= out.b + wl.tol / 2 + slack)
+
+
+def test_ovo_full_size():
+    R = ref(4)
+    wl = synth.workload(4)
+    k = wl.classes
+    X, lab, Xt, _ = synth.generate(4)
+    nt = len(R["test_pred"])
+    assert digest(X, lab, Xt[:nt]) == R["inputs_sha256"], "inputs differ from the stored reference"
+    Xd, ld = dev(X), dev(lab)
+    out = svmx.svm_train_ovo(Xd, ld, k, wl.C, wl.gamma, wl.tol)
+    assert out.status == svmx.SVM_OK
+    for p, rp in enumerate(R["pairs"]):
+        assert abs(out.stats[p]["dual_obj"] - rp["dual_obj"]) <= 1e-4 * abs(rp["dual_obj"])
+    dec, pred = svmx.svm_predict_ovo(Xd, ld, k, out.alpha, out.b, wl.gamma, dev(Xt[:nt]))
+    d_ref = np.array(R["test_decisions"])
+    dec = dec.cpu().numpy()
+    err = np.max(np.abs(dec - d_ref))
+    print(f"\none-vs-one: max |d_gpu - d_oracle| = {err:.2e}")
+    assert err <= 1e-3
+    sure = np.all(np.abs(d_ref) >= 1e-3, axis=1)
+    assert np.array_equal(pred.cpu().numpy()[sure], np.array(R["test_pred"])[sure])
