@@ -38,6 +38,7 @@ def main():
     ap.add_argument("--gram", choices=["auto", "on", "off"], default="auto")
     ap.add_argument("--row-path-steps", type=int, default=4000, help="SMO steps of the row-path measurement (0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time (0 = skip)")
+    ap.add_argument("--no-ovo", action="store_true", help="skip the one-vs-one measurement (60000x784, 10 classes)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
@@ -134,6 +135,32 @@ def main():
         result["row_path"] = {"kernel": "smo_solve (row path)", "bound": "hbm", "smo_steps": s["iterations"],
                               "iters_per_s": s["iterations"] / s["t_kernel"], "bytes_per_step": rb,
                               "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS}
+
+    if not args.no_ovo:
+        wo = synth.workload(4)
+        Xo, lo, Xto, lto = synth.generate(4)
+        Xod, lod, Xtod = (torch.from_numpy(a).cuda() for a in (Xo, lo, Xto))
+        svmx.svm_train_ovo(Xod, lod, wo.classes, wo.C, wo.gamma, wo.tol)  # warm-up
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        oo = svmx.svm_train_ovo(Xod, lod, wo.classes, wo.C, wo.gamma, wo.tol)
+        torch.cuda.synchronize()
+        t_train = time.perf_counter() - t1
+        t1 = time.perf_counter()
+        _, pred = svmx.svm_predict_ovo(Xod, lod, wo.classes, oo.alpha, oo.b, wo.gamma, Xtod)
+        torch.cuda.synchronize()
+        t_pred = time.perf_counter() - t1
+        it = sum(p["iterations"] for p in oo.stats)
+        no = Xo.shape[0]
+        result["ovo"] = {"workload": f"{wo.name}: {wo.classes}-class one-vs-one RBF-SVM, 45 pairs, C={wo.C:g}, "
+                                     f"gamma={wo.gamma:g}, tol={wo.tol:g}",
+                         "train_seconds": t_train, "smo_iterations": it, "iters_per_s": it / t_train,
+                         "gram_seconds": oo.stats[0]["t_gram"],
+                         "gram_tflops": float(no) * no * Xo.shape[1] / oo.stats[0]["t_gram"] / 1e12,
+                         "solver_kernel_seconds": oo.stats[0]["t_kernel"], "predict_seconds": t_pred,
+                         "test_accuracy": float(np.mean(pred.cpu().numpy() == lto))}
+        del Xod, lod, Xtod, oo
+        torch.cuda.empty_cache()
 
     if args.cpu_seconds > 0:
         import oracle

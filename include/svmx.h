@@ -72,8 +72,9 @@ typedef struct {
   double *trace_b;           /* host [2*trace_len]: (b_up, b_low) of each step, or NULL */
   double *f_out;             /* device [n]: final f, or NULL (binary training only) */
   void *stream;              /* hipStream_t, or NULL */
-  int32_t workgroups;        /* solver workgroups per binary problem; 0 = automatic */
-  int32_t reserved;
+  int32_t workgroups;        /* solver workgroups per problem; 0 = automatic */
+  int32_t exchange_levels;   /* levels of the cross-workgroup exchange: 1, 2, or 0 = automatic
+                                (two levels above 128 workgroups per problem) */
 } svm_options;
 
 typedef struct {

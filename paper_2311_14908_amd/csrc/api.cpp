@@ -66,6 +66,7 @@ struct Opts {
   double *f_out;
   hipStream_t stream;
   int32_t workgroups;
+  int32_t levels;
 };
 
 bool resolve(const svm_options *o, int64_t n, Opts *r) {
@@ -84,7 +85,8 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
   r->f_out = o->f_out;
   r->stream = reinterpret_cast<hipStream_t>(o->stream);
   r->workgroups = std::max<int32_t>(0, o->workgroups);
-  return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF;
+  r->levels = o->exchange_levels;
+  return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF && r->levels >= 0 && r->levels <= 2;
 }
 
 // How a problem of n samples is spread over workgroups.
@@ -92,20 +94,22 @@ struct Shape {
   int32_t nwg, per_wg, per_thread, g1, ng;
 };
 
-constexpr int32_t TWO_LEVEL_ABOVE = 64;  // workgroups per problem above which the exchange has two levels
+constexpr int32_t TWO_LEVEL_ABOVE = 128;  // workgroups per problem above which the exchange has two levels
 
 // Gram path: one workgroup up to 4096 samples (no exchange at all), else about sqrt(n)/3.5
-// workgroups -- the measured optimum between per-workgroup work and exchange cost on MI355X
-// (40 at n = 20,000, 64 at 50,000, 90 at 100,000).  Row path: up to 256 workgroups of 512
+// workgroups, at most 64 -- the measured optimum between per-workgroup work and exchange
+// cost on MI355X (40 at n = 20,000, 64 at 50,000 and 100,000).  Row path: up to 256 workgroups of 512
 // threads (at least 64 samples each), so that the streaming of X keeps every CU busy.  `cap` bounds the count
 // (one-vs-one runs all pairs in one launch, so their workgroups must fit together).
-bool choose_shape(int64_t n, bool gram, int32_t requested, Shape *s, int64_t cap = 256) {
+bool choose_shape(int64_t n, bool gram, int32_t requested, int32_t levels, Shape *s, int64_t cap = 256) {
   const int64_t BS = solver_block_size(gram), MAXP = max_per_thread(gram);
   int64_t nwg;
   if (requested > 0)
     nwg = requested;
   else if (gram)
-    nwg = n <= 4096 ? 1 : std::min<int64_t>(cap, std::max<int64_t>(8, (int64_t)std::ceil(std::sqrt((double)n) / 3.5)));
+    nwg = n <= 4096 ? 1
+                    : std::min<int64_t>(std::min<int64_t>(cap, 64),
+                                        std::max<int64_t>(8, (int64_t)std::ceil(std::sqrt((double)n) / 3.5)));
   else
     nwg = std::min<int64_t>(cap, std::max<int64_t>(1, (n + 63) / 64));
   nwg = std::max<int64_t>(1, std::min<int64_t>(nwg, n));
@@ -118,7 +122,7 @@ bool choose_shape(int64_t n, bool gram, int32_t requested, Shape *s, int64_t cap
   s->nwg = (int32_t)nwg;
   s->per_wg = (int32_t)per_wg;
   s->per_thread = (int32_t)p;
-  if (nwg > TWO_LEVEL_ABOVE) {
+  if (nwg > 1 && (levels == 2 || (levels == 0 && nwg > TWO_LEVEL_ABOVE))) {
     s->g1 = (int32_t)std::ceil(std::sqrt((double)nwg));
     s->ng = (int32_t)((nwg + s->g1 - 1) / s->g1);
   } else {
@@ -161,15 +165,14 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   else
     p->gram = gram_bytes <= (double)o.gram_budget;
   if (p->gram && gram_bytes > 9.0e18) return fail(SVM_ENOMEM, "Gram size overflows");
-  if (!choose_shape(n, p->gram, o.workgroups, &p->shape)) return fail(SVM_ENOMEM, "problem too large to place");
+  if (!choose_shape(n, p->gram, o.workgroups, o.levels, &p->shape))
+    return fail(SVM_ENOMEM, "problem too large to place");
   p->cache_cap = 0;
   if (!p->gram) {
     if (o.row_cache_bytes > 0)
       p->cache_cap = (int32_t)std::min<int64_t>(CACHE_CAP_MAX, std::min<int64_t>(n, o.row_cache_bytes / (4 * p->ld)));
-    const int64_t lds = (2 * d + 2 * (int64_t)p->shape.per_wg) * 4 + 4LL * p->cache_cap + 64 + 4096;
-    if (lds > LDS_BYTES)
-      return fail(SVM_EINVAL, "row path: d=%lld does not fit the 160 KiB LDS of a workgroup; use the Gram path",
-                  (long long)d);
+    const int64_t lds = 2LL * solver_block_size(false) * p->shape.per_thread * 4 + 4LL * p->cache_cap + 8192;
+    if (lds > LDS_BYTES) return fail(SVM_EINVAL, "row path: row slices and cache tags do not fit the LDS");
   }
   Layout L;
   p->off_f = L.add(8 * n);
@@ -292,10 +295,6 @@ svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) 
   p->ld = round_up(n, 64);
   const double gram_bytes = 4.0 * (double)n * (double)p->ld;
   p->gram = o.gram == SVM_GRAM_ON || (o.gram == SVM_GRAM_AUTO && gram_bytes <= (double)o.gram_budget);
-  if (!p->gram) {
-    const int64_t lds = (2 * d + 2 * (int64_t)solver_block_size(false) * max_per_thread(false)) * 4 + 4096;
-    if (lds > LDS_BYTES) return fail(SVM_EINVAL, "row path: d=%lld does not fit LDS", (long long)d);
-  }
   Layout L;
   p->off_perm = L.add(4 * n);
   p->off_xs = L.add(4 * n * d);
@@ -567,7 +566,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
       P.ctl = ctl + q;
       Shape sh;
       const int64_t cap = std::max<int64_t>(1, OVO_TOTAL_WG / p.P);
-      if (!choose_shape(P.n, p.gram, r.workgroups, &sh, cap) || sh.nwg > OVO_MAX_WG_PER_PAIR)
+      if (!choose_shape(P.n, p.gram, r.workgroups, r.levels, &sh, cap) || sh.nwg > OVO_MAX_WG_PER_PAIR)
         return fail(SVM_ENOMEM, "pair (%d,%d) too large to place", a, bb);
       P.slots = slots + (size_t)q * 2 * OVO_MAX_WG_PER_PAIR * SLOT_WORDS;
       P.g1 = sh.g1;

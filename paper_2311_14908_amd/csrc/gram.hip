@@ -203,7 +203,7 @@ __global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X
 #pragma unroll
     for (int b = 0; b < SB; ++b) xs[b] = X + (j0 + (b < nb ? b : nb - 1)) * d;
     double du[SB], dl[SB];
-    dist2_batch<VEC4, SB>(xs, nb, sx, sx + d, d, lig, gs, du, dl);
+    dist2_batch<VEC4, SB, 4>(xs, nb, sx, sx + d, d, lig, gs, du, dl);
     for (int v = lig; v < 2 * SB; v += gs) {
       const int b = v < SB ? v : v - SB;
       if (b >= nb) continue;

@@ -31,6 +31,7 @@ namespace svmx {
 constexpr int BS_GRAM = 256, MAXP_GRAM = 16;
 constexpr int BS_ROWS = 512, MAXP_ROWS = 8;
 constexpr int ROW_BATCH = 4;  // samples per lane group and batch in the row evaluation
+constexpr int ROW_MAXM = 4;   // feature positions per lane whose loads are issued together
 constexpr int IBIG = 0x7fffffff;
 
 int solver_block_size(bool gram) { return gram ? BS_GRAM : BS_ROWS; }
@@ -285,8 +286,8 @@ __device__ __forceinline__ void consider(Sel &s, double f, double a, int y, int 
 template <int BS, int PER, bool GRAM, bool VEC4>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   constexpr int NW = BS / 64;
-  constexpr int SB = ROW_BATCH;
-  extern __shared__ float4 dyn4[];  // row path: x_u[d], x_l[d], krow[2][per_wg], tags[cap]
+  constexpr int SB = PER == 1 ? ROW_BATCH : 2;  // a sample's arithmetic does not depend on SB
+  extern __shared__ float4 dyn4[];  // row path: krow[2][per_wg], tags[cap]
   float *dyn = reinterpret_cast<float *>(dyn4);
   __shared__ SelLds<NW> sh;
   __shared__ int s_abort;
@@ -319,8 +320,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
     }
   }
 
-  float *sxu = dyn, *sxl = dyn + p.d;
-  float *krow = dyn + 2 * p.d;  // [2][per_wg]
+  float *krow = dyn;  // [2][per_wg]
   int *tags = reinterpret_cast<int *>(krow + 2 * (int64_t)P.per_wg);
   const bool use_cache = !GRAM && p.cache != nullptr && p.cache_cap > 0;
   if (use_cache) {
@@ -391,11 +391,9 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       const int lig = threadIdx.x & (gs - 1);
       const int ngroups = BS / gs;
       const int grp = threadIdx.x / gs;
+      // x_u and x_l are read by every group straight from global memory (L2-resident after
+      // the first touch), so the loads of the rows overlap those of the samples.
       const float *xu = p.X + gu * d, *xl = p.X + gl * d;
-      for (int64_t k = threadIdx.x; k < d; k += BS) {
-        sxu[k] = xu[k];
-        sxl[k] = xl[k];
-      }
       int su = -1, sl = -1;
       bool hit_u = false, hit_l = false;
       if (use_cache) {
@@ -404,12 +402,11 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         hit_u = tags[su] == (int)gu;
         hit_l = tags[sl] == (int)gl;
       }
-      __syncthreads();
-      // K_ul: x_l as the sample against the staged x_u, exactly as the row of u evaluates it
+      // K_ul: x_l as the sample against x_u, exactly as the row of u evaluates sample l
       if (grp == 0) {
-        const float *xs1[1] = {sxl};
+        const float *xs1[1] = {xl};
         double du1[1], dl1[1];
-        dist2_batch<VEC4, 1>(xs1, 1, sxu, sxu, d, lig, gs, du1, dl1);
+        dist2_batch<VEC4, 1, ROW_MAXM>(xs1, 1, xu, xu, d, lig, gs, du1, dl1);
         if (lig == 0) s_kul = (double)rbf_of(du1[0], p.gamma);
       }
       if (!(hit_u && hit_l)) {
@@ -420,7 +417,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
 #pragma unroll
           for (int b = 0; b < SB; ++b) xs[b] = p.X + gmap(P, base + q0 + min(b, nb - 1)) * d;
           double du[SB], dl[SB];
-          dist2_batch<VEC4, SB>(xs, nb, sxu, sxl, d, lig, gs, du, dl);
+          dist2_batch<VEC4, SB, ROW_MAXM>(xs, nb, xu, xl, d, lig, gs, du, dl);
           for (int v = lig; v < 2 * SB; v += gs) {
             const int b = v < SB ? v : v - SB;
             if (b < nb) krow[(v < SB ? 0 : P.per_wg) + q0 + b] = rbf_of(batch_value<SB>(du, dl, v), p.gamma);
@@ -578,9 +575,9 @@ hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thr
       default: return hipErrorInvalidValue;
     }
   }
-  // row path: x_u, x_l, two row slices of per_wg floats, tags
+  // row path: two row slices of per_wg floats, tags
   const size_t per_wg = (size_t)BS_ROWS * per_thread;
-  const size_t shmem = (2 * (size_t)p.d + 2 * per_wg) * sizeof(float) + (size_t)p.cache_cap * sizeof(int) + 16;
+  const size_t shmem = 2 * per_wg * sizeof(float) + (size_t)p.cache_cap * sizeof(int) + 16;
   const bool vec4 = (p.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(p.X) & 15) == 0);
   switch (per_thread * 2 + (vec4 ? 1 : 0)) {
     case 2: return launch_one<BS_ROWS, 1, false, false>(p, total_wg, shmem, s, max_coresident);

@@ -32,7 +32,8 @@ class svm_options(C.Structure):
     _fields_ = [("struct_size", C.c_int32), ("gram", C.c_int32), ("gram_budget_bytes", C.c_int64),
                 ("row_cache_bytes", C.c_int64), ("max_iter", C.c_int64), ("check_every", C.c_int32),
                 ("trace_len", C.c_int32), ("trace_ws", C.POINTER(C.c_int32)), ("trace_b", C.POINTER(C.c_double)),
-                ("f_out", C.c_void_p), ("stream", C.c_void_p), ("workgroups", C.c_int32), ("reserved", C.c_int32)]
+                ("f_out", C.c_void_p), ("stream", C.c_void_p), ("workgroups", C.c_int32),
+                ("exchange_levels", C.c_int32)]
 
 
 class svm_stats(C.Structure):
@@ -105,7 +106,7 @@ def _dev(t: torch.Tensor, dtype, name):
 
 
 def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, check_every=0, trace_len=0,
-            workgroups=0, f_out: torch.Tensor | None = None, stream=None):
+            workgroups=0, exchange_levels=0, f_out: torch.Tensor | None = None, stream=None):
     o = svm_options()
     load().svm_default_options(C.byref(o))
     o.gram = gram
@@ -116,6 +117,7 @@ def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, 
         o.check_every = check_every
     o.trace_len = trace_len
     o.workgroups = workgroups
+    o.exchange_levels = exchange_levels
     o.f_out = None if f_out is None else f_out.data_ptr()
     s = stream if stream is not None else torch.cuda.current_stream()
     o.stream = s.cuda_stream
