@@ -332,6 +332,27 @@ svm_status class_sort(const int32_t *label, int64_t n, int32_t k, hipStream_t st
   return SVM_OK;
 }
 
+// Layout of the prediction scratch for up to ntr training samples and m test samples.
+int64_t predict_scratch_bytes(int64_t ntr, int64_t m) {
+  Layout L;
+  L.add(4 * ntr);
+  L.add(8 * ntr);
+  L.add(8);
+  L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1));
+  return round_up(L.total, ALIGN);
+}
+
+PredictScratch predict_scratch(void *base, int64_t ntr, int64_t m) {
+  Layout L;
+  char *b = static_cast<char *>(base);
+  PredictScratch s;
+  s.sv_row = reinterpret_cast<int32_t *>(b + L.add(4 * ntr));
+  s.sv_coef = reinterpret_cast<double *>(b + L.add(8 * ntr));
+  s.count = reinterpret_cast<int64_t *>(b + L.add(8));
+  s.part = reinterpret_cast<double *>(b + L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1)));
+  return s;
+}
+
 }  // namespace
 
 // ============================================================================ C ABI
@@ -482,25 +503,27 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
 }
 
 int64_t svm_predict_workspace_bytes(int64_t n, int64_t d, int64_t m) {
-  if (n < 1 || d < 1 || m < 0) return -1;
-  return ALIGN;
+  if (n < 1 || d < 1 || m < 0 || n > 0x7ffffffeLL || m > (INT64_MAX / 8) / 64 / std::max<int64_t>(n, 1)) return -1;
+  return predict_scratch_bytes(n, m);
 }
 
 svm_status svm_predict(const float *X_train, const int32_t *y, const double *alpha, double b, int64_t n, int64_t d,
                        double gamma, const float *X_test, int64_t m, double *dec, void *workspace,
                        int64_t workspace_bytes, const svm_options *o) {
   g_err.clear();
-  (void)workspace;
-  (void)workspace_bytes;
   if (n < 1 || d < 1 || m < 0) return fail(SVM_EINVAL, "need n >= 1, d >= 1, m >= 0");
   if (!X_train || !y || !alpha || (m > 0 && (!X_test || !dec))) return fail(SVM_EINVAL, "NULL pointer argument");
   if (!finite_pos(gamma) || !std::isfinite(b)) return fail(SVM_EINVAL, "gamma must be finite and > 0, b finite");
-  if (d > (INT64_MAX / 8) / std::max<int64_t>(n, m)) return fail(SVM_ENOMEM, "sizes overflow");
-  if ((int64_t)8 * 4 * d > LDS_BYTES) return fail(SVM_EINVAL, "d=%lld too large for the staged test tile", (long long)d);
+  if (n > 0x7ffffffeLL || d > (INT64_MAX / 8) / std::max<int64_t>(n, m)) return fail(SVM_ENOMEM, "sizes overflow");
   Opts r;
   if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options");
   if (m == 0) return SVM_OK;
-  HIPCHK(launch_predict_map(X_train, d, 0, n, n, y, nullptr, alpha, n, gamma, X_test, m, b, dec, 1, r.stream));
+  const int64_t need = svm_predict_workspace_bytes(n, d, m);
+  if (need < 0) return fail(SVM_ENOMEM, "sizes overflow");
+  if (!workspace || workspace_bytes < need)
+    return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)need, (long long)workspace_bytes);
+  const PredictScratch ps = predict_scratch(workspace, n, m);
+  HIPCHK(launch_predict_map(X_train, d, 0, n, n, y, nullptr, alpha, n, gamma, X_test, m, b, dec, 1, ps, r.stream));
   HIPCHK(hipStreamSynchronize(r.stream));
   return SVM_OK;
 }
@@ -648,8 +671,8 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
 }
 
 int64_t svm_predict_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, int64_t m) {
-  if (n < 2 || d < 1 || k < 2 || k > MAX_CLASSES || m < 0) return -1;
-  return round_up(4 * n, ALIGN);
+  if (n < 2 || d < 1 || k < 2 || k > MAX_CLASSES || m < 0 || n > 0x7ffffffeLL) return -1;
+  return round_up(4 * n, ALIGN) + predict_scratch_bytes(n, m);
 }
 
 svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k,
@@ -661,7 +684,6 @@ svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int6
   if (k < 2 || k > MAX_CLASSES) return fail(SVM_EINVAL, "k=%d must be in [2, %d]", k, MAX_CLASSES);
   if (!X || !label || !alpha || !b || (m > 0 && (!X_test || !dec || !pred))) return fail(SVM_EINVAL, "NULL pointer");
   if (!finite_pos(gamma)) return fail(SVM_EINVAL, "gamma must be finite and > 0");
-  if ((int64_t)8 * 4 * d > LDS_BYTES) return fail(SVM_EINVAL, "d too large for the staged test tile");
   Opts r;
   if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options");
   const int64_t need = svm_predict_ovo_workspace_bytes(n, d, k, m);
@@ -675,6 +697,7 @@ svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int6
   if (s0 != SVM_OK) return s0;
   if (m == 0) return SVM_OK;
   int32_t *dperm = static_cast<int32_t *>(workspace);
+  const PredictScratch ps = predict_scratch(static_cast<char *>(workspace) + round_up(4 * n, ALIGN), n, m);
   HIPCHK(hipMemcpyAsync(dperm, perm.data(), 4 * n, hipMemcpyHostToDevice, r.stream));
   int64_t pack = 0;
   int32_t q = 0;
@@ -682,7 +705,7 @@ svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int6
     for (int32_t bb = a + 1; bb < k; ++bb, ++q) {
       const int64_t np = cnt[a] + cnt[bb];
       HIPCHK(launch_predict_map(X, d, start[a], cnt[a], start[bb], nullptr, dperm, alpha + pack, np, gamma, X_test, m,
-                                b[q], dec + q, P, r.stream));
+                                b[q], dec + q, P, ps, r.stream));
       pack += np;
     }
   HIPCHK(launch_ovo_vote(dec, m, k, pred, r.stream));

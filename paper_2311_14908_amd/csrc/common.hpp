@@ -74,11 +74,20 @@ hipError_t launch_solver_init(const Prob *probs, int32_t nprob, int64_t max_n, h
 hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
                          int32_t *max_coresident);
 hipError_t launch_finalize(const Prob *probs, int32_t nprob, double C, double *out /*[nprob][4]*/, hipStream_t s);
+// Device scratch of one prediction: compacted support vectors and per-split partial sums.
+struct PredictScratch {
+  int32_t *sv_row;  // [ntr]
+  double *sv_coef;  // [ntr]
+  int64_t *count;   // [1]
+  double *part;     // [predict_splits(m, ntr)][m]
+};
+int predict_splits(int64_t m, int64_t nsv_max);
 // Decision values for training samples addressed like Prob (local j -> row off0+j or
 // off1+j-len0, then through perm when perm != NULL); labels from y by that row, or by range.
 hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t len0, int64_t off1,
                               const int32_t *y, const int32_t *perm, const double *alpha, int64_t ntr, double gamma,
-                              const float *T, int64_t m, double b, double *dec, int64_t dec_stride, hipStream_t s);
+                              const float *T, int64_t m, double b, double *dec, int64_t dec_stride,
+                              const PredictScratch &ws, hipStream_t s);
 hipError_t launch_ovo_vote(const double *dec, int64_t m, int32_t k, int32_t *pred, hipStream_t s);
 
 int solver_block_size(bool gram);

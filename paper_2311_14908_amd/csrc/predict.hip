@@ -1,17 +1,26 @@
 // predict.hip -- decision values d(x) = sum_{a_i>0} a_i y_i K(x_i, x) - b and one-vs-one votes.
 //
-// A workgroup stages TQ test samples in LDS and streams the training samples past them: a
-// group of lanes takes one training sample with a_i > 0, accumulates its squared distance to
-// each staged test sample in fp64, and adds a_i y_i exp(-gamma d^2) into per-group fp64 sums;
-// the group sums are then combined in a fixed order, so results are deterministic.
+// 1. sv_compact: the support vectors (a_i > 0) in increasing local index, as rows of X with
+//    coefficient a_i y_i (one workgroup, ballot prefix sums; deterministic order).
+// 2. predict_mfma: 128 test samples x 128 support vectors per tile; the dot products run on
+//    v_mfma_f32_16x16x4f32 (fp32 in, fp32 accumulate), norms come from the same LDS slabs,
+//    K = exp2(c * max(0, |t|^2 + |x|^2 - 2 t.x)) with c = -gamma log2(e), and each test row
+//    sums coef * K in fp64 over the tile in a fixed tree.  Support-vector tiles are split
+//    over `nsplit` workgroups per test tile; each split writes its own partial sums.
+// 3. predict_final: dec = sum over splits (fixed order) - b.
+// Results are deterministic: no atomics touch values.
 #include "common.hpp"
 
 #include <math.h>
 
 namespace svmx {
 
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int PT = 128;        // tile edge
+constexpr int PKC = 16;        // k per LDS stage
+constexpr int PPAD = PT + 16;  // LDS pitch (conflict-free operand reads)
 constexpr int PBS = 256;
-constexpr int TQ = 8;
 
 struct PredMap {  // local training index j -> row of X, and its label
   int64_t off0, len0, off1;
@@ -19,94 +28,223 @@ struct PredMap {  // local training index j -> row of X, and its label
   const int32_t *perm;  // sorted position -> row of X, or NULL (identity)
 };
 
-__device__ __forceinline__ int64_t pm_row(const PredMap &m, int64_t j) {
-  const int64_t r = j < m.len0 ? m.off0 + j : m.off1 + (j - m.len0);
-  return m.perm ? (int64_t)m.perm[r] : r;
-}
-__device__ __forceinline__ double pm_label(const PredMap &m, int64_t j) {
-  return m.y ? (double)m.y[pm_row(m, j)] : (j < m.len0 ? 1.0 : -1.0);
+__device__ __forceinline__ int64_t pm_pos(const PredMap &m, int64_t j) { return j < m.len0 ? m.off0 + j : m.off1 + (j - m.len0); }
+
+// One workgroup of 1024 threads: stable compaction of the samples with a > 0.
+__global__ void __launch_bounds__(1024) sv_compact_k(const double *__restrict__ alpha, int64_t n, PredMap map,
+                                                     int32_t *__restrict__ sv_row, double *__restrict__ sv_coef,
+                                                     int64_t *__restrict__ count) {
+  __shared__ int wave_cnt[16];
+  __shared__ int64_t s_base;
+  if (threadIdx.x == 0) s_base = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int64_t c0 = 0; c0 < n; c0 += 1024) {
+    const int64_t j = c0 + threadIdx.x;
+    const double a = j < n ? alpha[j] : 0.0;
+    const bool sv = a > 0.0;
+    const unsigned long long mask = __ballot(sv);
+    const int before = __popcll(mask & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_cnt[w] = __popcll(mask);
+    __syncthreads();
+    int off = 0;
+    for (int q = 0; q < w; ++q) off += wave_cnt[q];
+    int tot = 0;
+    for (int q = 0; q < 16; ++q) tot += wave_cnt[q];
+    if (sv) {
+      const int64_t pos = pm_pos(map, j);
+      const int64_t row = map.perm ? (int64_t)map.perm[pos] : pos;
+      const double y = map.y ? (double)map.y[row] : (j < map.len0 ? 1.0 : -1.0);
+      const int64_t dst = s_base + off + before;
+      sv_row[dst] = (int32_t)row;
+      sv_coef[dst] = a * y;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) s_base += tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *count = s_base;
 }
 
-template <int GS>
-__global__ void __launch_bounds__(PBS) predict_k(const float *__restrict__ Xtr, int64_t d, PredMap map,
-                                                 const double *__restrict__ alpha, int64_t ntr, double gamma,
-                                                 const float *__restrict__ T, int64_t m, double b, double *dec,
-                                                 int64_t dec_stride) {
-  extern __shared__ float4 st4[];  // [TQ][d]
-  float *st = reinterpret_cast<float *>(st4);
-  __shared__ double part[PBS / GS][TQ];
-  const int64_t q0 = (int64_t)blockIdx.x * TQ;
-  const int nq = (int)(m - q0 < TQ ? m - q0 : TQ);
-  for (int64_t e = threadIdx.x; e < (int64_t)TQ * d; e += PBS) {
-    const int64_t q = e / d, k = e - q * d;
-    st[e] = q < nq ? T[(q0 + q) * d + k] : 0.f;
-  }
-  __syncthreads();
-  const int lig = threadIdx.x % GS, grp = threadIdx.x / GS;
-  constexpr int NG = PBS / GS;
-  double acc[TQ];
+// Load 128 rows x 16 columns into LDS transposed to [k][row] and add the squares into the
+// thread's norm partials (thread t: rows t/4 and 64 + t/4, columns 4*(t%4) .. +3).  Rows come
+// from `idx` (row numbers of X) when given, else r0.. directly; rows at or past `nrows` are 0.
+template <bool VEC4>
+__device__ __forceinline__ void load_rows(const float *__restrict__ X, const int32_t *__restrict__ idx, int64_t nrows,
+                                          int64_t d, int64_t r0, int64_t k0, float (*S)[PPAD], float nacc[2]) {
+  const int t = threadIdx.x;
+  const int kq = (t & 3) * 4;
 #pragma unroll
-  for (int q = 0; q < TQ; ++q) acc[q] = 0.0;
-  for (int64_t i = grp; i < ntr; i += NG) {
-    const double ai = alpha[i];
-    if (!(ai > 0.0)) continue;
-    const float *xi = Xtr + pm_row(map, i) * d;
-    double ds[TQ];
+  for (int h = 0; h < 2; ++h) {
+    const int row = h * 64 + (t >> 2);
+    const int64_t r = r0 + row;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (r < nrows) {
+      const int64_t xr = idx ? (int64_t)idx[r] : r;
+      const float *src = X + xr * d + k0 + kq;
+      if (VEC4 && k0 + kq + 3 < d) {
+        const float4 q = *reinterpret_cast<const float4 *>(src);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+      } else {
 #pragma unroll
-    for (int q = 0; q < TQ; ++q) ds[q] = 0.0;
-    for (int64_t k = lig; k < d; k += GS) {
-      const double v = (double)xi[k];
-#pragma unroll
-      for (int q = 0; q < TQ; ++q) {
-        const double e = v - (double)st[q * d + k];
-        ds[q] += e * e;
+        for (int e = 0; e < 4; ++e)
+          if (k0 + kq + e < d) v[e] = src[e];
       }
     }
 #pragma unroll
-    for (int q = 0; q < TQ; ++q) {
-      for (int o = GS >> 1; o > 0; o >>= 1) ds[q] += __shfl_xor(ds[q], o);
+    for (int e = 0; e < 4; ++e) {
+      S[kq + e][row] = v[e];
+      nacc[h] += v[e] * v[e];
     }
-    const double coef = ai * pm_label(map, i);
+  }
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+  const long long b = __double_as_longlong(v);
+  const int hi = __builtin_amdgcn_update_dpp((int)(b >> 32), (int)(b >> 32), CTRL, 0xf, 0xf, false);
+  const int lo = __builtin_amdgcn_update_dpp((int)b, (int)b, CTRL, 0xf, 0xf, false);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane of the row gets the same bits.
+__device__ __forceinline__ double row16_sum(double v) {
+  v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_d<0x141>(v);  // row_half_mirror
+  v += dpp_d<0x140>(v);  // row_mirror
+  return v;
+}
+
+template <bool VEC4>
+__global__ void __launch_bounds__(PBS) predict_mfma_k(const float *__restrict__ T, int64_t m, const float *__restrict__ X,
+                                                      const int32_t *__restrict__ sv_row,
+                                                      const double *__restrict__ sv_coef,
+                                                      const int64_t *__restrict__ sv_count, int64_t d, float c,
+                                                      int nsplit, double *__restrict__ part) {
+  __shared__ float As[PKC][PPAD];
+  __shared__ float Bs[PKC][PPAD];
+  __shared__ float nA[PT], nB[PT];
+  __shared__ double cB[PT];
+  __shared__ double rs[2][PT];
+  const int64_t nsv = *sv_count;
+  const int64_t q0 = (int64_t)blockIdx.x * PT;
+  const int split = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  double row_acc = 0.0;  // thread t < 128 owns test row q0 + t
+  const int64_t ntile = (nsv + PT - 1) / PT;
+  for (int64_t st = split; st < ntile; st += nsplit) {
+    const int64_t s0 = st * PT;
+    v4f acc[4][4];
 #pragma unroll
-    for (int q = 0; q < TQ; ++q) acc[q] += coef * exp(-gamma * ds[q]);
-  }
-  if (lig == 0) {
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int q = 0; q < TQ; ++q) part[grp][q] = acc[q];
+      for (int b = 0; b < 4; ++b) acc[a][b] = (v4f){0.f, 0.f, 0.f, 0.f};
+    float na[2] = {0.f, 0.f}, nb[2] = {0.f, 0.f};
+    for (int64_t k0 = 0; k0 < d; k0 += PKC) {
+      load_rows<VEC4>(T, nullptr, m, d, q0, k0, As, na);
+      load_rows<VEC4>(X, sv_row + s0, nsv - s0, d, 0, k0, Bs, nb);
+      __syncthreads();
+#pragma unroll
+      for (int kk = 0; kk < PKC; kk += 4) {
+        float av[4], bv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) av[q] = As[kk + (lane >> 4)][wm * 64 + q * 16 + (lane & 15)];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bv[q] = Bs[kk + (lane >> 4)][wn * 64 + q * 16 + (lane & 15)];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      na[h] += __shfl_xor(na[h], 1);
+      na[h] += __shfl_xor(na[h], 2);
+      nb[h] += __shfl_xor(nb[h], 1);
+      nb[h] += __shfl_xor(nb[h], 2);
+    }
+    if ((threadIdx.x & 3) == 0) {
+      nA[threadIdx.x >> 2] = na[0];
+      nA[64 + (threadIdx.x >> 2)] = na[1];
+      nB[threadIdx.x >> 2] = nb[0];
+      nB[64 + (threadIdx.x >> 2)] = nb[1];
+    }
+    if (threadIdx.x < PT) cB[threadIdx.x] = s0 + threadIdx.x < nsv ? sv_coef[s0 + threadIdx.x] : 0.0;
+    __syncthreads();
+    // per test row: sum over this wave's 64 columns (4 blocks x 16 lanes), then the two halves
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int lr = wm * 64 + a * 16 + 4 * (lane >> 4) + e;
+        double sacc = 0.0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int lc = wn * 64 + b * 16 + (lane & 15);
+          float t = nA[lr] + nB[lc] - 2.0f * acc[a][b][e];
+          t = t > 0.f ? t : 0.f;
+          sacc = __builtin_fma(cB[lc], (double)__builtin_amdgcn_exp2f(c * t), sacc);
+        }
+        sacc = row16_sum(sacc);
+        if ((lane & 15) == 0) rs[wn][lr] = sacc;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < PT) row_acc += rs[0][threadIdx.x] + rs[1][threadIdx.x];
+    __syncthreads();
   }
-  __syncthreads();
-  if (threadIdx.x < nq) {
-    double s = 0.0;
-    for (int g = 0; g < NG; ++g) s += part[g][threadIdx.x];
-    dec[(q0 + threadIdx.x) * dec_stride] = s - b;
-  }
+  if (threadIdx.x < PT && q0 + threadIdx.x < m) part[(int64_t)split * m + q0 + threadIdx.x] = row_acc;
+}
+
+__global__ void predict_final_k(const double *__restrict__ part, int64_t m, int nsplit, double b, double *dec,
+                                int64_t stride) {
+  const int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (q >= m) return;
+  double s = 0.0;
+  for (int k = 0; k < nsplit; ++k) s += part[(int64_t)k * m + q];
+  dec[q * stride] = s - b;
+}
+
+int predict_splits(int64_t m, int64_t nsv_max) {
+  if (m <= 0) return 1;
+  const int64_t row_tiles = (m + PT - 1) / PT;
+  const int64_t sv_tiles = nsv_max > 0 ? (nsv_max + PT - 1) / PT : 1;
+  int64_t s = (512 + row_tiles - 1) / row_tiles;
+  if (s > sv_tiles) s = sv_tiles;
+  if (s > 64) s = 64;
+  if (s < 1) s = 1;
+  return (int)s;
 }
 
 hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t len0, int64_t off1,
                               const int32_t *y, const int32_t *perm, const double *alpha, int64_t ntr, double gamma,
-                              const float *T, int64_t m, double b, double *dec, int64_t dec_stride, hipStream_t s) {
+                              const float *T, int64_t m, double b, double *dec, int64_t dec_stride,
+                              const PredictScratch &ws, hipStream_t s) {
   if (m <= 0) return hipSuccess;
   PredMap map{off0, len0, off1, y, perm};
-  const int64_t blocks = (m + TQ - 1) / TQ;
-  const size_t shmem = (size_t)TQ * d * sizeof(float);
-  int gs = 1;
-  while (gs < d && gs < 64) gs <<= 1;
-  const void *fn;
-  switch (gs) {
-    case 1: fn = reinterpret_cast<const void *>(&predict_k<1>); break;
-    case 2: fn = reinterpret_cast<const void *>(&predict_k<2>); break;
-    case 4: fn = reinterpret_cast<const void *>(&predict_k<4>); break;
-    case 8: fn = reinterpret_cast<const void *>(&predict_k<8>); break;
-    case 16: fn = reinterpret_cast<const void *>(&predict_k<16>); break;
-    case 32: fn = reinterpret_cast<const void *>(&predict_k<32>); break;
-    default: fn = reinterpret_cast<const void *>(&predict_k<64>); break;
-  }
-  if (shmem > 48 * 1024) {
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
-    if (e != hipSuccess) return e;
-  }
-  void *args[] = {(void *)&Xtr, &d, &map, (void *)&alpha, &ntr, &gamma, (void *)&T, &m, &b, &dec, &dec_stride};
-  return hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(PBS), args, shmem, s);
+  hipLaunchKernelGGL(sv_compact_k, dim3(1), dim3(1024), 0, s, alpha, ntr, map, ws.sv_row, ws.sv_coef, ws.count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nsplit = predict_splits(m, ntr);
+  const float c = (float)(-gamma * 1.4426950408889634);
+  dim3 grid((unsigned)((m + PT - 1) / PT), (unsigned)nsplit);
+  const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(T) & 15) == 0) &&
+                    ((reinterpret_cast<uintptr_t>(Xtr) & 15) == 0);
+  if (vec4)
+    hipLaunchKernelGGL(predict_mfma_k<true>, grid, dim3(PBS), 0, s, T, m, Xtr, ws.sv_row, ws.sv_coef, ws.count, d, c,
+                       nsplit, ws.part);
+  else
+    hipLaunchKernelGGL(predict_mfma_k<false>, grid, dim3(PBS), 0, s, T, m, Xtr, ws.sv_row, ws.sv_coef, ws.count, d, c,
+                       nsplit, ws.part);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(predict_final_k, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, ws.part, m, nsplit, b, dec,
+                     dec_stride);
+  return hipGetLastError();
 }
 
 // pred[q] = class with most votes over the k(k-1)/2 pairs (a<b, lexicographic), pair (a,b)

@@ -125,6 +125,16 @@ def test_predict_and_rows_reject():
     assert lib.svm_gram(FAKE, 10, 4, -0.5, FAKE, 10, C.byref(o)) == -1
 
 
+def test_predict_workspace_sizes():
+    lib = svmx.load()
+    for n, m in [(1, 0), (10, 0), (20_000, 0), (20_000, 1), (20_000, 10_000), (100_000, 129)]:
+        w = lib.svm_predict_workspace_bytes(n, 16, m)
+        assert w >= 12 * n + 8
+        assert lib.svm_predict_ovo_workspace_bytes(max(n, 2), 16, 3, m) >= w
+    assert lib.svm_predict_workspace_bytes(0, 16, 5) == -1
+    assert lib.svm_predict_workspace_bytes(10, 16, -1) == -1
+
+
 def test_predict_m0_is_noop():
     lib = svmx.load()
     o = _opts()
