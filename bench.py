@@ -23,6 +23,28 @@ import time
 
 HBM_PEAK_GBPS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+ROOT = os.path.dirname(os.path.abspath(__file__))
+COUNTERS = os.path.join(ROOT, "profiles", "smo_solve_n20000_d784_hbm_counters.md")
+SOLVER_SOURCES = ("paper_2311_14908_amd/csrc/smo.hip", "paper_2311_14908_amd/csrc/rbf_rows.hpp",
+                  "paper_2311_14908_amd/csrc/common.hpp")
+
+
+def counter_bytes_per_step(workload_name):
+    """HBM bytes per SMO step measured with rocprofv3 FETCH_SIZE/WRITE_SIZE (scaled by a copy of
+    known size), as recorded in profiles/; None when missing, for another workload, or when the
+    solver sources changed after the counters were taken."""
+    import hashlib
+    try:
+        line = [l for l in open(COUNTERS) if "solver_sources_sha256" in l][0]
+        rec = json.loads(line.strip())
+    except (OSError, IndexError, ValueError):
+        return None
+    h = hashlib.sha256()
+    for p in SOLVER_SOURCES:
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    if rec.get("solver_sources_sha256") != h.hexdigest() or rec.get("workload") != workload_name:
+        return None
+    return rec
 
 
 def log(*a):
@@ -39,6 +61,8 @@ def main():
     ap.add_argument("--row-path-steps", type=int, default=4000, help="SMO steps of the row-path measurement (0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time (0 = skip)")
     ap.add_argument("--no-ovo", action="store_true", help="skip the one-vs-one measurement (60000x784, 10 classes)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="first run one plain device-to-device copy of BYTES (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
@@ -53,6 +77,13 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     svmx.load()
+    if args.copy_calibration > 0:
+        src = torch.ones(args.copy_calibration // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
     wl = synth.workload(args.workload)
     if wl.classes != 2:
         print("bench.py times the binary workloads (0..3)", file=sys.stderr)
@@ -91,6 +122,10 @@ def main():
     t_kernel = sum(s["t_kernel"] for s in st)
     step_bytes = 25.0 * n
     solver_gbps = step_bytes * iters / t_kernel / 1e9
+    counters = counter_bytes_per_step(wl.name)
+    gram_used = bool(st[0]["gram_used"])
+    traffic = (counters["gram_path_hbm_bytes_per_smo_step"] * iters / launches
+               if counters and gram_used else None)
     gram_flops = float(n) * n * d
     gram_tflops = gram_flops / mean("t_gram") / 1e12 if mean("t_gram") > 0 else None
 
@@ -116,7 +151,7 @@ def main():
         "n_sv": st[-1]["n_sv"], "n_bound_sv": st[-1]["n_bound_sv"], "dual_obj": st[-1]["dual_obj"],
         "test_accuracy": acc,
         "roofline": {"kernel": "smo_solve", "bound": "hbm", "achieved": solver_gbps, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": solver_gbps / HBM_PEAK_GBPS, "traffic": None,
+                     "unit": "GB/s", "frac": solver_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "bytes_per_step": step_bytes, "launch_avg_ms": 1e3 * t_kernel / launches,
                      "us_per_smo_step": 1e6 * t_kernel / iters},
         "gram_build": {"kernel": "gram_rbf_mfma", "bound": "mfma", "flops": gram_flops,
@@ -132,9 +167,12 @@ def main():
         s = r.stats
         rb = 4.0 * n * d + 21.0 * n
         gbps = rb * s["iterations"] / s["t_kernel"] / 1e9
+        rtraffic = (counters["row_path_hbm_bytes_per_smo_step"] * s["iterations"] / s["launches"]
+                    if counters else None)
         result["row_path"] = {"kernel": "smo_solve (row path)", "bound": "hbm", "smo_steps": s["iterations"],
                               "iters_per_s": s["iterations"] / s["t_kernel"], "bytes_per_step": rb,
-                              "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS}
+                              "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS,
+                              "traffic": rtraffic}
 
     if not args.no_ovo:
         wo = synth.workload(4)
