@@ -64,52 +64,77 @@ __device__ __forceinline__ double readlane_d(double v, int lane) {
   return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// One DPP round of the (value, index) reduction of both sides.  Lanes outside ROW_MASK keep
-// their own values (update_dpp with old = src), which the idempotent merge leaves unchanged.
 template <int CTRL, int ROW_MASK>
 __device__ __forceinline__ int dpp_mov(int v) {
   return __builtin_amdgcn_update_dpp(v, v, CTRL, ROW_MASK, 0xf, false);
 }
 
 template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ void dpp_round(double &vu, int &iu, double &vl, int &il) {
-  const long long bu = __double_as_longlong(vu), bl = __double_as_longlong(vl);
-  const unsigned uh = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)(bu >> 32));
-  const unsigned ul = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)bu);
-  const unsigned lh = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)(bl >> 32));
-  const unsigned ll = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)bl);
-  const int oiu = dpp_mov<CTRL, ROW_MASK>(iu), oil = dpp_mov<CTRL, ROW_MASK>(il);
-  const double ou = __longlong_as_double((long long)(((unsigned long long)uh << 32) | ul));
-  const double ol = __longlong_as_double((long long)(((unsigned long long)lh << 32) | ll));
-  if (lt_min(ou, oiu, vu, iu)) { vu = ou; iu = oiu; }
-  if (gt_max(ol, oil, vl, il)) { vl = ol; il = oil; }
+__device__ __forceinline__ double dpp_mov_d(double v) {
+  const long long b = __double_as_longlong(v);
+  const unsigned hi = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)(b >> 32));
+  const unsigned lo = (unsigned)dpp_mov<CTRL, ROW_MASK>((int)b);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// Wave-wide selection, returned to every lane.  The (value, index) pairs are reduced with
-// DPP row operations (xor 1 and 2 inside quads, rotations by 4 and 8 inside rows of 16, then
-// the row-15 and row-31 broadcasts), which leaves the result in lane 63; the multiplier and
-// label of the winner are then read from the lane that holds it.  Must be called by all 64
-// lanes of the wave.
+// Wave-wide min (MAX = false) or max (MAX = true) of v, returned to every lane.  DPP row
+// operations (xor 1 and 2 inside quads, rotations by 4 and 8 inside rows of 16, then the
+// row-15 and row-31 broadcasts) leave the result in lane 63.  Lanes outside a broadcast's row
+// mask keep their own value, which min/max leaves unchanged.
+template <bool MAX>
+__device__ __forceinline__ double wave_extreme(double v) {
+#define SVMX_EXT_ROUND(CTRL, RM)                      \
+  {                                                   \
+    const double o = dpp_mov_d<CTRL, RM>(v);          \
+    v = MAX ? fmax(v, o) : fmin(v, o);                \
+  }
+  SVMX_EXT_ROUND(0xB1, 0xF)   // quad_perm [1,0,3,2]
+  SVMX_EXT_ROUND(0x4E, 0xF)   // quad_perm [2,3,0,1]
+  SVMX_EXT_ROUND(0x124, 0xF)  // row_ror:4
+  SVMX_EXT_ROUND(0x128, 0xF)  // row_ror:8
+  SVMX_EXT_ROUND(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
+  SVMX_EXT_ROUND(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
+#undef SVMX_EXT_ROUND
+  return readlane_d(v, 63);
+}
+
+// Wave-wide min of an int, returned to every lane (same DPP pattern).
+__device__ __forceinline__ int wave_min_int(int v) {
+  v = min(v, dpp_mov<0xB1, 0xF>(v));
+  v = min(v, dpp_mov<0x4E, 0xF>(v));
+  v = min(v, dpp_mov<0x124, 0xF>(v));
+  v = min(v, dpp_mov<0x128, 0xF>(v));
+  v = min(v, dpp_mov<0x142, 0xA>(v));
+  v = min(v, dpp_mov<0x143, 0xC>(v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
+// Winner of one side: the extreme value, then the smallest index among the lanes holding it
+// (an index reduction runs only when several lanes tie), then value, index, multiplier and label
+// read from that lane.  This is the (value, index) lexicographic order: -0 and +0 compare equal.
+template <bool MAX>
+__device__ __forceinline__ void side_winner(double v, int i, double a, int y, double &rv, int &ri, double &ra,
+                                            int &ry) {
+  rv = wave_extreme<MAX>(v);
+  const unsigned long long tie = (unsigned long long)__ballot(v == rv);
+  int lane;
+  if (__popcll(tie) == 1) {
+    lane = __ffsll(tie) - 1;
+  } else {
+    const int best = wave_min_int(v == rv ? i : IBIG);
+    lane = __ffsll((unsigned long long)__ballot(v == rv && i == best)) - 1;
+  }
+  rv = readlane_d(v, lane);  // the winner's own value (its sign of zero included)
+  ri = __builtin_amdgcn_readlane(i, lane);
+  ra = readlane_d(a, lane);
+  ry = __builtin_amdgcn_readlane(y, lane);
+}
+
+// Wave-wide selection, returned to every lane.  Must be called by all 64 lanes of the wave.
 __device__ __forceinline__ Sel sel_wave(const Sel &mine) {
-  double vu = mine.vu, vl = mine.vl;
-  int iu = mine.iu, il = mine.il;
-  dpp_round<0xB1, 0xF>(vu, iu, vl, il);   // quad_perm [1,0,3,2]
-  dpp_round<0x4E, 0xF>(vu, iu, vl, il);   // quad_perm [2,3,0,1]
-  dpp_round<0x124, 0xF>(vu, iu, vl, il);  // row_ror:4
-  dpp_round<0x128, 0xF>(vu, iu, vl, il);  // row_ror:8
-  dpp_round<0x142, 0xA>(vu, iu, vl, il);  // row_bcast:15 -> rows 1, 3
-  dpp_round<0x143, 0xC>(vu, iu, vl, il);  // row_bcast:31 -> rows 2, 3
   Sel r;
-  r.vu = readlane_d(vu, 63);
-  r.iu = __builtin_amdgcn_readlane(iu, 63);
-  r.vl = readlane_d(vl, 63);
-  r.il = __builtin_amdgcn_readlane(il, 63);
-  const int lu = __ffsll((unsigned long long)__ballot(mine.iu == r.iu)) - 1;
-  const int ll = __ffsll((unsigned long long)__ballot(mine.il == r.il)) - 1;
-  r.au = readlane_d(mine.au, lu);
-  r.yu = __builtin_amdgcn_readlane(mine.yu, lu);
-  r.al = readlane_d(mine.al, ll);
-  r.yl = __builtin_amdgcn_readlane(mine.yl, ll);
+  side_winner<false>(mine.vu, mine.iu, mine.au, mine.yu, r.vu, r.iu, r.au, r.yu);
+  side_winner<true>(mine.vl, mine.il, mine.al, mine.yl, r.vl, r.il, r.al, r.yl);
   return r;
 }
 
