@@ -85,7 +85,9 @@ typedef struct {
   double dual_obj;      /* W(a) = 1/2 sum a - 1/2 sum a y f */
   int32_t gram_used;    /* 1 if the full Gram was precomputed */
   int32_t launches;     /* solver launches (host convergence checks) */
-  double t_gram, t_solve, t_finalize, t_total; /* seconds */
+  double t_gram;        /* seconds of the precompute: the Gram build, or the squared row norms
+                           of the row path */
+  double t_solve, t_finalize, t_total; /* seconds */
   double t_kernel;      /* seconds the solver kernel ran, summed over its launches (HIP events on
                            the launch stream) */
 } svm_stats;

@@ -96,6 +96,7 @@ struct Shape {
 
 constexpr int32_t TWO_LEVEL_ABOVE = 128;  // workgroups per problem above which the exchange has two levels
 
+
 // Gram path: one workgroup up to 4096 samples (no exchange at all), else about sqrt(n)/3.5
 // workgroups, at most 64 -- the measured optimum between per-workgroup work and exchange
 // cost on MI355X (40 at n = 20,000, 64 at 50,000 and 100,000).  Row path: up to 256 workgroups of 512
@@ -122,6 +123,8 @@ bool choose_shape(int64_t n, bool gram, int32_t requested, int32_t levels, Shape
   s->nwg = (int32_t)nwg;
   s->per_wg = (int32_t)per_wg;
   s->per_thread = (int32_t)p;
+  // One level up to 128 workgroups; beyond that, every workgroup polling every record costs
+  // more (the polls of all workgroups crowd the same lines) than a second round trip.
   if (nwg > 1 && (levels == 2 || (levels == 0 && nwg > TWO_LEVEL_ABOVE))) {
     s->g1 = (int32_t)std::ceil(std::sqrt((double)nwg));
     s->ng = (int32_t)((nwg + s->g1 - 1) / s->g1);
@@ -147,8 +150,8 @@ struct TrainPlan {
   int64_t ld;
   Shape shape;
   int32_t cache_cap;
-  int64_t off_f, off_gram, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_tul, off_tb,
-      off_fin, off_err;
+  int64_t off_f, off_gram, off_sqn, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_tul,
+      off_tb, off_fin, off_err;
   int64_t total;
 };
 
@@ -177,6 +180,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   Layout L;
   p->off_f = L.add(8 * n);
   p->off_gram = p->gram ? L.add((int64_t)gram_bytes) : -1;
+  p->off_sqn = p->gram ? -1 : L.add(8 * n);
   p->off_cache = p->cache_cap ? L.add(4LL * p->cache_cap * p->ld) : -1;
   p->off_tags = p->cache_cap ? L.add(4LL * p->cache_cap * p->shape.nwg) : -1;
   p->off_ctl = L.add(sizeof(Ctl));
@@ -278,7 +282,8 @@ struct OvoPlan {
   bool gram;
   int64_t ld;
   int32_t P;
-  int64_t off_perm, off_xs, off_f, off_gram, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_fin, off_err;
+  int64_t off_perm, off_xs, off_f, off_gram, off_sqn, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_fin,
+      off_err;
   int64_t total;
 };
 
@@ -300,6 +305,7 @@ svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) 
   p->off_xs = L.add(4 * n * d);
   p->off_f = L.add(8 * (int64_t)(k - 1) * n);
   p->off_gram = p->gram ? L.add((int64_t)gram_bytes) : -1;
+  p->off_sqn = p->gram ? -1 : L.add(8 * n);
   p->off_ctl = L.add((int64_t)sizeof(Ctl) * p->P);
   p->off_prob = L.add((int64_t)sizeof(Prob) * p->P);
   p->off_wgp = L.add(4LL * p->P * OVO_MAX_WG_PER_PAIR);
@@ -440,7 +446,11 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   HIPCHK(ts.init());
   HIPCHK(tf.init());
   HIPCHK(hipEventRecord(tg.a, stream));
-  if (p.gram) HIPCHK(launch_gram(X, n, d, (float)gamma, G, p.ld, stream));
+  double *sqn = p.gram ? nullptr : reinterpret_cast<double *>(ws + p.off_sqn);
+  if (p.gram)
+    HIPCHK(launch_gram(X, n, d, (float)gamma, G, p.ld, stream));
+  else
+    HIPCHK(launch_row_norms(X, n, d, sqn, stream));
   HIPCHK(hipEventRecord(tg.b, stream));
 
   HIPCHK(hipEventRecord(ts.a, stream));
@@ -456,6 +466,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   sp.gram = G;
   sp.ld = p.ld;
   sp.X = X;
+  sp.sqn = sqn;
   sp.d = d;
   sp.cache = p.cache_cap ? reinterpret_cast<float *>(ws + p.off_cache) : nullptr;
   sp.cache_tags = p.cache_cap ? reinterpret_cast<int32_t *>(ws + p.off_tags) : nullptr;
@@ -493,7 +504,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     st->dual_obj = 0.5 * hfin[0] - 0.5 * hfin[1];
     st->gram_used = p.gram ? 1 : 0;
     st->launches = launches;
-    st->t_gram = p.gram ? tg.seconds() : 0.0;
+    st->t_gram = tg.seconds();
     st->t_solve = ts.seconds();
     st->t_finalize = tf.seconds();
     st->t_total = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
@@ -615,7 +626,11 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   HIPCHK(ts.init());
   HIPCHK(tf.init());
   HIPCHK(hipEventRecord(tg.a, stream));
-  if (p.gram) HIPCHK(launch_gram(Xs, n, d, (float)gamma, G, p.ld, stream));
+  double *sqn = p.gram ? nullptr : reinterpret_cast<double *>(ws + p.off_sqn);
+  if (p.gram)
+    HIPCHK(launch_gram(Xs, n, d, (float)gamma, G, p.ld, stream));
+  else
+    HIPCHK(launch_row_norms(Xs, n, d, sqn, stream));
   HIPCHK(hipEventRecord(tg.b, stream));
   HIPCHK(hipEventRecord(ts.a, stream));
   HIPCHK(launch_solver_init(dprob, p.P, max_n, stream));
@@ -630,6 +645,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   sp.gram = G;
   sp.ld = p.ld;
   sp.X = Xs;
+  sp.sqn = sqn;
   sp.d = d;
   sp.spin_limit = spin_ticks();
   sp.error = err;
@@ -660,7 +676,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
       S.dual_obj = 0.5 * hfin[4 * q2] - 0.5 * hfin[4 * q2 + 1];
       S.gram_used = p.gram ? 1 : 0;
       S.launches = launches;
-      S.t_gram = p.gram ? tg.seconds() : 0.0;
+      S.t_gram = tg.seconds();
       S.t_solve = ts.seconds();
       S.t_finalize = tf.seconds();
       S.t_total = t_total;

@@ -56,6 +56,7 @@ struct SolveParams {
   int64_t ld;
   // Row path
   const float *X;          // [N][d] (global order)
+  const double *sqn;       // [N] squared row norms of X (row_norms_k)
   int64_t d;
   float *cache;            // [cap][ld] row slices, or NULL
   int32_t *cache_tags;     // [nwg_total][cap] per-workgroup tag copies
@@ -69,6 +70,7 @@ struct SolveParams {
 hipError_t launch_gram(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, hipStream_t s);
 hipError_t launch_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, const int64_t *rows, int64_t r,
                               float *out, hipStream_t s);
+hipError_t launch_row_norms(const float *X, int64_t n, int64_t d, double *sqn, hipStream_t s);
 hipError_t launch_gather_rows(const float *X, int64_t d, const int32_t *perm, int64_t n, float *Xs, hipStream_t s);
 hipError_t launch_solver_init(const Prob *probs, int32_t nprob, int64_t max_n, hipStream_t s);
 hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,

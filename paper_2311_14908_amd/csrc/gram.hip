@@ -176,38 +176,40 @@ hipError_t launch_gram(const float *X, int64_t n, int64_t d, float gamma, float 
   return hipGetLastError();
 }
 
-// out[q][j] = K(x_rows[q], x_j), evaluated with the row path's routine (pairs of rows).
+// out[q][j] = K(x_rows[q], x_j), evaluated with the row path's routines (pairs of rows, the
+// sample norms computed here with the routine that fills the solver's norm table).
 template <bool VEC4>
 __global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X, int64_t n, int64_t d, double gamma,
                                                       const int64_t *__restrict__ rows, int64_t r,
                                                       float *__restrict__ out) {
-  constexpr int SB = 4;
-  extern __shared__ float4 sx4[];  // two staged rows
-  float *sx = reinterpret_cast<float *>(sx4);
+  constexpr int SB = 2, MAXM = 4;
   const int64_t q0 = 2 * (int64_t)blockIdx.y;
   const int64_t q1 = q0 + 1 < r ? q0 + 1 : q0;
   const int64_t ru = rows[q0], rl = rows[q1];
-  for (int64_t k = threadIdx.x; k < d; k += 256) {
-    sx[k] = X[ru * d + k];
-    sx[d + k] = X[rl * d + k];
-  }
-  __syncthreads();
+  const float *xu = X + ru * d, *xl = X + rl * d;
   const int gs = group_size_for(d, VEC4);
   const int lig = threadIdx.x & (gs - 1);
   const int ngroups = 256 / gs;
   const int grp = threadIdx.x / gs;
+  const double nu = sq_norm<VEC4>(xu, d, lig, gs), nl = sq_norm<VEC4>(xl, d, lig, gs);
+  RowPair<VEC4, MAXM> rp;
+  load_pair(rp, xu, xl, d, lig, gs);
   const int64_t chunk = (int64_t)ngroups * SB;
   for (int64_t j0 = (int64_t)blockIdx.x * chunk + (int64_t)grp * SB; j0 < n; j0 += (int64_t)gridDim.x * chunk) {
     const int nb = (int)(n - j0 < SB ? n - j0 : SB);
     const float *xs[SB];
+    double nj[SB];
 #pragma unroll
-    for (int b = 0; b < SB; ++b) xs[b] = X + (j0 + (b < nb ? b : nb - 1)) * d;
+    for (int b = 0; b < SB; ++b) {
+      xs[b] = X + (j0 + (b < nb ? b : nb - 1)) * d;
+      nj[b] = sq_norm<VEC4>(xs[b], d, lig, gs);
+    }
     double du[SB], dl[SB];
-    dist2_batch<VEC4, SB, 4>(xs, nb, sx, sx + d, d, lig, gs, du, dl);
+    dot_batch<VEC4, SB, MAXM>(xs, nb, xu, xl, d, lig, gs, rp, du, dl);
     for (int v = lig; v < 2 * SB; v += gs) {
       const int b = v < SB ? v : v - SB;
       if (b >= nb) continue;
-      const float kv = rbf_of(batch_value<SB>(du, dl, v), gamma);
+      const float kv = rbf_from_dot(v < SB ? nu : nl, nj[b], batch_value<SB>(du, dl, v), gamma);
       if (v < SB)
         out[q0 * n + j0 + b] = kv;
       else if (q1 != q0)
@@ -216,26 +218,44 @@ __global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X
   }
 }
 
+// sqn[j] = |x_j|^2, one group of lanes per row (the routine kernel_rows_k uses).
+template <bool VEC4>
+__global__ void __launch_bounds__(256) row_norms_k(const float *__restrict__ X, int64_t n, int64_t d,
+                                                    double *__restrict__ sqn) {
+  const int gs = group_size_for(d, VEC4);
+  const int lig = threadIdx.x & (gs - 1);
+  const int64_t groups = (int64_t)gridDim.x * (256 / gs);
+  for (int64_t j = (int64_t)blockIdx.x * (256 / gs) + threadIdx.x / gs; j < n; j += groups) {
+    const double v = sq_norm<VEC4>(X + j * d, d, lig, gs);
+    if (lig == 0) sqn[j] = v;
+  }
+}
+
+hipError_t launch_row_norms(const float *X, int64_t n, int64_t d, double *sqn, hipStream_t s) {
+  const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);
+  int64_t blocks = (n + 3) / 4;  // at least four rows per block (64-lane groups); grid-stride beyond
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  if (vec4)
+    hipLaunchKernelGGL(row_norms_k<true>, dim3((unsigned)blocks), dim3(256), 0, s, X, n, d, sqn);
+  else
+    hipLaunchKernelGGL(row_norms_k<false>, dim3((unsigned)blocks), dim3(256), 0, s, X, n, d, sqn);
+  return hipGetLastError();
+}
+
 hipError_t launch_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, const int64_t *rows, int64_t r,
                               float *out, hipStream_t s) {
   const int64_t pairs = (r + 1) / 2;
   if (pairs > 65535) return hipErrorInvalidValue;
   int64_t bx = (n + 255) / 256;
   if (bx > 1024) bx = 1024;
-  const size_t shmem = 2 * (size_t)d * sizeof(float);
   const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(X) & 15) == 0);
-  const void *fn = vec4 ? reinterpret_cast<const void *>(&kernel_rows_k<true>)
-                        : reinterpret_cast<const void *>(&kernel_rows_k<false>);
-  if (shmem > 48 * 1024) {
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
-    if (e != hipSuccess) return e;
-  }
   if (vec4)
-    hipLaunchKernelGGL(kernel_rows_k<true>, dim3((unsigned)bx, (unsigned)pairs), dim3(256), shmem, s, X, n, d, gamma,
+    hipLaunchKernelGGL(kernel_rows_k<true>, dim3((unsigned)bx, (unsigned)pairs), dim3(256), 0, s, X, n, d, gamma,
                        rows, r, out);
   else
-    hipLaunchKernelGGL(kernel_rows_k<false>, dim3((unsigned)bx, (unsigned)pairs), dim3(256), shmem, s, X, n, d,
-                       gamma, rows, r, out);
+    hipLaunchKernelGGL(kernel_rows_k<false>, dim3((unsigned)bx, (unsigned)pairs), dim3(256), 0, s, X, n, d, gamma,
+                       rows, r, out);
   return hipGetLastError();
 }
 

@@ -1,6 +1,8 @@
 // rbf_rows.hpp -- device routines that evaluate RBF kernel values between two rows (x_u, x_l)
-// and samples of X.  Shared by the solver's row path, its K_ul, and the exposed kernel-row
-// entry point, so all of them produce bit-identical values.
+// and samples of X as a GEMV: fp32 dot products against both rows in one pass over the
+// samples, combined with squared norms computed the same way.  Shared by the solver's row
+// path, its K_ul, and
+// the exposed kernel-row entry point, so all of them produce bit-identical values.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -15,11 +17,6 @@ __device__ __forceinline__ int group_size_for(int64_t d, bool vec4) {
   int gs = 1;
   while (gs < units && gs < 64) gs <<= 1;
   return gs;
-}
-
-__device__ __forceinline__ double sqdiff_acc(float v, float a, double acc) {
-  const float e = v - a;  // fp32 difference (relative error 6e-8), squared and summed in fp64
-  return __builtin_fma((double)e, (double)e, acc);
 }
 
 // Sum of `v` over aligned groups of gs lanes (gs a power of two <= 64), in every lane of the
@@ -45,93 +42,137 @@ __device__ __forceinline__ double group_sum(double v, int gs) {
   return v;
 }
 
-// Squared distances from x_u (xu) and x_l (xl) to nb <= SB samples xs[0..nb), computed by a
-// group of gs lanes: lane `lig` accumulates the features k = lig, lig+gs, ... (float4 units
-// when VEC4) in increasing order -- all loads of a chunk of MAXM such positions are issued
-// before any arithmetic -- then the group sums its lanes with group_sum.  The arithmetic of a
-// sample does not depend on SB, on the batch it shares, or on where x_u / x_l are read from.
-// Called with the whole wave active (nb, gs uniform per group).
-template <bool VEC4, int SB, int MAXM>
-__device__ __forceinline__ void dist2_batch(const float *const *xs, int nb, const float *xu, const float *xl, int64_t d,
-                                            int lig, int gs, double *du, double *dl) {
-#pragma unroll
-  for (int s = 0; s < SB; ++s) {
-    du[s] = 0.0;
-    dl[s] = 0.0;
+// Per-lane operand type: a float4 of features when VEC4, else one float.
+template <bool VEC4> struct Lane;
+template <> struct Lane<true> {
+  typedef float4 T;
+  static __device__ __forceinline__ float4 scale(float4 v, float m) { return make_float4(v.x * m, v.y * m, v.z * m, v.w * m); }
+  static __device__ __forceinline__ float dot(float4 v, float4 a, float acc) {
+    acc = __builtin_fmaf(v.x, a.x, acc);
+    acc = __builtin_fmaf(v.y, a.y, acc);
+    acc = __builtin_fmaf(v.z, a.z, acc);
+    return __builtin_fmaf(v.w, a.w, acc);
   }
-  if (VEC4) {
-    const int64_t d4 = d >> 2;
-    const float4 *u4 = reinterpret_cast<const float4 *>(xu);
-    const float4 *l4 = reinterpret_cast<const float4 *>(xl);
-    for (int64_t k0 = lig; k0 < d4; k0 += (int64_t)gs * MAXM) {
-      float4 a[MAXM], b[MAXM], v[SB][MAXM];
+};
+template <> struct Lane<false> {
+  typedef float T;
+  static __device__ __forceinline__ float scale(float v, float m) { return v * m; }
+  static __device__ __forceinline__ float dot(float v, float a, float acc) { return __builtin_fmaf(v, a, acc); }
+};
+
+// Squared norm of row x, computed exactly as dot_batch computes the dot product of a sample
+// with itself (a group of gs lanes; lane `lig` accumulates positions lig, lig+gs, ... in
+// increasing order in fp32, the group sums the partials in fp64).  So |x|^2 + |x|^2 - 2 x.x is
+// exactly 0 for identical rows (K = 1 on the diagonal and between duplicates), and every caller
+// gets the same bits for a row.
+template <bool VEC4>
+__device__ __forceinline__ double sq_norm(const float *x, int64_t d, int lig, int gs) {
+  typedef typename Lane<VEC4>::T T;
+  const T *p = reinterpret_cast<const T *>(x);
+  const int64_t units = VEC4 ? (d >> 2) : d;
+  float acc = 0.f;
+  for (int64_t k = lig; k < units; k += gs) acc = Lane<VEC4>::dot(p[k], p[k], acc);
+  return group_sum((double)acc, gs);
+}
+
+// Operands of a pair of rows (x_u, x_l) held by one lane for the first MAXM positions
+// k = lig + m*gs (float4 units when VEC4); positions past d are zeroed and masked.
+template <bool VEC4, int MAXM>
+struct RowPair {
+  typename Lane<VEC4>::T a[MAXM], b[MAXM];
+  float mk[MAXM];  // 1 inside d, 0 past it
+};
+
+template <bool VEC4, int MAXM>
+__device__ __forceinline__ void load_pair(RowPair<VEC4, MAXM> &r, const float *xu, const float *xl, int64_t d, int lig,
+                                          int gs) {
+  typedef typename Lane<VEC4>::T T;
+  const int64_t units = VEC4 ? (d >> 2) : d;
 #pragma unroll
-      for (int m = 0; m < MAXM; ++m) {
-        const int64_t k = k0 + (int64_t)m * gs;
-        if (k < d4) {
-          a[m] = u4[k];
-          b[m] = l4[k];
-#pragma unroll
-          for (int s = 0; s < SB; ++s)
-            if (s < nb) v[s][m] = reinterpret_cast<const float4 *>(xs[s])[k];
-        }
-      }
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m) {
-        if (k0 + (int64_t)m * gs < d4) {
-#pragma unroll
-          for (int s = 0; s < SB; ++s) {
-            if (s < nb) {
-              du[s] = sqdiff_acc(v[s][m].x, a[m].x, du[s]);
-              du[s] = sqdiff_acc(v[s][m].y, a[m].y, du[s]);
-              du[s] = sqdiff_acc(v[s][m].z, a[m].z, du[s]);
-              du[s] = sqdiff_acc(v[s][m].w, a[m].w, du[s]);
-              dl[s] = sqdiff_acc(v[s][m].x, b[m].x, dl[s]);
-              dl[s] = sqdiff_acc(v[s][m].y, b[m].y, dl[s]);
-              dl[s] = sqdiff_acc(v[s][m].z, b[m].z, dl[s]);
-              dl[s] = sqdiff_acc(v[s][m].w, b[m].w, dl[s]);
-            }
-          }
-        }
-      }
-    }
-  } else {
-    for (int64_t k0 = lig; k0 < d; k0 += (int64_t)gs * MAXM) {
-      float a[MAXM], b[MAXM], v[SB][MAXM];
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m) {
-        const int64_t k = k0 + (int64_t)m * gs;
-        if (k < d) {
-          a[m] = xu[k];
-          b[m] = xl[k];
-#pragma unroll
-          for (int s = 0; s < SB; ++s)
-            if (s < nb) v[s][m] = xs[s][k];
-        }
-      }
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m) {
-        if (k0 + (int64_t)m * gs < d) {
-#pragma unroll
-          for (int s = 0; s < SB; ++s) {
-            if (s < nb) {
-              du[s] = sqdiff_acc(v[s][m], a[m], du[s]);
-              dl[s] = sqdiff_acc(v[s][m], b[m], dl[s]);
-            }
-          }
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int s = 0; s < SB; ++s) {
-    du[s] = group_sum(du[s], gs);
-    dl[s] = group_sum(dl[s], gs);
+  for (int m = 0; m < MAXM; ++m) {
+    const int64_t k = lig + (int64_t)m * gs;
+    const int64_t kk = k < units ? k : units - 1;
+    r.mk[m] = k < units ? 1.f : 0.f;
+    r.a[m] = Lane<VEC4>::scale(reinterpret_cast<const T *>(xu)[kk], r.mk[m]);
+    r.b[m] = Lane<VEC4>::scale(reinterpret_cast<const T *>(xl)[kk], r.mk[m]);
   }
 }
 
-// K = exp(-gamma d^2) rounded to fp32.
-__device__ __forceinline__ float rbf_of(double d2, double gamma) { return (float)exp(-gamma * d2); }
+// Dot products of nb <= SB samples xs[0..nb) with x_u (pu) and x_l (pl), computed by a group
+// of gs lanes.  Lane `lig` accumulates the products of its positions k = lig, lig+gs, ... in
+// increasing order in fp32 (all loads of a block of MAXM positions issued before the
+// arithmetic; block 0 of x_u / x_l comes from `r`, later blocks are loaded here), and the group
+// sums the lanes' fp32 partials in fp64.  A sample's arithmetic does not depend on SB, on the
+// batch it shares, or on which of the two rows is x_u.  Called with the whole wave active (nb,
+// gs uniform per group); loads are unconditional (clamped positions and samples), so the
+// compiler can keep the loads of consecutive batches in flight together.
+template <bool VEC4, int SB, int MAXM>
+__device__ __forceinline__ void dot_batch(const float *const *xs, int nb, const float *xu, const float *xl, int64_t d,
+                                          int lig, int gs, const RowPair<VEC4, MAXM> &r, double *pu, double *pl) {
+  typedef typename Lane<VEC4>::T T;
+  const int64_t units = VEC4 ? (d >> 2) : d;
+  float fu[SB], fl[SB];
+  {
+    T v[SB][MAXM];
+#pragma unroll
+    for (int s = 0; s < SB; ++s) {
+      const T *p = reinterpret_cast<const T *>(xs[s < nb ? s : nb - 1]);
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) {
+        const int64_t k = lig + (int64_t)m * gs;
+        v[s][m] = p[k < units ? k : units - 1];
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < SB; ++s) {
+      fu[s] = 0.f;
+      fl[s] = 0.f;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) {  // r.a / r.b are zero past d (X is finite)
+        fu[s] = Lane<VEC4>::dot(v[s][m], r.a[m], fu[s]);
+        fl[s] = Lane<VEC4>::dot(v[s][m], r.b[m], fl[s]);
+      }
+    }
+  }
+  for (int64_t k0 = lig + (int64_t)gs * MAXM; k0 < units; k0 += (int64_t)gs * MAXM) {
+    T a[MAXM], b[MAXM], v[SB][MAXM];
+    float mk[MAXM];
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) {
+      const int64_t k = k0 + (int64_t)m * gs;
+      const int64_t kk = k < units ? k : units - 1;
+      mk[m] = k < units ? 1.f : 0.f;
+      a[m] = reinterpret_cast<const T *>(xu)[kk];
+      b[m] = reinterpret_cast<const T *>(xl)[kk];
+#pragma unroll
+      for (int s = 0; s < SB; ++s) v[s][m] = reinterpret_cast<const T *>(xs[s < nb ? s : nb - 1])[kk];
+    }
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) {
+      const T am = Lane<VEC4>::scale(a[m], mk[m]), bm = Lane<VEC4>::scale(b[m], mk[m]);
+#pragma unroll
+      for (int s = 0; s < SB; ++s) {
+        fu[s] = Lane<VEC4>::dot(v[s][m], am, fu[s]);
+        fl[s] = Lane<VEC4>::dot(v[s][m], bm, fl[s]);
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < SB; ++s) {
+    pu[s] = group_sum((double)fu[s], gs);
+    pl[s] = group_sum((double)fl[s], gs);
+  }
+}
+
+// K = exp(-gamma d^2) rounded to fp32, with d^2 = (|x|^2 + |y|^2) - 2 x.y from the norms and
+// the dot product (clamped at 0 against cancellation).  Not contracted, so the bits do not
+// depend on the caller; (|x|^2 + |y|^2) is symmetric in x and y.
+__device__ __forceinline__ float rbf_from_dot(double nx, double ny, double dot, double gamma) {
+#pragma clang fp contract(off)
+  double d2 = (nx + ny) - 2.0 * dot;
+  d2 = d2 > 0.0 ? d2 : 0.0;
+  return (float)exp(-gamma * d2);
+}
 
 // Value v (0..2*SB) of a batch: the u row for v < SB, else the l row.
 template <int SB>

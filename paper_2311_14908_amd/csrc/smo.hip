@@ -9,13 +9,16 @@
 //      (ties to the smaller index) with DPP wave reductions and one LDS hand-off;
 //   2. the nwg partial results are exchanged through global memory as self-stamped 64-bit
 //      words (payload | step stamp), so no fence or cache flush is needed: a reader simply
-//      waits until every word it needs carries the current stamp.  Above 64 workgroups the
-//      exchange has two levels (group leaders reduce about sqrt(nwg) records each and publish
-//      a group record; every workgroup then reads the group records);
+//      waits until every word it needs carries the current stamp.  With one level every
+//      workgroup polls all records, one record per lane over as many waves as needed; with
+//      two levels (the default above 128 workgroups) group leaders reduce about sqrt(nwg)
+//      records each and publish a group record, and every workgroup then reads the group
+//      records;
 //   3. every workgroup reduces the same nwg records to the same pair (u, l), tests the stop
 //      rule, and solves the 2x2 sub-problem redundantly (identical fp64 arithmetic);
-//   4. every workgroup fetches K(u, j) and K(l, j) for its own samples -- from the Gram or
-//      computed from X -- and applies f_j += da_u y_u K_uj + da_l y_l K_lj.
+//   4. every workgroup fetches K(u, j) and K(l, j) for its own samples -- from the Gram, or
+//      computed from X as a GEMV against x_u and x_l with the squared row norms -- and
+//      applies f_j += da_u y_u K_uj + da_l y_l K_lj.
 // Every wait is bounded by a wall-clock limit; on expiry the kernel records an error and
 // all waits end, so a launch always drains.
 #include "common.hpp"
@@ -26,11 +29,11 @@
 namespace svmx {
 
 // Gram path: 256-thread workgroups, up to 16 samples per thread.  Row path: 512-thread
-// workgroups (8 waves per CU, each with 4 samples x the lane's float4 loads in flight, keep
+// workgroups (8 waves per CU, each with 2 samples x the lane's float4 loads in flight, keep
 // the streaming of X busy without spilling), up to 8 samples per thread.
 constexpr int BS_GRAM = 256, MAXP_GRAM = 16;
 constexpr int BS_ROWS = 512, MAXP_ROWS = 8;
-constexpr int ROW_BATCH = 4;  // samples per lane group and batch in the row evaluation
+constexpr int ROW_BATCH = 2;  // samples per lane group and batch in the row evaluation
 constexpr int ROW_MAXM = 4;   // feature positions per lane whose loads are issued together
 constexpr int IBIG = 0x7fffffff;
 
@@ -192,13 +195,14 @@ __device__ __forceinline__ void put_record(u64 *rec, unsigned stamp, const Sel &
   }
 }
 
-// Wave-level: wait for records [q0, q1) of `words` to carry `stamp`, reduce them, and return
-// the result to every lane of the wave (all 64 lanes must call).
-__device__ Sel poll_reduce(const u64 *words, int q0, int q1, unsigned stamp, uint64_t spin_limit, int32_t *err,
-                           int *abort_flag) {
+// Wave-level: wait for records q0 + lane, q0 + lane + stride, ... below q1 of `words` to carry
+// `stamp`, reduce them, and return the result to every lane of the wave (all 64 lanes must
+// call).
+__device__ Sel poll_reduce(const u64 *words, int q0, int q1, int stride, unsigned stamp, uint64_t spin_limit,
+                           int32_t *err, int *abort_flag) {
   Sel s;
   sel_init(s);
-  for (int q = q0 + (int)(threadIdx.x & 63); q < q1; q += 64) {
+  for (int q = q0 + (int)(threadIdx.x & 63); q < q1; q += stride) {
     const u64 *rec = words + (size_t)q * SLOT_WORDS;
     u64 w[10];
     const uint64_t t0 = wall_clock64();
@@ -231,31 +235,40 @@ __device__ Sel poll_reduce(const u64 *words, int q0, int q1, unsigned stamp, uin
 }
 
 // Exchange of the workgroup selections of one problem (see file comment, item 2).  Wave 0
-// does the global-memory work; the result reaches the other waves through LDS.
+// publishes the record.  With one level, the records are polled by as many waves as needed
+// for one record per lane (wave w takes records w*64 + lane, then every 64*pollers-th), each
+// wave reduces its share, and the shares meet in LDS.  With two levels, wave 0 does the
+// global-memory work of both levels.
 template <int NW>
 __device__ Sel exchange(const Prob &P, int rank, unsigned stamp, const Sel &mine, SelLds<NW> &L, int &buf,
                         uint64_t spin_limit, int32_t *err, int *abort_flag) {
   const size_t par = stamp & 1u;
   u64 *lv1 = P.slots + par * (size_t)P.nwg * SLOT_WORDS;
-  if (threadIdx.x < 64) {
-    put_record(lv1 + (size_t)rank * SLOT_WORDS, stamp, mine);
-    Sel s;
-    if (P.g1 > 0) {
+  const int wave = threadIdx.x >> 6;
+  int pollers = 1;
+  if (wave == 0) put_record(lv1 + (size_t)rank * SLOT_WORDS, stamp, mine);
+  if (P.g1 > 0) {
+    if (wave == 0) {
       u64 *lv2 = P.slots2 + par * (size_t)P.ng * SLOT_WORDS;
       const int g = rank / P.g1;
       if (rank % P.g1 == 0) {
         const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
-        const Sel gs = poll_reduce(lv1, q0, q1, stamp, spin_limit, err, abort_flag);
+        const Sel gs = poll_reduce(lv1, q0, q1, 64, stamp, spin_limit, err, abort_flag);
         put_record(lv2 + (size_t)g * SLOT_WORDS, stamp, gs);
       }
-      s = poll_reduce(lv2, 0, P.ng, stamp, spin_limit, err, abort_flag);
-    } else {
-      s = poll_reduce(lv1, 0, P.nwg, stamp, spin_limit, err, abort_flag);
+      const Sel s = poll_reduce(lv2, 0, P.ng, 64, stamp, spin_limit, err, abort_flag);
+      if (threadIdx.x == 0) L.slot[buf][0] = s;
     }
-    if (threadIdx.x == 0) L.slot[buf][0] = s;
+  } else {
+    pollers = min(NW, (P.nwg + 63) >> 6);
+    if (wave < pollers) {
+      const Sel s = poll_reduce(lv1, wave * 64, P.nwg, 64 * pollers, stamp, spin_limit, err, abort_flag);
+      if ((threadIdx.x & 63) == 0) L.slot[buf][wave] = s;
+    }
   }
   __syncthreads();
-  const Sel r = L.slot[buf][0];
+  Sel r = L.slot[buf][0];
+  for (int q = 1; q < pollers; ++q) sel_merge(r, L.slot[buf][q]);
   buf ^= 1;
   return r;
 }
@@ -311,7 +324,7 @@ __device__ __forceinline__ void consider(Sel &s, double f, double a, int y, int 
 template <int BS, int PER, bool GRAM, bool VEC4>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   constexpr int NW = BS / 64;
-  constexpr int SB = PER == 1 ? ROW_BATCH : 2;  // a sample's arithmetic does not depend on SB
+  constexpr int SB = ROW_BATCH;  // a sample's arithmetic does not depend on SB
   extern __shared__ float4 dyn4[];  // row path: krow[2][per_wg], tags[cap]
   float *dyn = reinterpret_cast<float *>(dyn4);
   __shared__ SelLds<NW> sh;
@@ -416,9 +429,12 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       const int lig = threadIdx.x & (gs - 1);
       const int ngroups = BS / gs;
       const int grp = threadIdx.x / gs;
-      // x_u and x_l are read by every group straight from global memory (L2-resident after
-      // the first touch), so the loads of the rows overlap those of the samples.
+      // Block 0 of x_u and x_l is held in registers for the whole step; the samples stream
+      // past it in batches of SB.
       const float *xu = p.X + gu * d, *xl = p.X + gl * d;
+      const double nu = p.sqn[gu], nl = p.sqn[gl];
+      RowPair<VEC4, ROW_MAXM> rp;
+      load_pair(rp, xu, xl, d, lig, gs);
       int su = -1, sl = -1;
       bool hit_u = false, hit_l = false;
       if (use_cache) {
@@ -430,22 +446,31 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       // K_ul: x_l as the sample against x_u, exactly as the row of u evaluates sample l
       if (grp == 0) {
         const float *xs1[1] = {xl};
-        double du1[1], dl1[1];
-        dist2_batch<VEC4, 1, ROW_MAXM>(xs1, 1, xu, xu, d, lig, gs, du1, dl1);
-        if (lig == 0) s_kul = (double)rbf_of(du1[0], p.gamma);
+        double pu1[1], pl1[1];
+        dot_batch<VEC4, 1, ROW_MAXM>(xs1, 1, xu, xl, d, lig, gs, rp, pu1, pl1);
+        if (lig == 0) s_kul = (double)rbf_from_dot(nu, nl, pu1[0], p.gamma);
       }
       if (!(hit_u && hit_l)) {
         const int64_t cnt = lim - base;
         for (int64_t q0 = (int64_t)grp * SB; q0 < cnt; q0 += (int64_t)ngroups * SB) {
           const int nb = (int)min<int64_t>(SB, cnt - q0);
           const float *xs[SB];
+          double nj[SB];
 #pragma unroll
-          for (int b = 0; b < SB; ++b) xs[b] = p.X + gmap(P, base + q0 + min(b, nb - 1)) * d;
+          for (int b = 0; b < SB; ++b) {
+            const int64_t g = gmap(P, base + q0 + min(b, nb - 1));
+            xs[b] = p.X + g * d;
+            nj[b] = p.sqn[g];
+          }
           double du[SB], dl[SB];
-          dist2_batch<VEC4, SB, ROW_MAXM>(xs, nb, xu, xl, d, lig, gs, du, dl);
+          dot_batch<VEC4, SB, ROW_MAXM>(xs, nb, xu, xl, d, lig, gs, rp, du, dl);
           for (int v = lig; v < 2 * SB; v += gs) {
             const int b = v < SB ? v : v - SB;
-            if (b < nb) krow[(v < SB ? 0 : P.per_wg) + q0 + b] = rbf_of(batch_value<SB>(du, dl, v), p.gamma);
+            double njb = nj[0];
+#pragma unroll
+            for (int q = 1; q < SB; ++q) njb = b == q ? nj[q] : njb;
+            if (b < nb)
+              krow[(v < SB ? 0 : P.per_wg) + q0 + b] = rbf_from_dot(v < SB ? nu : nl, njb, batch_value<SB>(du, dl, v), p.gamma);
           }
         }
       }

@@ -155,6 +155,22 @@ def test_ragged_sizes(n, wgs, gram):
     check_decisions(d_gpu, oracle.decision(X, y, r.alpha, r.b, X[:500], 0.3))
 
 
+@pytest.mark.parametrize("gram", [svmx.GRAM_ON, svmx.GRAM_OFF])
+def test_exchange_configurations_agree(gram):
+    """The exchange is an exact reduction under a total order, so the number of workgroups,
+    the number of polling waves (one per 64 records) and the number of levels change nothing."""
+    X, y = synth.two_blobs(12000, 8, seed=7)
+    Xd, yd = dev(X), dev(y)
+    kw = dict(gram=gram, max_iter=300, trace_len=300)
+    base = svmx.svm_train(Xd, yd, 1.0, 0.3, 1e-3, workgroups=40, exchange_levels=1, **kw)
+    for wgs, lv in [(100, 1), (100, 2), (190, 1), (190, 2)]:
+        out = svmx.svm_train(Xd, yd, 1.0, 0.3, 1e-3, workgroups=wgs, exchange_levels=lv, **kw)
+        assert out.stats["iterations"] == base.stats["iterations"]
+        np.testing.assert_array_equal(out.trace_ul, base.trace_ul)
+        np.testing.assert_array_equal(out.trace_b, base.trace_b)
+        np.testing.assert_array_equal(out.alpha.cpu().numpy(), base.alpha.cpu().numpy())
+
+
 def test_duplicate_samples_eta_floor():
     X, y = synth.two_blobs(200, 4, seed=1)
     X = np.concatenate([X, X[:20]])
