@@ -10,8 +10,10 @@ Prints ONE JSON line.  ``value`` is SMO iterations per second over the timed ste
 kernel (the persistent SMO solver) against the HBM roofline with the algorithmic bytes of
 an SMO step (two kernel rows 8n, f read+write 16n, status n = 25n bytes); ``row_path``
 reports the same solve with kernel rows evaluated from X at every step (4nd + 21n bytes a
-step).  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same
-workload (first SMO steps of the same problem, on this host's cores).
+step).  ``ovo_row_path`` runs the 45 one-vs-one pairs of the 10-class workload on the row
+path, all pairs in one launch, for a fixed number of steps (4 n_p d + 21 n_p bytes per pair
+step).  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
+(first SMO steps of the same problem, on this host's cores).
 """
 from __future__ import annotations
 
@@ -61,6 +63,8 @@ def main():
     ap.add_argument("--row-path-steps", type=int, default=4000, help="SMO steps of the row-path measurement (0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time (0 = skip)")
     ap.add_argument("--no-ovo", action="store_true", help="skip the one-vs-one measurement (60000x784, 10 classes)")
+    ap.add_argument("--ovo-row-steps", type=int, default=300,
+                    help="SMO steps per pair of the one-vs-one row-path measurement (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="first run one plain device-to-device copy of BYTES (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -197,6 +201,23 @@ def main():
                          "gram_tflops": float(no) * no * Xo.shape[1] / oo.stats[0]["t_gram"] / 1e12,
                          "solver_kernel_seconds": oo.stats[0]["t_kernel"], "predict_seconds": t_pred,
                          "test_accuracy": float(np.mean(pred.cpu().numpy() == lto))}
+        if args.ovo_row_steps > 0:
+            # the same 45 pairs on the row path: every pair evaluates its kernel rows from X at
+            # every step, all pairs in one launch (batched one-vs-one steps)
+            svmx.svm_train_ovo(Xod, lod, wo.classes, wo.C, wo.gamma, wo.tol, gram=svmx.GRAM_OFF, max_iter=20)
+            torch.cuda.synchronize()
+            orow = svmx.svm_train_ovo(Xod, lod, wo.classes, wo.C, wo.gamma, wo.tol, gram=svmx.GRAM_OFF,
+                                      max_iter=args.ovo_row_steps)
+            _, sizes = svmx.ovo_offsets(lo, wo.classes)
+            its = [p["iterations"] for p in orow.stats]
+            ob = sum(float(i) * (4.0 * m * Xo.shape[1] + 21.0 * m) for i, m in zip(its, sizes))
+            tko = orow.stats[0]["t_kernel"]
+            result["ovo_row_path"] = {"kernel": "smo_solve (row path, 45 pairs in one launch)", "bound": "hbm",
+                                      "smo_steps_per_pair": [min(its), max(its)], "bytes": ob,
+                                      "bytes_per_pair_step": "4*n_p*d + 21*n_p", "kernel_seconds": tko,
+                                      "achieved": ob / tko / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                      "frac": ob / tko / 1e9 / HBM_PEAK_GBPS}
+            del orow
         del Xod, lod, Xtod, oo
         torch.cuda.empty_cache()
 

@@ -584,37 +584,62 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
 
   std::vector<Prob> hp(p.P);
   std::vector<int32_t> hwgp;
-  int64_t pack = 0, max_n = 0;
-  int32_t per_thread = 1, wg = 0, q = 0;
-  for (int32_t a = 0; a < k; ++a)
-    for (int32_t bb = a + 1; bb < k; ++bb, ++q) {
-      Prob &P = hp[q];
-      P = Prob{};
-      P.n = cnt[a] + cnt[bb];
-      P.off0 = start[a];
-      P.len0 = cnt[a];
-      P.off1 = start[bb];
-      P.y = nullptr;
-      P.alpha = alpha + pack;
-      P.f = f + pack;
-      P.ctl = ctl + q;
-      Shape sh;
-      const int64_t cap = std::max<int64_t>(1, OVO_TOTAL_WG / p.P);
-      if (!choose_shape(P.n, p.gram, r.workgroups, r.levels, &sh, cap) || sh.nwg > OVO_MAX_WG_PER_PAIR)
-        return fail(SVM_ENOMEM, "pair (%d,%d) too large to place", a, bb);
-      P.slots = slots + (size_t)q * 2 * OVO_MAX_WG_PER_PAIR * SLOT_WORDS;
-      P.g1 = sh.g1;
-      P.ng = sh.ng;
-      P.slots2 = sh.g1 ? slots2 + (size_t)q * 2 * OVO_MAX_GROUPS * SLOT_WORDS : nullptr;
-      P.wg0 = wg;
-      P.nwg = sh.nwg;
-      P.per_wg = sh.per_wg;
-      per_thread = std::max(per_thread, sh.per_thread);
-      for (int32_t w = 0; w < sh.nwg; ++w) hwgp.push_back(q);
-      wg += sh.nwg;
-      pack += P.n;
-      max_n = std::max(max_n, P.n);
-    }
+  int64_t max_n = 0;
+  int32_t per_thread = 1, wg = 0;
+  // Spread a workgroup budget over the pairs; all pairs run in one cooperative launch.
+  auto assign = [&](int64_t budget) -> svm_status {
+    hwgp.clear();
+    int64_t pack = 0;
+    max_n = 0;
+    per_thread = 1;
+    wg = 0;
+    int32_t q = 0;
+    for (int32_t a = 0; a < k; ++a)
+      for (int32_t bb = a + 1; bb < k; ++bb, ++q) {
+        Prob &P = hp[q];
+        P = Prob{};
+        P.n = cnt[a] + cnt[bb];
+        P.off0 = start[a];
+        P.len0 = cnt[a];
+        P.off1 = start[bb];
+        P.y = nullptr;
+        P.alpha = alpha + pack;
+        P.f = f + pack;
+        P.ctl = ctl + q;
+        Shape sh;
+        const int64_t cap = std::max<int64_t>(1, budget / p.P);
+        if (!choose_shape(P.n, p.gram, r.workgroups, r.levels, &sh, cap) || sh.nwg > OVO_MAX_WG_PER_PAIR)
+          return fail(SVM_ENOMEM, "pair (%d,%d) too large to place", a, bb);
+        P.slots = slots + (size_t)q * 2 * OVO_MAX_WG_PER_PAIR * SLOT_WORDS;
+        P.g1 = sh.g1;
+        P.ng = sh.ng;
+        P.slots2 = sh.g1 ? slots2 + (size_t)q * 2 * OVO_MAX_GROUPS * SLOT_WORDS : nullptr;
+        P.wg0 = wg;
+        P.nwg = sh.nwg;
+        P.per_wg = sh.per_wg;
+        per_thread = std::max(per_thread, sh.per_thread);
+        for (int32_t w = 0; w < sh.nwg; ++w) hwgp.push_back(q);
+        wg += sh.nwg;
+        pack += P.n;
+        max_n = std::max(max_n, P.n);
+      }
+    return SVM_OK;
+  };
+  // Shrink the budget until the variant the shapes need fits on the device at once.
+  int64_t budget = OVO_TOTAL_WG;
+  for (;;) {
+    s0 = assign(budget);
+    if (s0 != SVM_OK) return s0;
+    SolveParams probe{};
+    probe.X = Xs;
+    probe.d = d;
+    int32_t capacity = 0;
+    HIPCHK(launch_solver(probe, 0, per_thread, p.gram, stream, &capacity));
+    if (wg <= capacity) break;
+    if (budget <= p.P || capacity <= 0)
+      return fail(SVM_ENOMEM, "%d solver workgroups do not fit on the device at once (at most %d)", wg, capacity);
+    budget = std::max<int64_t>(p.P, std::min<int64_t>(budget - 1, capacity));
+  }
   HIPCHK(hipMemcpyAsync(dperm, perm.data(), 4 * n, hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(dprob, hp.data(), sizeof(Prob) * hp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));

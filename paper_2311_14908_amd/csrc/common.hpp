@@ -73,6 +73,7 @@ hipError_t launch_kernel_rows(const float *X, int64_t n, int64_t d, double gamma
 hipError_t launch_row_norms(const float *X, int64_t n, int64_t d, double *sqn, hipStream_t s);
 hipError_t launch_gather_rows(const float *X, int64_t d, const int32_t *perm, int64_t n, float *Xs, hipStream_t s);
 hipError_t launch_solver_init(const Prob *probs, int32_t nprob, int64_t max_n, hipStream_t s);
+// total_wg <= 0 only reports in *max_coresident how many workgroups of the variant fit at once.
 hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
                          int32_t *max_coresident);
 hipError_t launch_finalize(const Prob *probs, int32_t nprob, double C, double *out /*[nprob][4]*/, hipStream_t s);

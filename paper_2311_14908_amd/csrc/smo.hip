@@ -307,6 +307,13 @@ __device__ __forceinline__ PairStep solve_pair(double C, double bu, double bl, d
   return PairStep{aun, aln};
 }
 
+// f_j + (c_u K_uj + c_l K_lj), rounded as written (no contraction), so that every solver
+// variant -- whatever its unrolling -- produces the same bits.
+__device__ __forceinline__ double f_update(double f, double cu, float ku, double cl, float kl) {
+#pragma clang fp contract(off)
+  return f + (cu * (double)ku + cl * (double)kl);
+}
+
 __device__ __forceinline__ int64_t gmap(const Prob &P, int64_t j) { return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0); }
 __device__ __forceinline__ int label_of(const Prob &P, int64_t j) {
   return P.y ? P.y[gmap(P, j)] : (j < P.len0 ? 1 : -1);
@@ -503,7 +510,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
     for (int k = 0; k < PER; ++k) {
       const int64_t j = base + threadIdx.x + (int64_t)k * BS;
       if (j < lim) {
-        f[k] += cu * (double)ku[k] + cl * (double)kl[k];
+        f[k] = f_update(f[k], cu, ku[k], cl, kl[k]);
         if (j == u) a[k] = au_new;
         if (j == l) a[k] = al_new;
         consider(s, f[k], a[k], yv[k], (int)j, C);
@@ -607,6 +614,7 @@ static hipError_t launch_one(const SolveParams &p, int32_t total_wg, size_t shme
   e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, BS, shmem);
   if (e != hipSuccess) return e;
   if (maxres) *maxres = per_cu * cus;
+  if (total_wg <= 0) return hipSuccess;  // capacity query only
   if ((int64_t)total_wg > (int64_t)per_cu * cus) return hipErrorCooperativeLaunchTooLarge;
   SolveParams pp = p;
   void *args[] = {&pp};

@@ -119,3 +119,24 @@ def test_ovo_full_size():
     assert err <= 1e-3
     sure = np.all(np.abs(d_ref) >= 1e-3, axis=1)
     assert np.array_equal(pred.cpu().numpy()[sure], np.array(R["test_pred"])[sure])
+
+
+def test_ovo_row_path_full_size_pairs_equal_binary():
+    """One-vs-one on the row path at the full workload size (45 pairs of 12000 samples in one
+    cooperative launch, the workgroup budget fitted to what the device holds at once): after a
+    fixed number of steps every pair equals a standalone binary row-path solve of that pair,
+    bit for bit (the row values of a sample do not depend on how samples are spread over
+    workgroups, and the exchange is an exact reduction)."""
+    wl = synth.workload(4)
+    k = wl.classes
+    X, lab, _, _ = synth.generate(4, m=1)
+    steps = 200
+    Xd, ld = dev(X), dev(lab)
+    out = svmx.svm_train_ovo(Xd, ld, k, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=steps)
+    assert out.status in (svmx.SVM_OK, svmx.SVM_NOT_CONVERGED)
+    offs, sizes = svmx.ovo_offsets(lab, k)
+    for p, (a, b) in enumerate(oracle.ovo_pairs(k)):
+        idx, y = oracle.ovo_local(lab, a, b)
+        r = svmx.svm_train(dev(X[idx]), dev(y), wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=steps)
+        assert out.stats[p]["iterations"] == r.stats["iterations"]
+        assert torch.equal(out.alpha[offs[p]:offs[p] + sizes[p]], r.alpha), f"pair {p}"
