@@ -60,6 +60,34 @@ def test_kernel_rows_full_size(cid):
     assert np.all(got[np.arange(len(rows)), rows] == 1.0)
 
 
+@pytest.mark.parametrize("n,d,misalign", [(3000, 1500, 0), (2000, 301, 0), (2000, 784, 1)])
+def test_row_path_wide_and_unaligned(n, d, misalign):
+    """Rows wider than one register block of the GEMV (d = 1500: 375 float4 per row, more than
+    4 x 64), scalar lanes (d = 301), and X that is not 16-byte aligned (scalar lanes at d = 784):
+    kernel rows against the oracle, K = 1 between identical rows, and the working set of a short
+    row-path training against the oracle's up to its first near-tie."""
+    X, y = synth.two_blobs(n, d, seed=d)
+    X[7] = X[3]  # a duplicate pair
+    gamma = 1.0 / d
+    buf = torch.empty(n * d + misalign, dtype=torch.float32, device="cuda")
+    Xd = buf[misalign:].view(n, d)
+    Xd.copy_(torch.from_numpy(X))
+    assert (Xd.data_ptr() % 16 != 0) == bool(misalign)
+    rows = np.array([0, 3, 7, n - 1, 1234 % n])
+    got = svmx.svm_kernel_rows(Xd, gamma, rows).cpu().numpy()
+    ref = oracle.kernel_rows(X, rows, gamma)
+    assert row_rel_err(got, ref) <= ROW_RTOL
+    assert np.all(got[np.arange(len(rows)), rows] == 1.0)
+    assert got[1, 7] == 1.0 and got[2, 3] == 1.0
+    r = oracle.train(X, y, 1.0, gamma, 1e-3, max_iter=300, trace_len=300)
+    out = svmx.svm_train(Xd, dev(y), 1.0, gamma, 1e-3, gram=svmx.GRAM_OFF, max_iter=300, trace_len=300)
+    tied = np.flatnonzero(np.asarray(r.trace_gap)[1:].min(axis=1) < 1e-6)
+    k = min(r.iterations + 1, 300, int(tied[0]) + 1 if tied.size else 300)
+    assert k >= 20
+    np.testing.assert_array_equal(out.trace_ul[:k], r.trace_ul[:k])
+    np.testing.assert_allclose(out.trace_b[:k], r.trace_b[:k], atol=F_ATOL, rtol=0)
+
+
 @pytest.mark.parametrize("cid,n,d", [(0, 1000, 16), (2, 1300, 128), (1, 700, 784), (3, 3001, 32), (0, 333, 13),
                                      (0, 129, 5)])
 def test_gram_small(cid, n, d):
