@@ -12,7 +12,9 @@ an SMO step (two kernel rows 8n, f read+write 16n, status n = 25n bytes); ``row_
 reports the same solve with kernel rows evaluated from X at every step (4nd + 21n bytes a
 step).  ``ovo_row_path`` runs the 45 one-vs-one pairs of the 10-class workload on the row
 path, all pairs in one launch, for a fixed number of steps (4 n_p d + 21 n_p bytes per pair
-step).  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
+step).  ``paper_shapes`` times single trainings at the shapes of the paper's own runs (102
+features, 200-800 samples per class, binary and nine-class one-vs-one) for context.
+``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
 (first SMO steps of the same problem, on this host's cores).
 """
 from __future__ import annotations
@@ -63,6 +65,8 @@ def main():
     ap.add_argument("--row-path-steps", type=int, default=4000, help="SMO steps of the row-path measurement (0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time (0 = skip)")
     ap.add_argument("--no-ovo", action="store_true", help="skip the one-vs-one measurement (60000x784, 10 classes)")
+    ap.add_argument("--no-paper-shapes", action="store_true",
+                    help="skip the context runs at the paper's shapes (d=102, 200-800 per class)")
     ap.add_argument("--ovo-row-steps", type=int, default=300,
                     help="SMO steps per pair of the one-vs-one row-path measurement (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -220,6 +224,32 @@ def main():
             del orow
         del Xod, lod, Xtod, oo
         torch.cuda.empty_cache()
+
+    if not args.no_paper_shapes:
+        # context runs of the paper's shapes (102 features, 200-800 samples per class; binary and
+        # nine-class one-vs-one): wall seconds of one training from device-resident inputs
+        ps = synth.PAPER_SHAPE
+        shapes = {"binary": {}, "ovo9": {}}
+        for per in (200, 400, 600, 800):
+            Xp, lp = synth.paper_shaped(per, 2, seed=per)
+            yp = np.where(lp == 0, 1, -1).astype(np.int32)
+            Xpd, ypd = torch.from_numpy(Xp).cuda(), torch.from_numpy(yp).cuda()
+            svmx.svm_train(Xpd, ypd, ps["C"], ps["gamma"], ps["tol"])
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            rp = svmx.svm_train(Xpd, ypd, ps["C"], ps["gamma"], ps["tol"])
+            torch.cuda.synchronize()
+            shapes["binary"][per] = {"train_seconds": time.perf_counter() - t1, "smo_iterations": rp.stats["iterations"]}
+            Xp, lp = synth.paper_shaped(per, 9, seed=per)
+            Xpd, lpd = torch.from_numpy(Xp).cuda(), torch.from_numpy(lp).cuda()
+            svmx.svm_train_ovo(Xpd, lpd, 9, ps["C"], ps["gamma"], ps["tol"])
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            op = svmx.svm_train_ovo(Xpd, lpd, 9, ps["C"], ps["gamma"], ps["tol"])
+            torch.cuda.synchronize()
+            shapes["ovo9"][per] = {"train_seconds": time.perf_counter() - t1,
+                                   "smo_iterations": sum(q["iterations"] for q in op.stats)}
+        result["paper_shapes"] = {"d": ps["d"], "per_class": [200, 400, 600, 800], **shapes}
 
     if args.cpu_seconds > 0:
         import oracle

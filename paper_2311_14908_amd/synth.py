@@ -182,3 +182,23 @@ def multiclass_blobs(n: int, d: int, k: int, seed: int):
     """Small k-class problem (recipe of workload 4) at any size."""
     Xtr, ltr, _, _ = _gen4(seed, n, 1, d, k)
     return Xtr, ltr
+
+
+# Paper-shaped context runs: the paper's binary and nine-class timings (Tables 3 and 4) use a
+# 102-band hyperspectral scene with 200-800 training samples per class.  This recipe only
+# matches that shape (d = 102, `per_class` samples of each of `classes` classes); the scene
+# itself is not used.  Class mean spectra ~ 0.5 + 0.2 N(0, I); samples = mean + 0.1 N(0, I),
+# clipped to [0, 1].  C = 10, gamma = 0.5, tol = 1e-3 (the paper states none of them).
+PAPER_SHAPE = dict(d=102, C=10.0, gamma=0.5, tol=1e-3)
+
+
+def paper_shaped(per_class: int, classes: int, seed: int = 0):
+    """Returns (X float32 [classes*per_class, 102], labels int32 in 0..classes-1), shuffled."""
+    d = PAPER_SHAPE["d"]
+    rng = np.random.default_rng(seed)
+    mu = 0.5 + 0.2 * rng.standard_normal((classes, d))
+    n = classes * per_class
+    lab = (np.arange(n) % classes)[rng.permutation(n)].astype(np.int32)
+    X = np.clip(mu[lab] + 0.1 * rng.standard_normal((n, d)), 0.0, 1.0).astype(np.float32)
+    return np.ascontiguousarray(X), np.ascontiguousarray(lab)
+

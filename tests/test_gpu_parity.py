@@ -324,6 +324,40 @@ def test_ovo_small(gram):
     assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
 
 
+def test_paper_shaped_context_runs():
+    """The shapes of the paper's own runs (102 features, 200 per class): binary against the
+    oracle's trajectory and result, nine-class one-vs-one (36 pairs) against the oracle's optimum
+    (tol 1e-5 on both sides, as for the other one-vs-one comparisons)."""
+    ps = synth.PAPER_SHAPE
+    X, lab = synth.paper_shaped(200, 2, seed=200)
+    y = np.where(lab == 0, 1, -1).astype(np.int32)
+    r = oracle.train(X, y, ps["C"], ps["gamma"], ps["tol"], trace_len=1000)
+    out = svmx.svm_train(dev(X), dev(y), ps["C"], ps["gamma"], ps["tol"], trace_len=1000)
+    tied = np.flatnonzero(np.asarray(r.trace_gap)[1:].min(axis=1) < 1e-6)
+    k = min(r.iterations + 1, 1000, int(tied[0]) + 1 if tied.size else 1000)
+    np.testing.assert_array_equal(out.trace_ul[:k], r.trace_ul[:k])
+    assert abs(out.stats["dual_obj"] - r.dual_obj) <= W_RTOL * abs(r.dual_obj)
+    check_decisions(svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, ps["gamma"], dev(X)).cpu().numpy(),
+                    oracle.decision(X, y, r.alpha, r.b, X, ps["gamma"]))
+
+    k9, tol = 9, 1e-5
+    X, lab = synth.paper_shaped(200, k9, seed=200)
+    models = oracle.train_ovo(X, lab, k9, ps["C"], ps["gamma"], tol)
+    out = svmx.svm_train_ovo(dev(X), dev(lab), k9, ps["C"], ps["gamma"], tol)
+    assert out.status == svmx.SVM_OK
+    offs, sizes = svmx.ovo_offsets(lab, k9)
+    a = out.alpha.cpu().numpy()
+    for p, (idx, yp, rp) in enumerate(models):
+        ap = a[offs[p]:offs[p] + sizes[p]]
+        assert abs(out.stats[p]["dual_obj"] - rp.dual_obj) <= W_RTOL * abs(rp.dual_obj)
+        assert kkt_ok(X[idx], yp, ap, out.b[p], ps["C"], ps["gamma"], tol, slack=1e-5)
+    dec_ref, pred_ref = oracle.predict_ovo(X, lab, k9, models, X, ps["gamma"])
+    dec, pred = svmx.svm_predict_ovo(dev(X), dev(lab), k9, out.alpha, out.b, ps["gamma"], dev(X))
+    assert np.max(np.abs(dec.cpu().numpy() - dec_ref)) <= DEC_ATOL
+    sure = np.all(np.abs(dec_ref) >= DEC_ATOL, axis=1)
+    assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
+
+
 def test_ovo_predict_matches_oracle_given_alpha():
     k = 5
     X, lab, Xt, _ = synth.generate(4, n=500, m=200, d=12, classes=k)
