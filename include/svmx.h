@@ -57,6 +57,14 @@ typedef enum {
   SVM_GRAM_OFF = 2   /* row path: evaluate the two kernel rows from X at every step */
 } svm_gram_mode;
 
+/* Which MFMA instruction computes the Gram's dot products (the Gram path and svm_gram). */
+typedef enum {
+  SVM_MFMA_SPLIT_F16 = 0, /* every row scaled by a power of two and split into two fp16 halves;
+                             three fp16 MFMA products per fp32 product (v_mfma_f32_16x16x32_f16),
+                             fp32 accumulation; values as accurate as SVM_MFMA_F32 */
+  SVM_MFMA_F32 = 1        /* fp32 inputs on v_mfma_f32_16x16x4f32 */
+} svm_gram_mfma;
+
 typedef struct {
   int32_t struct_size;       /* = sizeof(svm_options); set by svm_default_options */
   int32_t gram;              /* svm_gram_mode */
@@ -75,6 +83,8 @@ typedef struct {
   int32_t workgroups;        /* solver workgroups per problem; 0 = automatic */
   int32_t exchange_levels;   /* levels of the cross-workgroup exchange: 1, 2, or 0 = automatic
                                 (two levels above 128 workgroups per problem) */
+  int32_t gram_mfma;         /* svm_gram_mfma */
+  int32_t reserved;          /* must be 0 */
 } svm_options;
 
 typedef struct {
@@ -169,10 +179,14 @@ svm_status svm_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, c
                            float *out, const svm_options *o);
 
 /*
- * The full fp32 RBF Gram the Gram path precomputes (MFMA X X^T with a row-norm epilogue):
- * G[i*ld + j] = K(x_i, x_j) for i, j < n; ld >= n.  G device fp32 [n][ld].
+ * The full fp32 RBF Gram the Gram path precomputes (MFMA X X^T with a row-norm epilogue, on the
+ * instruction o->gram_mfma selects): G[i*ld + j] = K(x_i, x_j) for i, j < n; ld >= n.  G device
+ * fp32 [n][ld].  workspace: device scratch of svm_gram_workspace_bytes(n, d, o) bytes (the split
+ * fp16 rows, scales and norms; 0 bytes for SVM_MFMA_F32, where workspace may be NULL).
  */
-svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G, int64_t ld, const svm_options *o);
+int64_t svm_gram_workspace_bytes(int64_t n, int64_t d, const svm_options *o);
+svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G, int64_t ld, void *workspace,
+                    int64_t workspace_bytes, const svm_options *o);
 
 /* Thread-local message for the last non-OK status of this thread ("" if none). */
 const char *svm_last_error(void);

@@ -67,6 +67,7 @@ struct Opts {
   hipStream_t stream;
   int32_t workgroups;
   int32_t levels;
+  int32_t gram_mfma;
 };
 
 bool resolve(const svm_options *o, int64_t n, Opts *r) {
@@ -86,7 +87,9 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
   r->stream = reinterpret_cast<hipStream_t>(o->stream);
   r->workgroups = std::max<int32_t>(0, o->workgroups);
   r->levels = o->exchange_levels;
-  return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF && r->levels >= 0 && r->levels <= 2;
+  r->gram_mfma = o->gram_mfma;
+  return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF && r->levels >= 0 && r->levels <= 2 &&
+         (r->gram_mfma == SVM_MFMA_SPLIT_F16 || r->gram_mfma == SVM_MFMA_F32) && o->reserved == 0;
 }
 
 // How a problem of n samples is spread over workgroups.
@@ -150,8 +153,8 @@ struct TrainPlan {
   int64_t ld;
   Shape shape;
   int32_t cache_cap;
-  int64_t off_f, off_gram, off_sqn, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_tul,
-      off_tb, off_fin, off_err;
+  int64_t off_f, off_gram, off_split, off_sqn, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2,
+      off_tul, off_tb, off_fin, off_err;
   int64_t total;
 };
 
@@ -180,6 +183,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   Layout L;
   p->off_f = L.add(8 * n);
   p->off_gram = p->gram ? L.add((int64_t)gram_bytes) : -1;
+  p->off_split = (p->gram && o.gram_mfma == SVM_MFMA_SPLIT_F16) ? L.add(gram_split_scratch_bytes(n, d)) : -1;
   p->off_sqn = p->gram ? -1 : L.add(8 * n);
   p->off_cache = p->cache_cap ? L.add(4LL * p->cache_cap * p->ld) : -1;
   p->off_tags = p->cache_cap ? L.add(4LL * p->cache_cap * p->shape.nwg) : -1;
@@ -282,8 +286,8 @@ struct OvoPlan {
   bool gram;
   int64_t ld;
   int32_t P;
-  int64_t off_perm, off_xs, off_f, off_gram, off_sqn, off_ctl, off_prob, off_wgp, off_slots, off_slots2, off_fin,
-      off_err;
+  int64_t off_perm, off_xs, off_f, off_gram, off_split, off_sqn, off_ctl, off_prob, off_wgp, off_slots, off_slots2,
+      off_fin, off_err;
   int64_t total;
 };
 
@@ -305,6 +309,7 @@ svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) 
   p->off_xs = L.add(4 * n * d);
   p->off_f = L.add(8 * (int64_t)(k - 1) * n);
   p->off_gram = p->gram ? L.add((int64_t)gram_bytes) : -1;
+  p->off_split = (p->gram && o.gram_mfma == SVM_MFMA_SPLIT_F16) ? L.add(gram_split_scratch_bytes(n, d)) : -1;
   p->off_sqn = p->gram ? -1 : L.add(8 * n);
   p->off_ctl = L.add((int64_t)sizeof(Ctl) * p->P);
   p->off_prob = L.add((int64_t)sizeof(Prob) * p->P);
@@ -447,7 +452,9 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   HIPCHK(tf.init());
   HIPCHK(hipEventRecord(tg.a, stream));
   double *sqn = p.gram ? nullptr : reinterpret_cast<double *>(ws + p.off_sqn);
-  if (p.gram)
+  if (p.gram && p.off_split >= 0)
+    HIPCHK(launch_gram_split(X, n, d, (float)gamma, G, p.ld, ws + p.off_split, stream));
+  else if (p.gram)
     HIPCHK(launch_gram(X, n, d, (float)gamma, G, p.ld, stream));
   else
     HIPCHK(launch_row_norms(X, n, d, sqn, stream));
@@ -652,7 +659,9 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   HIPCHK(tf.init());
   HIPCHK(hipEventRecord(tg.a, stream));
   double *sqn = p.gram ? nullptr : reinterpret_cast<double *>(ws + p.off_sqn);
-  if (p.gram)
+  if (p.gram && p.off_split >= 0)
+    HIPCHK(launch_gram_split(Xs, n, d, (float)gamma, G, p.ld, ws + p.off_split, stream));
+  else if (p.gram)
     HIPCHK(launch_gram(Xs, n, d, (float)gamma, G, p.ld, stream));
   else
     HIPCHK(launch_row_norms(Xs, n, d, sqn, stream));
@@ -774,7 +783,14 @@ svm_status svm_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, c
   return SVM_OK;
 }
 
-svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G, int64_t ld, const svm_options *o) {
+int64_t svm_gram_workspace_bytes(int64_t n, int64_t d, const svm_options *o) {
+  Opts op;
+  if (n < 1 || d < 1 || d > (INT64_MAX / 8) / n || !resolve(o, n, &op)) return -1;
+  return op.gram_mfma == SVM_MFMA_SPLIT_F16 ? gram_split_scratch_bytes(n, d) : 0;
+}
+
+svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G, int64_t ld, void *workspace,
+                    int64_t workspace_bytes, const svm_options *o) {
   g_err.clear();
   if (!X || !G) return fail(SVM_EINVAL, "NULL pointer argument");
   if (n < 1 || d < 1 || ld < n) return fail(SVM_EINVAL, "need n, d >= 1 and ld >= n");
@@ -782,7 +798,15 @@ svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G
   if (d > (INT64_MAX / 8) / n || ld > (INT64_MAX / 8) / n) return fail(SVM_ENOMEM, "sizes overflow");
   Opts op;
   if (!resolve(o, n, &op)) return fail(SVM_EINVAL, "bad options");
-  HIPCHK(launch_gram(X, n, d, (float)gamma, G, ld, op.stream));
+  if (op.gram_mfma == SVM_MFMA_SPLIT_F16) {
+    const int64_t need = gram_split_scratch_bytes(n, d);
+    if (!workspace || workspace_bytes < need)
+      return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)need,
+                  (long long)workspace_bytes);
+    HIPCHK(launch_gram_split(X, n, d, (float)gamma, G, ld, workspace, op.stream));
+  } else {
+    HIPCHK(launch_gram(X, n, d, (float)gamma, G, ld, op.stream));
+  }
   HIPCHK(hipStreamSynchronize(op.stream));
   return SVM_OK;
 }

@@ -20,6 +20,7 @@ from .build import lib_path
 SVM_OK, SVM_NOT_CONVERGED = 0, 1
 SVM_EINVAL, SVM_ENOMEM, SVM_EDEVICE, SVM_EWORKSPACE = -1, -2, -3, -4
 GRAM_AUTO, GRAM_ON, GRAM_OFF = 0, 1, 2
+MFMA_SPLIT_F16, MFMA_F32 = 0, 1
 
 
 class SvmError(RuntimeError):
@@ -33,7 +34,7 @@ class svm_options(C.Structure):
                 ("row_cache_bytes", C.c_int64), ("max_iter", C.c_int64), ("check_every", C.c_int32),
                 ("trace_len", C.c_int32), ("trace_ws", C.POINTER(C.c_int32)), ("trace_b", C.POINTER(C.c_double)),
                 ("f_out", C.c_void_p), ("stream", C.c_void_p), ("workgroups", C.c_int32),
-                ("exchange_levels", C.c_int32)]
+                ("exchange_levels", C.c_int32), ("gram_mfma", C.c_int32), ("reserved", C.c_int32)]
 
 
 class svm_stats(C.Structure):
@@ -48,7 +49,7 @@ class svm_stats(C.Structure):
 
 EXPORTS = ("svm_default_options", "svm_train_workspace_bytes", "svm_train", "svm_predict_workspace_bytes",
            "svm_predict", "svm_train_ovo_workspace_bytes", "svm_train_ovo", "svm_predict_ovo_workspace_bytes",
-           "svm_predict_ovo", "svm_kernel_rows", "svm_gram", "svm_last_error")
+           "svm_predict_ovo", "svm_kernel_rows", "svm_gram_workspace_bytes", "svm_gram", "svm_last_error")
 
 _lib = None
 
@@ -75,7 +76,8 @@ def load(path: str | None = None):
         "svm_predict_ovo_workspace_bytes": (I64, [I64, I64, I32, I64]),
         "svm_predict_ovo": (C.c_int, [V, V, I64, I64, I32, V, V, D, V, I64, V, V, V, I64, OP]),
         "svm_kernel_rows": (C.c_int, [V, I64, I64, D, V, I64, V, OP]),
-        "svm_gram": (C.c_int, [V, I64, I64, D, V, I64, OP]),
+        "svm_gram_workspace_bytes": (I64, [I64, I64, OP]),
+        "svm_gram": (C.c_int, [V, I64, I64, D, V, I64, V, I64, OP]),
         "svm_last_error": (C.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -106,7 +108,7 @@ def _dev(t: torch.Tensor, dtype, name):
 
 
 def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, check_every=0, trace_len=0,
-            workgroups=0, exchange_levels=0, f_out: torch.Tensor | None = None, stream=None):
+            workgroups=0, exchange_levels=0, gram_mfma=0, f_out: torch.Tensor | None = None, stream=None):
     o = svm_options()
     load().svm_default_options(C.byref(o))
     o.gram = gram
@@ -118,6 +120,7 @@ def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, 
     o.trace_len = trace_len
     o.workgroups = workgroups
     o.exchange_levels = exchange_levels
+    o.gram_mfma = gram_mfma
     o.f_out = None if f_out is None else f_out.data_ptr()
     s = stream if stream is not None else torch.cuda.current_stream()
     o.stream = s.cuda_stream
@@ -247,7 +250,11 @@ def svm_gram(X, gamma: float, ld: int | None = None, **opt) -> torch.Tensor:
     ld = n if ld is None else int(ld)
     G = torch.empty((n, ld), dtype=torch.float32, device=X.device)
     o = options(**opt)
-    _check(lib.svm_gram(_ptr(X), n, d, float(gamma), _ptr(G), ld, C.byref(o)))
+    wsb = lib.svm_gram_workspace_bytes(n, d, C.byref(o))
+    if wsb < 0:
+        raise SvmError(SVM_EINVAL, "invalid sizes or options")
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=X.device)
+    _check(lib.svm_gram(_ptr(X), n, d, float(gamma), _ptr(G), ld, _ptr(ws), wsb, C.byref(o)))
     return G
 
 

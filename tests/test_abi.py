@@ -37,7 +37,7 @@ def test_struct_layouts_match_header():
     lib = svmx.load()
     o = svmx.svm_options()
     lib.svm_default_options(C.byref(o))
-    assert o.struct_size == C.sizeof(svmx.svm_options) == 80
+    assert o.struct_size == C.sizeof(svmx.svm_options) == 88
     assert o.check_every == 65536 and o.gram == svmx.GRAM_AUTO
     assert C.sizeof(svmx.svm_stats) == 96
 
@@ -54,9 +54,13 @@ def _opts(**kw):
 def test_workspace_sizes():
     lib = svmx.load()
     ws = lambda n, d, **kw: lib.svm_train_workspace_bytes(n, d, C.byref(_opts(**kw)))
-    # full Gram of the 100k x 32 workload: 100000 * ld(100032) * 4 bytes, plus small state
+    # full Gram of the 100k x 32 workload: 100000 * ld(100032) * 4 bytes, plus small state and,
+    # for the default split-fp16 Gram, its scratch (two fp16 halves of X, scales, norms)
     w3 = ws(100_000, 32)
-    assert 4 * 100_000 * 100_032 <= w3 < 4 * 100_000 * 100_032 + (8 << 20)
+    split = 2 * 2 * 100_000 * 32 + 8 * 100_000
+    assert 4 * 100_000 * 100_032 + split <= w3 < 4 * 100_000 * 100_032 + split + (8 << 20)
+    w3f = ws(100_000, 32, gram_mfma=svmx.MFMA_F32)
+    assert 4 * 100_000 * 100_032 <= w3f < 4 * 100_000 * 100_032 + (8 << 20)
     # row path: no Gram
     assert ws(100_000, 32, gram=svmx.GRAM_OFF) < (16 << 20)
     # a Gram budget below the Gram size selects the row path under AUTO
@@ -121,8 +125,15 @@ def test_predict_and_rows_reject():
     assert lib.svm_predict(FAKE, FAKE, FAKE, 0.0, 10, 4, 0.0, FAKE, 10, FAKE, FAKE, 256, C.byref(o)) == -1
     assert lib.svm_predict(FAKE, FAKE, FAKE, float("nan"), 10, 4, 0.5, FAKE, 10, FAKE, FAKE, 256, C.byref(o)) == -1
     assert lib.svm_kernel_rows(FAKE, 10, 4, 0.5, None, 2, FAKE, C.byref(o)) == -1
-    assert lib.svm_gram(FAKE, 10, 4, 0.5, FAKE, 9, C.byref(o)) == -1
-    assert lib.svm_gram(FAKE, 10, 4, -0.5, FAKE, 10, C.byref(o)) == -1
+    assert lib.svm_gram(FAKE, 10, 4, 0.5, FAKE, 9, FAKE, 1 << 20, C.byref(o)) == -1
+    assert lib.svm_gram(FAKE, 10, 4, -0.5, FAKE, 10, FAKE, 1 << 20, C.byref(o)) == -1
+    # the split-fp16 Gram needs scratch: 2 halves x n x (d rounded up to 32) x 2 B + scales and norms
+    assert lib.svm_gram_workspace_bytes(10, 4, C.byref(o)) >= 2 * 2 * 10 * 32 + 8 * 10
+    assert lib.svm_gram(FAKE, 10, 4, 0.5, FAKE, 10, None, 0, C.byref(o)) == -4
+    f32 = _opts(gram_mfma=svmx.MFMA_F32)
+    assert lib.svm_gram_workspace_bytes(10, 4, C.byref(f32)) == 0
+    bad = _opts(gram_mfma=7)
+    assert lib.svm_gram_workspace_bytes(10, 4, C.byref(bad)) == -1
 
 
 def test_predict_workspace_sizes():

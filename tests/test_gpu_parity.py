@@ -88,22 +88,27 @@ def test_row_path_wide_and_unaligned(n, d, misalign):
     np.testing.assert_allclose(out.trace_b[:k], r.trace_b[:k], atol=F_ATOL, rtol=0)
 
 
+MFMAS = [svmx.MFMA_SPLIT_F16, svmx.MFMA_F32]
+
+
+@pytest.mark.parametrize("mfma", MFMAS)
 @pytest.mark.parametrize("cid,n,d", [(0, 1000, 16), (2, 1300, 128), (1, 700, 784), (3, 3001, 32), (0, 333, 13),
                                      (0, 129, 5)])
-def test_gram_small(cid, n, d):
+def test_gram_small(cid, n, d, mfma):
     wl = synth.workload(cid)
     X, _, _, _ = synth.generate(cid, n=n, m=1, d=d)
-    G = svmx.svm_gram(dev(X), wl.gamma, ld=n + 3).cpu().numpy()[:, :n]
+    G = svmx.svm_gram(dev(X), wl.gamma, ld=n + 3, gram_mfma=mfma).cpu().numpy()[:, :n]
     ref = oracle.kernel_rows(X, np.arange(n), wl.gamma)
     assert row_rel_err(G, ref) <= ROW_RTOL
     assert np.all(np.diag(G) == 1.0)
 
 
-@pytest.mark.parametrize("cid", [1, 2])
-def test_gram_sampled_full_size(cid):
+@pytest.mark.parametrize("mfma", MFMAS)
+@pytest.mark.parametrize("cid", [1, 2, 4])
+def test_gram_sampled_full_size(cid, mfma):
     wl = synth.workload(cid)
     X, _, _, _ = synth.generate(cid, m=1)
-    Gd = svmx.svm_gram(dev(X), wl.gamma)
+    Gd = svmx.svm_gram(dev(X), wl.gamma, gram_mfma=mfma)
     rows = np.random.default_rng(7).integers(0, X.shape[0], 6)
     got = Gd[torch.from_numpy(rows).cuda()].cpu().numpy()
     del Gd
@@ -124,11 +129,13 @@ def c0():
     return X, y, Xt, ref
 
 
-@pytest.mark.parametrize("gram,wgs", [(svmx.GRAM_ON, 0), (svmx.GRAM_ON, 3), (svmx.GRAM_ON, 8), (svmx.GRAM_OFF, 0),
-                                      (svmx.GRAM_OFF, 1)])
-def test_train_c0_trace_and_result(c0, gram, wgs):
+@pytest.mark.parametrize("gram,wgs,mfma", [(svmx.GRAM_ON, 0, 0), (svmx.GRAM_ON, 3, 0), (svmx.GRAM_ON, 8, 0),
+                                           (svmx.GRAM_ON, 0, svmx.MFMA_F32), (svmx.GRAM_ON, 8, svmx.MFMA_F32),
+                                           (svmx.GRAM_OFF, 0, 0), (svmx.GRAM_OFF, 1, 0)])
+def test_train_c0_trace_and_result(c0, gram, wgs, mfma):
     X, y, Xt, ref = c0
-    out = svmx.svm_train(dev(X), dev(y), C0.C, C0.gamma, C0.tol, gram=gram, workgroups=wgs, trace_len=1001)
+    out = svmx.svm_train(dev(X), dev(y), C0.C, C0.gamma, C0.tol, gram=gram, workgroups=wgs, trace_len=1001,
+                         gram_mfma=mfma)
     assert out.status == svmx.SVM_OK
     st = out.stats
     assert st["iterations"] == ref.iterations
