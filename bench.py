@@ -14,7 +14,8 @@ step).  ``ovo_row_path`` runs the 45 one-vs-one pairs of the 10-class workload o
 path, all pairs in one launch, for a fixed number of steps (4 n_p d + 21 n_p bytes per pair
 step).  ``paper_shapes`` times single trainings at the shapes of the paper's own runs (102
 features, 200-800 samples per class, binary and nine-class one-vs-one) for context.
-``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
+``workloads`` trains the other binary workloads (1,000 x 16, 50,000 x 128, 100,000 x 32) end to
+end once each.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
 (first SMO steps of the same problem, on this host's cores).
 """
 from __future__ import annotations
@@ -66,6 +67,8 @@ def main():
     ap.add_argument("--row-path-steps", type=int, default=4000, help="SMO steps of the row-path measurement (0 = skip)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time (0 = skip)")
     ap.add_argument("--no-ovo", action="store_true", help="skip the one-vs-one measurement (60000x784, 10 classes)")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the end-to-end trainings of the other binary workloads")
     ap.add_argument("--no-paper-shapes", action="store_true",
                     help="skip the context runs at the paper's shapes (d=102, 200-800 per class)")
     ap.add_argument("--ovo-row-steps", type=int, default=300,
@@ -230,6 +233,29 @@ def main():
             del orow
         del Xod, lod, Xtod, oo
         torch.cuda.empty_cache()
+
+    if not args.no_workloads:
+        # the other binary workloads, end to end (one warm-up and one timed training each)
+        per = {}
+        for cid in (0, 2, 3):
+            if cid == args.workload:
+                continue
+            wk = synth.workload(cid)
+            Xk, yk, _, _ = synth.generate(cid, m=1)
+            Xkd, ykd = torch.from_numpy(Xk).cuda(), torch.from_numpy(yk).cuda()
+            svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            rk = svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol)
+            torch.cuda.synchronize()
+            tk = time.perf_counter() - t1
+            sk = rk.stats
+            per[wk.name] = {"train_seconds": tk, "smo_iterations": sk["iterations"],
+                            "iters_per_s": sk["iterations"] / sk["t_solve"], "gram_seconds": sk["t_gram"],
+                            "us_per_smo_step": 1e6 * sk["t_kernel"] / sk["iterations"], "gram_used": sk["gram_used"]}
+            del Xkd, ykd, rk
+            torch.cuda.empty_cache()
+        result["workloads"] = per
 
     if not args.no_paper_shapes:
         # context runs of the paper's shapes (102 features, 200-800 samples per class; binary and

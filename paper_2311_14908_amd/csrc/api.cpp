@@ -343,25 +343,49 @@ svm_status class_sort(const int32_t *label, int64_t n, int32_t k, hipStream_t st
   return SVM_OK;
 }
 
-// Layout of the prediction scratch for up to ntr training samples and m test samples.
-int64_t predict_scratch_bytes(int64_t ntr, int64_t m) {
+// Layout of the prediction scratch for up to ntr training samples and m test samples of d
+// features: compacted support vectors, partial sums, and the split-fp16 rows of both sets.
+struct PredictWs {
+  PredictScratch ps;
+  SplitX train, test;
+};
+
+int64_t predict_scratch_bytes(int64_t ntr, int64_t m, int64_t d) {
   Layout L;
   L.add(4 * ntr);
   L.add(8 * ntr);
   L.add(8);
   L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1));
+  L.add(gram_split_scratch_bytes(ntr, d));
+  L.add(gram_split_scratch_bytes(std::max<int64_t>(m, 1), d));
   return round_up(L.total, ALIGN);
 }
 
-PredictScratch predict_scratch(void *base, int64_t ntr, int64_t m) {
+PredictWs predict_scratch(void *base, int64_t ntr, int64_t m, int64_t d) {
   Layout L;
   char *b = static_cast<char *>(base);
-  PredictScratch s;
-  s.sv_row = reinterpret_cast<int32_t *>(b + L.add(4 * ntr));
-  s.sv_coef = reinterpret_cast<double *>(b + L.add(8 * ntr));
-  s.count = reinterpret_cast<int64_t *>(b + L.add(8));
-  s.part = reinterpret_cast<double *>(b + L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1)));
-  return s;
+  PredictWs w;
+  w.ps.sv_row = reinterpret_cast<int32_t *>(b + L.add(4 * ntr));
+  w.ps.sv_coef = reinterpret_cast<double *>(b + L.add(8 * ntr));
+  w.ps.count = reinterpret_cast<int64_t *>(b + L.add(8));
+  w.ps.part = reinterpret_cast<double *>(b + L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1)));
+  w.train = split_views(b + L.add(gram_split_scratch_bytes(ntr, d)), ntr, d);
+  w.test = split_views(b + L.add(gram_split_scratch_bytes(std::max<int64_t>(m, 1), d)), std::max<int64_t>(m, 1), d);
+  return w;
+}
+
+// Split rows of the training and test sets for the split-fp16 predict kernel (default), or
+// leave the fp32 kernel selected.
+hipError_t predict_prepare(PredictWs &w, const Opts &r, const float *Xtr, int64_t ntr, const float *T, int64_t m,
+                           int64_t d) {
+  if (r.gram_mfma != SVM_MFMA_SPLIT_F16) return hipSuccess;
+  hipError_t e = launch_split_rows(Xtr, ntr, d, w.train, r.stream);
+  if (e != hipSuccess) return e;
+  e = launch_split_rows(T, m, d, w.test, r.stream);
+  if (e != hipSuccess) return e;
+  w.ps.split_train = &w.train;
+  w.ps.split_test = &w.test;
+  return hipSuccess;
 }
 
 }  // namespace
@@ -522,7 +546,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
 
 int64_t svm_predict_workspace_bytes(int64_t n, int64_t d, int64_t m) {
   if (n < 1 || d < 1 || m < 0 || n > 0x7ffffffeLL || m > (INT64_MAX / 8) / 64 / std::max<int64_t>(n, 1)) return -1;
-  return predict_scratch_bytes(n, m);
+  return predict_scratch_bytes(n, m, d);
 }
 
 svm_status svm_predict(const float *X_train, const int32_t *y, const double *alpha, double b, int64_t n, int64_t d,
@@ -540,8 +564,9 @@ svm_status svm_predict(const float *X_train, const int32_t *y, const double *alp
   if (need < 0) return fail(SVM_ENOMEM, "sizes overflow");
   if (!workspace || workspace_bytes < need)
     return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)need, (long long)workspace_bytes);
-  const PredictScratch ps = predict_scratch(workspace, n, m);
-  HIPCHK(launch_predict_map(X_train, d, 0, n, n, y, nullptr, alpha, n, gamma, X_test, m, b, dec, 1, ps, r.stream));
+  PredictWs pw = predict_scratch(workspace, n, m, d);
+  HIPCHK(predict_prepare(pw, r, X_train, n, X_test, m, d));
+  HIPCHK(launch_predict_map(X_train, d, 0, n, n, y, nullptr, alpha, n, gamma, X_test, m, b, dec, 1, pw.ps, r.stream));
   HIPCHK(hipStreamSynchronize(r.stream));
   return SVM_OK;
 }
@@ -722,7 +747,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
 
 int64_t svm_predict_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, int64_t m) {
   if (n < 2 || d < 1 || k < 2 || k > MAX_CLASSES || m < 0 || n > 0x7ffffffeLL) return -1;
-  return round_up(4 * n, ALIGN) + predict_scratch_bytes(n, m);
+  return round_up(4 * n, ALIGN) + predict_scratch_bytes(n, m, d);
 }
 
 svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k,
@@ -747,7 +772,8 @@ svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int6
   if (s0 != SVM_OK) return s0;
   if (m == 0) return SVM_OK;
   int32_t *dperm = static_cast<int32_t *>(workspace);
-  const PredictScratch ps = predict_scratch(static_cast<char *>(workspace) + round_up(4 * n, ALIGN), n, m);
+  PredictWs pw = predict_scratch(static_cast<char *>(workspace) + round_up(4 * n, ALIGN), n, m, d);
+  HIPCHK(predict_prepare(pw, r, X, n, X_test, m, d));
   HIPCHK(hipMemcpyAsync(dperm, perm.data(), 4 * n, hipMemcpyHostToDevice, r.stream));
   int64_t pack = 0;
   int32_t q = 0;
@@ -755,7 +781,7 @@ svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int6
     for (int32_t bb = a + 1; bb < k; ++bb, ++q) {
       const int64_t np = cnt[a] + cnt[bb];
       HIPCHK(launch_predict_map(X, d, start[a], cnt[a], start[bb], nullptr, dperm, alpha + pack, np, gamma, X_test, m,
-                                b[q], dec + q, P, ps, r.stream));
+                                b[q], dec + q, P, pw.ps, r.stream));
       pack += np;
     }
   HIPCHK(launch_ovo_vote(dec, m, k, pred, r.stream));

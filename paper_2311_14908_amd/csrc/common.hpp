@@ -70,6 +70,16 @@ struct SolveParams {
 hipError_t launch_gram(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, hipStream_t s);
 hipError_t launch_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, const int64_t *rows, int64_t r,
                               float *out, hipStream_t s);
+// Rows of X scaled by powers of two and split into two fp16 halves (gram_split.hip): hi and lo
+// [n][dp] (dp = d rounded up to 32, zero padded), the row scales and the row norms.
+struct SplitX {
+  _Float16 *hi, *lo;
+  float *scale, *nrm;
+  int64_t dp;
+};
+SplitX split_views(void *scratch, int64_t n, int64_t d);
+hipError_t launch_split_rows(const float *X, int64_t n, int64_t d, const SplitX &s, hipStream_t st);
+
 // Split-fp16 Gram (gram_split.hip): scratch bytes, and the build into G.
 int64_t gram_split_scratch_bytes(int64_t n, int64_t d);
 hipError_t launch_gram_split(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, void *scratch,
@@ -87,6 +97,8 @@ struct PredictScratch {
   double *sv_coef;  // [ntr]
   int64_t *count;   // [1]
   double *part;     // [predict_splits(m, ntr)][m]
+  const SplitX *split_train = nullptr;  // split rows of the training X and of the test samples
+  const SplitX *split_test = nullptr;   // (both set: the split-fp16 kernel; host pointers)
 };
 int predict_splits(int64_t m, int64_t nsv_max);
 // Decision values for training samples addressed like Prob (local j -> row off0+j or

@@ -32,13 +32,7 @@ int64_t gram_split_scratch_bytes(int64_t n, int64_t d) {
   return 2 * (2 * n * dp) + 8 * n + 256;
 }
 
-struct SplitX {
-  _Float16 *hi, *lo;
-  float *scale, *nrm;
-  int64_t dp;
-};
-
-static SplitX split_views(void *scratch, int64_t n, int64_t d) {
+SplitX split_views(void *scratch, int64_t n, int64_t d) {
   SplitX s;
   s.dp = split_pitch(d);
   char *p = static_cast<char *>(scratch);
@@ -241,14 +235,18 @@ __global__ void __launch_bounds__(SBS) gram_rbf_f16x3(SplitX s, int64_t n, float
   }
 }
 
+hipError_t launch_split_rows(const float *X, int64_t n, int64_t d, const SplitX &s, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  int64_t pb = (n + 3) / 4;
+  if (pb > 8192) pb = 8192;
+  hipLaunchKernelGGL(gram_split_k, dim3((unsigned)pb), dim3(256), 0, st, X, n, d, s);
+  return hipGetLastError();
+}
+
 hipError_t launch_gram_split(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, void *scratch,
                              hipStream_t st) {
   const SplitX s = split_views(scratch, n, d);
-  int64_t pb = (n + 3) / 4;
-  if (pb > 8192) pb = 8192;
-  if (pb < 1) pb = 1;
-  hipLaunchKernelGGL(gram_split_k, dim3((unsigned)pb), dim3(256), 0, st, X, n, d, s);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_split_rows(X, n, d, s, st);
   if (e != hipSuccess) return e;
   const int64_t nt = (n + ST - 1) / ST;
   const int64_t ntiles = nt * (nt + 1) / 2;

@@ -7,6 +7,9 @@
 //    K = exp2(c * max(0, |t|^2 + |x|^2 - 2 t.x)) with c = -gamma log2(e), and each test row
 //    sums coef * K in fp64 over the tile in a fixed tree.  Support-vector tiles are split
 //    over `nsplit` workgroups per test tile; each split writes its own partial sums.
+//    By default the contraction runs instead on v_mfma_f32_16x16x32_f16 with the rows scaled by
+//    powers of two and split into two fp16 halves, three products per fp32 product, as in the
+//    Gram build (predict_f16x3); `gram_mfma = SVM_MFMA_F32` keeps the fp32 kernel.
 // 3. predict_final: dec = sum over splits (fixed order) - b.
 // Results are deterministic: no atomics touch values.
 #include "common.hpp"
@@ -200,6 +203,141 @@ __global__ void __launch_bounds__(PBS) predict_mfma_k(const float *__restrict__ 
   if (threadIdx.x < PT && q0 + threadIdx.x < m) part[(int64_t)split * m + q0 + threadIdx.x] = row_acc;
 }
 
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+constexpr int PKS = 32;  // k per stage of the split kernel (one MFMA K)
+
+struct PredStage {
+  h8 v[4][PKS / 8][PT];  // [A hi, A lo, B hi, B lo][k chunk of 8][row]
+};
+
+// This thread's share of one stage: rows t/2 of the test tile (A, rows q0..) and of the
+// support-vector tile (B, rows sv_row[s0..]), k chunks 2*(t%2), +1.  Rows past the end are 0.
+__device__ __forceinline__ void pred_split_load(const SplitX &st, const SplitX &sx, int64_t m, int64_t q0,
+                                                const int32_t *__restrict__ sv_row, int64_t nsv, int64_t s0, int64_t k0,
+                                                h8 (&r)[8]) {
+  const int t = threadIdx.x;
+  const int row = t >> 1, kq = (t & 1) * 2;
+  const int64_t qa = q0 + row, qb = s0 + row;
+  const bool va = qa < m, vb = qb < nsv;
+  const int64_t rb = vb ? (int64_t)sv_row[qb] : 0;
+#pragma unroll
+  for (int sl = 0; sl < 4; ++sl) {
+    const bool v = sl < 2 ? va : vb;
+    const SplitX &S = sl < 2 ? st : sx;
+    const int64_t g = sl < 2 ? qa : rb;
+    const _Float16 *base = (sl & 1) ? S.lo : S.hi;
+    if (v) {
+      const h8 *p = reinterpret_cast<const h8 *>(base + g * S.dp + k0) + kq;
+      r[2 * sl] = p[0];
+      r[2 * sl + 1] = p[1];
+    } else {
+      r[2 * sl] = (h8){};
+      r[2 * sl + 1] = (h8){};
+    }
+  }
+}
+
+__device__ __forceinline__ void pred_split_store(PredStage &S, const h8 (&r)[8]) {
+  const int t = threadIdx.x;
+  const int row = t >> 1, kq = (t & 1) * 2;
+#pragma unroll
+  for (int sl = 0; sl < 4; ++sl) {
+    S.v[sl][kq][row] = r[2 * sl];
+    S.v[sl][kq + 1][row] = r[2 * sl + 1];
+  }
+}
+
+// predict_mfma_k on the split representation: st holds the test rows, sx the training rows
+// (support vectors addressed through sv_row); dot = acc * s_q * s_j.
+__global__ void __launch_bounds__(PBS) predict_f16x3_k(SplitX st, int64_t m, SplitX sx,
+                                                       const int32_t *__restrict__ sv_row,
+                                                       const double *__restrict__ sv_coef,
+                                                       const int64_t *__restrict__ sv_count, float c, int nsplit,
+                                                       double *__restrict__ part) {
+  __shared__ PredStage S[2];
+  __shared__ float sA[PT], nA[PT], sB[PT], nB[PT];
+  __shared__ double cB[PT];
+  __shared__ double rs[2][PT];
+  const int64_t nsv = *sv_count;
+  const int64_t q0 = (int64_t)blockIdx.x * PT;
+  const int split = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int kq = lane >> 4, r16 = lane & 15;
+  if (threadIdx.x < PT) {
+    const int64_t q = q0 + threadIdx.x;
+    sA[threadIdx.x] = q < m ? st.scale[q] : 0.f;
+    nA[threadIdx.x] = q < m ? st.nrm[q] : 0.f;
+  }
+  double row_acc = 0.0;  // thread t < 128 owns test row q0 + t
+  const int64_t ntile = (nsv + PT - 1) / PT;
+  const int64_t stages = st.dp / PKS;
+  for (int64_t tile = split; tile < ntile; tile += nsplit) {
+    const int64_t s0 = tile * PT;
+    if (threadIdx.x < PT) {
+      const int64_t q = s0 + threadIdx.x;
+      const int64_t rr = q < nsv ? (int64_t)sv_row[q] : -1;
+      sB[threadIdx.x] = rr >= 0 ? sx.scale[rr] : 0.f;
+      nB[threadIdx.x] = rr >= 0 ? sx.nrm[rr] : 0.f;
+      cB[threadIdx.x] = rr >= 0 ? sv_coef[q] : 0.0;
+    }
+    v4f acc[4][4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = (v4f){0.f, 0.f, 0.f, 0.f};
+    h8 r[8];
+    pred_split_load(st, sx, m, q0, sv_row, nsv, s0, 0, r);
+    pred_split_store(S[0], r);
+    __syncthreads();
+    for (int64_t sg = 0; sg < stages; ++sg) {
+      const int cur = (int)(sg & 1);
+      if (sg + 1 < stages) pred_split_load(st, sx, m, q0, sv_row, nsv, s0, (sg + 1) * PKS, r);
+      h8 ah[4], al[4], bh[4], bl[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        ah[a] = S[cur].v[0][kq][wm * 64 + a * 16 + r16];
+        al[a] = S[cur].v[1][kq][wm * 64 + a * 16 + r16];
+        bh[a] = S[cur].v[2][kq][wn * 64 + a * 16 + r16];
+        bl[a] = S[cur].v[3][kq][wn * 64 + a * 16 + r16];
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bh[b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bl[b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[a], bh[b], acc[a][b], 0, 0, 0);
+        }
+      if (sg + 1 < stages) pred_split_store(S[cur ^ 1], r);
+      __syncthreads();
+    }
+    // per test row: sum over this wave's 64 columns (4 blocks x 16 lanes), then the two halves
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int lr = wm * 64 + a * 16 + 4 * kq + e;
+        double sacc = 0.0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int lc = wn * 64 + b * 16 + r16;
+          const float dot = (acc[a][b][e] * sA[lr]) * sB[lc];
+          float t = nA[lr] + nB[lc] - 2.0f * dot;
+          t = t > 0.f ? t : 0.f;
+          sacc = __builtin_fma(cB[lc], (double)__builtin_amdgcn_exp2f(c * t), sacc);
+        }
+        sacc = row16_sum(sacc);
+        if (r16 == 0) rs[wn][lr] = sacc;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < PT) row_acc += rs[0][threadIdx.x] + rs[1][threadIdx.x];
+    __syncthreads();
+  }
+  if (threadIdx.x < PT && q0 + threadIdx.x < m) part[(int64_t)split * m + q0 + threadIdx.x] = row_acc;
+}
+
 __global__ void predict_final_k(const double *__restrict__ part, int64_t m, int nsplit, double b, double *dec,
                                 int64_t stride) {
   const int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -225,6 +363,7 @@ hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t
                               const float *T, int64_t m, double b, double *dec, int64_t dec_stride,
                               const PredictScratch &ws, hipStream_t s) {
   if (m <= 0) return hipSuccess;
+  const bool split = ws.split_test != nullptr && ws.split_train != nullptr;
   PredMap map{off0, len0, off1, y, perm};
   hipLaunchKernelGGL(sv_compact_k, dim3(1), dim3(1024), 0, s, alpha, ntr, map, ws.sv_row, ws.sv_coef, ws.count);
   hipError_t e = hipGetLastError();
@@ -234,7 +373,10 @@ hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t
   dim3 grid((unsigned)((m + PT - 1) / PT), (unsigned)nsplit);
   const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(T) & 15) == 0) &&
                     ((reinterpret_cast<uintptr_t>(Xtr) & 15) == 0);
-  if (vec4)
+  if (split)
+    hipLaunchKernelGGL(predict_f16x3_k, grid, dim3(PBS), 0, s, *ws.split_test, m, *ws.split_train, ws.sv_row,
+                       ws.sv_coef, ws.count, c, nsplit, ws.part);
+  else if (vec4)
     hipLaunchKernelGGL(predict_mfma_k<true>, grid, dim3(PBS), 0, s, T, m, Xtr, ws.sv_row, ws.sv_coef, ws.count, d, c,
                        nsplit, ws.part);
   else

@@ -266,13 +266,14 @@ def test_deterministic_repeat():
 
 # --- predict ----------------------------------------------------------------------------------
 
+@pytest.mark.parametrize("mfma", MFMAS)
 @pytest.mark.parametrize("cid,n,m,d", [(0, 1500, 777, 16), (2, 1500, 777, 128), (1, 700, 300, 784), (0, 300, 129, 13)])
-def test_predict_matches_oracle_given_alpha(cid, n, m, d):
+def test_predict_matches_oracle_given_alpha(cid, n, m, d, mfma):
     wl = synth.workload(cid)
     X, y, Xt, _ = synth.generate(cid, n=n, m=m, d=d)
     r = oracle.train(X, y, wl.C, wl.gamma, wl.tol)
     d_ref = oracle.decision(X, y, r.alpha, r.b, Xt, wl.gamma)
-    d_gpu = svmx.svm_predict(dev(X), dev(y), dev(r.alpha), r.b, wl.gamma, dev(Xt)).cpu().numpy()
+    d_gpu = svmx.svm_predict(dev(X), dev(y), dev(r.alpha), r.b, wl.gamma, dev(Xt), gram_mfma=mfma).cpu().numpy()
     # same alpha and b: the only difference is the fp32 kernel values of the MFMA path
     assert np.max(np.abs(d_gpu - d_ref)) <= PRED_ATOL
 
