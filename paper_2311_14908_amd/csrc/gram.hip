@@ -7,6 +7,7 @@
 // kernel is the Gaussian RBF the paper names (Section III.C).
 #include "common.hpp"
 #include "rbf_rows.hpp"
+#include "tile_order.hpp"
 
 #include <math.h>
 
@@ -54,8 +55,8 @@ __device__ __forceinline__ void load_slab(const float *__restrict__ X, int64_t n
 
 // One 128x128 tile (rows i0.., columns j0..) of the Gram for each tile with ti <= tj (the
 // upper triangle); a tile off the diagonal is stored twice, as itself and mirrored.  Tiles are
-// handed out XCD-major: consecutive workgroups of one XCD take consecutive tiles of one tile
-// row, so they share its row slab in that XCD's L2.  The RBF map is exp2(c * t) with
+// handed out XCD-major in super-tile order (tile_order.hpp): the workgroups one XCD holds at
+// once share their row and column slabs in that XCD's L2.  The RBF map is exp2(c * t) with
 // c = -gamma * log2(e) and t = |x_i|^2 + |x_j|^2 - 2 x_i.x_j clamped at 0 (v_exp_f32).
 template <bool VEC4, bool STORE4>
 __global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X, int64_t n, int64_t d, float c,
@@ -63,19 +64,13 @@ __global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X
   __shared__ float As[GKC][GPAD];
   __shared__ float Bs[GKC][GPAD];
   __shared__ float nA[GT], nB[GT];
-  // XCD-major swizzle of the linear tile index, then (ti, tj) of the upper triangle
+  // XCD-major swizzle of the linear tile index, then (ti, tj) in super-tile order
   const int64_t per_xcd = (ntiles + 7) / 8;
   const int64_t b = (int64_t)blockIdx.x;
   const int64_t lin = (b % 8) * per_xcd + b / 8;
   if (lin >= ntiles) return;
-  // row ti starts at s(ti) = ti*nt - ti*(ti-1)/2; invert with a square root and fix up
-  const double tw = 2.0 * (double)nt + 1.0;
-  int64_t ti = (int64_t)((tw - sqrt(tw * tw - 8.0 * (double)lin)) * 0.5);
-  if (ti < 0) ti = 0;
-  if (ti >= nt) ti = nt - 1;
-  while (ti > 0 && ti * nt - ti * (ti - 1) / 2 > lin) --ti;
-  while ((ti + 1) * nt - (ti + 1) * ti / 2 <= lin) ++ti;
-  const int64_t tj = ti + (lin - (ti * nt - ti * (ti - 1) / 2));
+  int64_t ti, tj;
+  upper_tile_super(lin, nt, ti, tj);
   const int64_t i0 = ti * GT, j0 = tj * GT;
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;

@@ -11,6 +11,7 @@
 // are as accurate as those of the fp32 MFMA kernel.  The row norms are fp64 sums of the fp32
 // inputs.
 #include "common.hpp"
+#include "tile_order.hpp"
 
 #include <math.h>
 
@@ -79,17 +80,6 @@ __global__ void __launch_bounds__(256) gram_split_k(const float *__restrict__ X,
   }
 }
 
-// (ti, tj) of linear upper-triangle tile index lin (row ti starts at ti*nt - ti*(ti-1)/2).
-__device__ __forceinline__ void upper_tile(int64_t lin, int64_t nt, int64_t &ti, int64_t &tj) {
-  const double tw = 2.0 * (double)nt + 1.0;
-  ti = (int64_t)((tw - sqrt(tw * tw - 8.0 * (double)lin)) * 0.5);
-  if (ti < 0) ti = 0;
-  if (ti >= nt) ti = nt - 1;
-  while (ti > 0 && ti * nt - ti * (ti - 1) / 2 > lin) --ti;
-  while ((ti + 1) * nt - (ti + 1) * ti / 2 <= lin) ++ti;
-  tj = ti + (lin - (ti * nt - ti * (ti - 1) / 2));
-}
-
 // LDS stage: [slab: A hi, A lo, B hi, B lo][k chunk of 8][row] of 16-byte vectors, so the 16
 // lanes that read one MFMA operand read 256 contiguous bytes.
 struct SplitStage {
@@ -125,8 +115,10 @@ __device__ __forceinline__ void split_store(SplitStage &S, const h8 (&r)[8]) {
   }
 }
 
-// One 128x128 tile of the upper triangle per workgroup (XCD-major order as in gram.hip); an
-// off-diagonal tile is stored twice, as itself and mirrored.  Lane l of an MFMA holds
+// One 128x128 tile of the upper triangle per workgroup; workgroup b runs on XCD b % 8 and takes
+// tile b / 8 of that XCD's contiguous share of the super-tile order (tile_order.hpp), so the
+// tiles an XCD holds at once share their row and column slabs in its L2.  An off-diagonal
+// tile is stored twice, as itself and mirrored.  Lane l of an MFMA holds
 // D[4*(l/16) + e][l%16] of each 16x16 block.
 template <bool STORE4>
 __global__ void __launch_bounds__(SBS) gram_rbf_f16x3(SplitX s, int64_t n, float c, float *__restrict__ G, int64_t ld,
@@ -138,7 +130,7 @@ __global__ void __launch_bounds__(SBS) gram_rbf_f16x3(SplitX s, int64_t n, float
   const int64_t lin = (b % 8) * per_xcd + b / 8;
   if (lin >= ntiles) return;
   int64_t ti, tj;
-  upper_tile(lin, nt, ti, tj);
+  upper_tile_super(lin, nt, ti, tj);
   const int64_t i0 = ti * ST, j0 = tj * ST;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w >> 1, wn = w & 1;
