@@ -657,20 +657,42 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
       }
     return SVM_OK;
   };
-  // Shrink the budget until the variant the shapes need fits on the device at once.
+  // Shrink the budget until the variant the shapes need fits on the device at once; with more
+  // pairs than that even at one workgroup each, the pairs run in consecutive batches (one
+  // cooperative launch sequence per batch).
   int64_t budget = OVO_TOTAL_WG;
+  int32_t capacity = 0;
   for (;;) {
     s0 = assign(budget);
     if (s0 != SVM_OK) return s0;
     SolveParams probe{};
     probe.X = Xs;
     probe.d = d;
-    int32_t capacity = 0;
     HIPCHK(launch_solver(probe, 0, per_thread, p.gram, stream, &capacity));
-    if (wg <= capacity) break;
-    if (budget <= p.P || capacity <= 0)
-      return fail(SVM_ENOMEM, "%d solver workgroups do not fit on the device at once (at most %d)", wg, capacity);
+    if (capacity <= 0) return fail(SVM_ENOMEM, "the solver does not fit on the device");
+    if (wg <= capacity || budget <= p.P) break;
     budget = std::max<int64_t>(p.P, std::min<int64_t>(budget - 1, capacity));
+  }
+  std::vector<int32_t> bstart{0}, bwg;  // batch boundaries over the pairs, workgroups per batch
+  {
+    int32_t acc = 0;
+    for (int32_t q = 0; q < p.P; ++q) {
+      if (hp[q].nwg > capacity)
+        return fail(SVM_ENOMEM, "pair %d needs %d workgroups, the device holds %d at once", q, hp[q].nwg, capacity);
+      if (acc + hp[q].nwg > capacity) {
+        bwg.push_back(acc);
+        bstart.push_back(q);
+        acc = 0;
+      }
+      hp[q].wg0 = acc;  // relative to its batch's launch
+      acc += hp[q].nwg;
+    }
+    bwg.push_back(acc);
+    bstart.push_back(p.P);
+    hwgp.clear();  // workgroup -> pair index within its batch
+    for (size_t bi = 0; bi + 1 < bstart.size(); ++bi)
+      for (int32_t q = bstart[bi]; q < bstart[bi + 1]; ++q)
+        for (int32_t w = 0; w < hp[q].nwg; ++w) hwgp.push_back(q - bstart[bi]);
   }
   HIPCHK(hipMemcpyAsync(dperm, perm.data(), 4 * n, hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(dprob, hp.data(), sizeof(Prob) * hp.size(), hipMemcpyHostToDevice, stream));
@@ -711,8 +733,22 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   int32_t launches = 0;
   std::vector<Ctl> hc;
   double t_kernel = 0.0;
-  svm_status s1 = run_solver(sp, p.P, wg, per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel);
-  if (s1 != SVM_OK) return s1;
+  int32_t woff = 0;
+  for (size_t bi = 0; bi + 1 < bstart.size(); ++bi) {
+    SolveParams sb = sp;
+    sb.probs = dprob + bstart[bi];
+    sb.wg_prob = wgp + woff;
+    std::vector<Ctl> hb;
+    int32_t lb = 0;
+    double tb = 0.0;
+    svm_status s1 = run_solver(sb, bstart[bi + 1] - bstart[bi], bwg[bi], per_thread, p.gram, ctl + bstart[bi], stream,
+                               &lb, hb, &tb);
+    if (s1 != SVM_OK) return s1;
+    launches += lb;
+    t_kernel += tb;
+    hc.insert(hc.end(), hb.begin(), hb.end());
+    woff += bwg[bi];
+  }
   HIPCHK(hipEventRecord(ts.b, stream));
   HIPCHK(hipEventRecord(tf.a, stream));
   HIPCHK(launch_finalize(dprob, p.P, C, fin, stream));

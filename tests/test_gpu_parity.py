@@ -366,6 +366,32 @@ def test_paper_shaped_context_runs():
     assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
 
 
+def test_ovo_many_classes_in_batches():
+    """64 classes: 2016 pairs.  On the row path the device holds fewer pair workgroups than
+    that at once, so the pairs run in consecutive launches; every pair must still equal a
+    standalone binary solve of it, bit for bit, and the votes must match the oracle's."""
+    k = 64
+    X, lab = synth.multiclass_blobs(640, 8, k, seed=3)
+    out = svmx.svm_train_ovo(dev(X), dev(lab), k, 1.0, 0.5, 1e-3, gram=svmx.GRAM_OFF)
+    assert out.status == svmx.SVM_OK
+    assert out.stats[0]["launches"] > 1  # batched
+    offs, sizes = svmx.ovo_offsets(lab, k)
+    pairs = oracle.ovo_pairs(k)
+    for p in (0, 1, 255, 256, 1000, len(pairs) - 1):
+        a, b = pairs[p]
+        idx, y = oracle.ovo_local(lab, a, b)
+        r = svmx.svm_train(dev(X[idx]), dev(y), 1.0, 0.5, 1e-3, gram=svmx.GRAM_OFF)
+        assert torch.equal(out.alpha[offs[p]:offs[p] + sizes[p]], r.alpha), f"pair {p}"
+        assert out.b[p] == r.b
+    models = oracle.train_ovo(X, lab, k, 1.0, 0.5, 1e-5)
+    dec_ref, pred_ref = oracle.predict_ovo(X, lab, k, models, X, 0.5)
+    out5 = svmx.svm_train_ovo(dev(X), dev(lab), k, 1.0, 0.5, 1e-5, gram=svmx.GRAM_OFF)
+    dec, pred = svmx.svm_predict_ovo(dev(X), dev(lab), k, out5.alpha, out5.b, 0.5, dev(X))
+    assert np.max(np.abs(dec.cpu().numpy() - dec_ref)) <= DEC_ATOL
+    sure = np.all(np.abs(dec_ref) >= DEC_ATOL, axis=1)
+    assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
+
+
 def test_ovo_predict_matches_oracle_given_alpha():
     k = 5
     X, lab, Xt, _ = synth.generate(4, n=500, m=200, d=12, classes=k)
