@@ -91,6 +91,24 @@ def test_row_path_wide_and_unaligned(n, d, misalign):
 MFMAS = [svmx.MFMA_SPLIT_F16, svmx.MFMA_F32]
 
 
+def test_row_path_largest_placement():
+    """The largest problem the row path places: 256 workgroups of 512 threads with 8 samples a
+    thread (n just below 2^20).  The first 40 steps against the oracle: selections, b_up/b_low
+    and the multipliers they moved."""
+    n, d = 1_048_000, 16
+    X, y = synth.two_blobs(n, d, seed=5)
+    steps = 40
+    r = oracle.train(X, y, 1.0, 1.0 / d, 1e-3, max_iter=steps, trace_len=steps)
+    out = svmx.svm_train(dev(X), dev(y), 1.0, 1.0 / d, 1e-3, gram=svmx.GRAM_OFF, max_iter=steps, trace_len=steps)
+    assert out.status == svmx.SVM_NOT_CONVERGED and out.stats["iterations"] == steps
+    tied = np.flatnonzero(np.asarray(r.trace_gap)[1:].min(axis=1) < 1e-6)
+    k = min(steps, int(tied[0]) + 1 if tied.size else steps)
+    np.testing.assert_array_equal(out.trace_ul[:k], r.trace_ul[:k])
+    np.testing.assert_allclose(out.trace_b[:k], r.trace_b[:k], atol=F_ATOL, rtol=0)
+    if k == steps:
+        np.testing.assert_allclose(out.alpha.cpu().numpy(), r.alpha, atol=1e-5, rtol=0)
+
+
 @pytest.mark.parametrize("mfma", MFMAS)
 @pytest.mark.parametrize("cid,n,d", [(0, 1000, 16), (2, 1300, 128), (1, 700, 784), (3, 3001, 32), (0, 333, 13),
                                      (0, 129, 5)])
