@@ -7,9 +7,10 @@
 // Each step:
 //   1. every workgroup selects its own candidates  u_r = argmin_{I_up} f,  l_r = argmax_{I_low} f
 //      (ties to the smaller index) with DPP wave reductions and one LDS hand-off;
-//   2. the nwg partial results are exchanged through global memory as self-stamped 64-bit
-//      words (payload | step stamp), so no fence or cache flush is needed: a reader simply
-//      waits until every word it needs carries the current stamp.  With one level every
+//   2. the nwg partial results are exchanged through global memory as records of six
+//      self-stamped 64-bit words (step stamp | payload, xchg_record.hpp), so no fence or cache
+//      flush is needed: a reader simply waits until every word it needs carries the current
+//      stamp.  With one level every
 //      workgroup polls all records, one record per lane over as many waves as needed; with
 //      two levels (the default above 128 workgroups) group leaders reduce about sqrt(nwg)
 //      records each and publish a group record, and every workgroup then reads the group
@@ -23,6 +24,7 @@
 // all waits end, so a launch always drains.
 #include "common.hpp"
 #include "rbf_rows.hpp"
+#include "xchg_record.hpp"
 
 #include <math.h>
 
@@ -164,34 +166,25 @@ __device__ __forceinline__ void st_word(u64 *p, u64 v) { __hip_atomic_store(p, v
 __device__ __forceinline__ u64 ld_word(const u64 *p) {
   return __hip_atomic_load(const_cast<u64 *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ u64 stamp_word(unsigned stamp, unsigned payload) { return ((u64)stamp << 32) | payload; }
-__device__ __forceinline__ double join_double(u64 hi, u64 lo) {
-  return __longlong_as_double((long long)(((hi & 0xffffffffull) << 32) | (lo & 0xffffffffull)));
-}
 __device__ __forceinline__ unsigned pack_index(int i, int y) { return (unsigned)i | (y < 0 ? 0x80000000u : 0u); }
 
-// Exchange record (10 words): vu hi, vu lo, iu|yu, au hi, au lo, vl hi, vl lo, il|yl, al hi,
-// al lo; the label travels in bit 31 of the index word.  Lanes 0..9 of the calling wave each
-// write one word.
+// Limbs of a record (xchg_record.hpp): v_up, a_up, index words, v_low, a_low; the label travels
+// in bit 31 of the index word.
+__device__ __forceinline__ void sel_limbs(const Sel &s, u64 (&L)[5]) {
+  L[0] = (u64)__double_as_longlong(s.vu);
+  L[1] = (u64)__double_as_longlong(s.au);
+  L[2] = (u64)pack_index(s.iu, s.yu) | ((u64)pack_index(s.il, s.yl) << 32);
+  L[3] = (u64)__double_as_longlong(s.vl);
+  L[4] = (u64)__double_as_longlong(s.al);
+}
+
+// Lanes 0..REC_WORDS-1 of the calling wave each write one word of the record.
 __device__ __forceinline__ void put_record(u64 *rec, unsigned stamp, const Sel &s) {
   const int t = threadIdx.x & 63;
-  if (t < 10) {
-    const u64 bvu = (u64)__double_as_longlong(s.vu), bau = (u64)__double_as_longlong(s.au);
-    const u64 bvl = (u64)__double_as_longlong(s.vl), bal = (u64)__double_as_longlong(s.al);
-    unsigned pl;
-    switch (t) {
-      case 0: pl = (unsigned)(bvu >> 32); break;
-      case 1: pl = (unsigned)bvu; break;
-      case 2: pl = pack_index(s.iu, s.yu); break;
-      case 3: pl = (unsigned)(bau >> 32); break;
-      case 4: pl = (unsigned)bau; break;
-      case 5: pl = (unsigned)(bvl >> 32); break;
-      case 6: pl = (unsigned)bvl; break;
-      case 7: pl = pack_index(s.il, s.yl); break;
-      case 8: pl = (unsigned)(bal >> 32); break;
-      default: pl = (unsigned)bal; break;
-    }
-    st_word(rec + t, stamp_word(stamp, pl));
+  if (t < REC_WORDS) {
+    u64 L[5];
+    sel_limbs(s, L);
+    st_word(rec + t, rec_word(L, t, stamp));
   }
 }
 
@@ -204,14 +197,14 @@ __device__ Sel poll_reduce(const u64 *words, int q0, int q1, int stride, unsigne
   sel_init(s);
   for (int q = q0 + (int)(threadIdx.x & 63); q < q1; q += stride) {
     const u64 *rec = words + (size_t)q * SLOT_WORDS;
-    u64 w[10];
+    u64 w[REC_WORDS];
     const uint64_t t0 = wall_clock64();
     for (;;) {
       bool ok = true;
 #pragma unroll
-      for (int k = 0; k < 10; ++k) {
+      for (int k = 0; k < REC_WORDS; ++k) {
         w[k] = ld_word(rec + k);
-        ok = ok && ((unsigned)(w[k] >> 32) == stamp);
+        ok = ok && rec_stamped(w[k], stamp);
       }
       if (ok) break;
       if (wall_clock64() - t0 > spin_limit) {
@@ -220,15 +213,17 @@ __device__ Sel poll_reduce(const u64 *words, int q0, int q1, int stride, unsigne
         break;
       }
     }
+    u64 L[5];
+    rec_limbs(w, L);
     Sel o;
-    o.vu = join_double(w[0], w[1]);
-    o.iu = (int)((unsigned)w[2] & 0x7fffffffu);
-    o.yu = ((unsigned)w[2] >> 31) ? -1 : 1;
-    o.au = join_double(w[3], w[4]);
-    o.vl = join_double(w[5], w[6]);
-    o.il = (int)((unsigned)w[7] & 0x7fffffffu);
-    o.yl = ((unsigned)w[7] >> 31) ? -1 : 1;
-    o.al = join_double(w[8], w[9]);
+    o.vu = __longlong_as_double((long long)L[0]);
+    o.au = __longlong_as_double((long long)L[1]);
+    o.iu = (int)((unsigned)L[2] & 0x7fffffffu);
+    o.yu = ((unsigned)L[2] >> 31) ? -1 : 1;
+    o.il = (int)((unsigned)(L[2] >> 32) & 0x7fffffffu);
+    o.yl = ((unsigned)(L[2] >> 32) >> 31) ? -1 : 1;
+    o.vl = __longlong_as_double((long long)L[3]);
+    o.al = __longlong_as_double((long long)L[4]);
     sel_merge(s, o);
   }
   return sel_wave(s);

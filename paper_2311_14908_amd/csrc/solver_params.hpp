@@ -43,7 +43,7 @@ struct Prob {
   int32_t pad;
 };
 
-constexpr int SLOT_WORDS = 16;  // 10 used; a record fills one 128-byte line
+constexpr int SLOT_WORDS = 16;  // 6 used; a record sits alone in one 128-byte line
 
 // Launch-wide parameters of the persistent solver.
 struct SolveParams {

@@ -1,7 +1,7 @@
-"""The Gram kernels enumerate upper-triangle tiles in super-tile order (csrc/tile_order.hpp);
-compiled for the host, the mapping must hit every tile (ti <= tj < nt) exactly once."""
+"""Host checks of index and bit arithmetic that the gfx950 kernels use, compiled with hipcc
+for the host: the upper-triangle tile order of the Gram kernels (csrc/tile_order.hpp) hits every
+tile exactly once, and the solver's exchange record (csrc/xchg_record.hpp) round-trips."""
 import os
-import shutil
 import subprocess
 
 import pytest
@@ -11,10 +11,18 @@ CSRC = os.path.join(os.path.dirname(HERE), "paper_2311_14908_amd", "csrc")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 
+def _run(src, tmp_path):
+    exe = tmp_path / os.path.splitext(src)[0]
+    subprocess.run([HIPCC, "-O2", "-x", "hip", "--offload-arch=gfx950", "-I", CSRC, os.path.join(HERE, src), "-o",
+                    str(exe)], check=True, capture_output=True)
+    return subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+
+
 @pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
 def test_tile_order_is_bijective(tmp_path):
-    exe = tmp_path / "tile_order_check"
-    subprocess.run([HIPCC, "-O2", "-x", "hip", "--offload-arch=gfx950", "-I", CSRC,
-                    os.path.join(HERE, "tile_order_check.cpp"), "-o", str(exe)], check=True, capture_output=True)
-    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
-    assert out.startswith("ok")
+    assert _run("tile_order_check.cpp", tmp_path).startswith("ok")
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
+def test_exchange_record_round_trip(tmp_path):
+    assert _run("xchg_record_check.cpp", tmp_path).startswith("ok")
