@@ -56,6 +56,12 @@ def _load():
         lib.oracle_f_from_alpha.restype = None
         lib.oracle_f_from_alpha.argtypes = [P, P, P, C.c_int64, C.c_int64, C.c_int, C.c_double, P, C.c_int64, P,
                                             C.c_int]
+        lib.oracle_train_ws.restype = C.c_int
+        lib.oracle_train_ws.argtypes = [P, P, C.c_int64, C.c_int64, C.c_int, C.c_double, C.c_double, C.c_double,
+                                        C.c_int64, C.c_double, C.c_int64, C.c_int64, C.c_int64, C.c_int, P, P,
+                                        C.POINTER(_Res), P, C.c_int64, P, P, C.c_int64, P]
+        lib.oracle_ws_select.restype = C.c_int64
+        lib.oracle_ws_select.argtypes = [P, P, P, C.c_int64, C.c_double, C.c_int64, P]
         lib.oracle_max_threads.restype = C.c_int
         lib.oracle_max_threads.argtypes = []
         _lib = lib
@@ -119,6 +125,65 @@ def train(X, y, C_, gamma, tol, *, kind=RBF, max_iter=None, cache_bytes=8 << 30,
                        status=int(res.status), f=f,
                        trace_ul=tul[:steps].copy() if tl else None, trace_b=tb[:steps].copy() if tl else None,
                        trace_gap=tg[:steps].copy() if tl else None)
+
+
+# Working-set variant: local tolerance factor and per-round step cap used unless given.
+WS_FRAC = 0.1
+WS_INNER_PER_Q = 100
+
+
+@dataclass
+class WsResult(TrainResult):
+    rounds: int = 0
+    ws_trace: np.ndarray | None = None  # [rounds, q] int32 working sets, -1 padded
+
+
+def train_ws(X, y, C_, gamma, tol, q, *, kind=RBF, frac=WS_FRAC, max_inner=None, max_iter=None,
+             cache_bytes=8 << 30, threads=None, trace_len=0, ws_trace_len=0, want_f=False) -> WsResult:
+    """Working-set decomposition: rounds of two-multiplier SMO steps on q samples (q = 2 is
+    the maximal-violating-pair SMO of ``train``)."""
+    lib = _load()
+    X = _f32(X)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    n, d = X.shape
+    if max_iter is None:
+        max_iter = max(10_000_000, 100 * n)
+    if max_inner is None:
+        max_inner = WS_INNER_PER_Q * int(q)
+    threads = max_threads() if threads is None else int(threads)
+    alpha = np.zeros(n, dtype=np.float64)
+    f = np.zeros(n, dtype=np.float64) if want_f else None
+    res = _Res()
+    rounds = C.c_int64(0)
+    tl, wl = int(trace_len), int(ws_trace_len)
+    tul = np.full((max(tl, 1), 2), -1, dtype=np.int32)
+    tb = np.full((max(tl, 1), 2), np.nan, dtype=np.float64)
+    wst = np.full((max(wl, 1), int(q)), -1, dtype=np.int32)
+    rc = lib.oracle_train_ws(_p(X), _p(y), n, d, int(kind), float(C_), float(gamma), float(tol), int(q), float(frac),
+                             int(max_inner), int(max_iter), int(cache_bytes), threads, _p(alpha),
+                             _p(f) if f is not None else None, C.byref(res), C.byref(rounds), tl, _p(tul), _p(tb), wl,
+                             _p(wst))
+    if rc < 0:
+        raise ValueError(f"oracle_train_ws rejected its input (status {rc})")
+    r = int(rounds.value)
+    steps = min(tl, r + 1) if tl else 0
+    return WsResult(alpha=alpha, b=res.b, b_up=res.b_up, b_low=res.b_low, dual_obj=res.dual_obj,
+                    iterations=int(res.iterations), n_sv=int(res.n_sv), n_bound=int(res.n_bound),
+                    status=int(res.status), f=f,
+                    trace_ul=tul[:steps].copy() if tl else None, trace_b=tb[:steps].copy() if tl else None,
+                    rounds=r, ws_trace=wst[:min(wl, r)].copy() if wl else None)
+
+
+def ws_select(f, y, alpha, C_, q) -> np.ndarray:
+    """The working set a round of ``train_ws`` takes for the given f and alpha."""
+    f = np.ascontiguousarray(f, dtype=np.float64)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    alpha = np.ascontiguousarray(alpha, dtype=np.float64)
+    B = np.full(int(q), -1, dtype=np.int64)
+    m = _load().oracle_ws_select(_p(f), _p(y), _p(alpha), f.shape[0], float(C_), int(q), _p(B))
+    if m < 0:
+        raise ValueError("oracle_ws_select rejected its input")
+    return B[:m].copy()
 
 
 def kernel_value(a, b, gamma, kind=RBF) -> float:

@@ -256,6 +256,211 @@ int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kin
   return status;
 }
 
+/*
+ * Working-set decomposition (the paper states only the two-multiplier step, Section III.B;
+ * this is the reading used for the working-set variant of that step).  Each round:
+ *   1. b_up, b_low and the stop rule exactly as in oracle_train;
+ *   2. the working set B: the q/2 members of I_up with the smallest (f_i, i), in that order,
+ *      then those of the q/2 members of I_low with the largest f_i (ties to the smaller i)
+ *      that are not already in B -- between q/2 and q samples;
+ *   3. the sub-problem on B, all other multipliers fixed, by the two-multiplier steps of
+ *      oracle_train restricted to B (pair, clipping and snapping as there; ties in the
+ *      selection to the smaller global index) on a copy of f_B, until its own gap is at most
+ *      max(tol, frac * gap of the round) or max_inner steps were taken;
+ *   4. f_j += s_j for every j, s_j = sum over p in B (in B's order, c_p != 0) of c_p K(B_p, j)
+ *      with c_p = (a_new - a_old) y at B_p, accumulated from zero.
+ * With q = 2 a round is one step of oracle_train (same pair, same update, same rounding).
+ * iterations counts two-multiplier steps; max_iter bounds their total.  For the first
+ * ws_trace_len rounds B is written to ws_trace (q entries per round, -1 padded).
+ */
+typedef struct {
+  const double *f;
+  int64_t sign; /* +1: ascending f, -1: descending f; ties by ascending index either way */
+} rank_ctx;
+
+static rank_ctx g_rank;
+
+static int rank_cmp(const void *pa, const void *pb) {
+  const int64_t a = *(const int64_t *)pa, b = *(const int64_t *)pb;
+  const double fa = (double)g_rank.sign * g_rank.f[a], fb = (double)g_rank.sign * g_rank.f[b];
+  if (fa < fb) return -1;
+  if (fa > fb) return 1;
+  return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+/* Step 2 of a round: B from f, y, alpha (scratch up[n], low[n]); returns |B|. */
+static int64_t ws_select(const double *f, const int32_t *y, const double *alpha, int64_t n, double C, int64_t q,
+                         int64_t *up, int64_t *low, int64_t *B) {
+  int64_t nu = 0, nl = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (in_up(y[i], alpha[i], C)) up[nu++] = i;
+    if (in_low(y[i], alpha[i], C)) low[nl++] = i;
+  }
+  g_rank.f = f;
+  g_rank.sign = 1;
+  qsort(up, (size_t)nu, sizeof(int64_t), rank_cmp);
+  g_rank.sign = -1;
+  qsort(low, (size_t)nl, sizeof(int64_t), rank_cmp);
+  const int64_t h = q / 2;
+  int64_t m = 0;
+  for (int64_t k = 0; k < nu && k < h; ++k) B[m++] = up[k];
+  const int64_t m_up = m;
+  for (int64_t k = 0; k < nl && k < h; ++k) {
+    int dup = 0;
+    for (int64_t r = 0; r < m_up; ++r)
+      if (B[r] == low[k]) { dup = 1; break; }
+    if (!dup) B[m++] = low[k];
+  }
+  return m;
+}
+
+/* The working set of step 2 alone, for given f and alpha (B has room for q entries). */
+int64_t oracle_ws_select(const double *f, const int32_t *y, const double *alpha, int64_t n, double C, int64_t q,
+                         int64_t *B) {
+  int64_t *up = (int64_t *)malloc((size_t)n * sizeof(int64_t));
+  int64_t *low = (int64_t *)malloc((size_t)n * sizeof(int64_t));
+  int64_t m = -1;
+  if (up && low && q >= 2 && !(q & 1)) m = ws_select(f, y, alpha, n, C, q, up, low, B);
+  free(up);
+  free(low);
+  return m;
+}
+
+int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int kind, double C, double gamma,
+                    double tol, int64_t q, double frac, int64_t max_inner, int64_t max_iter, int64_t cache_bytes,
+                    int threads, double *alpha, double *f_out, oracle_result *res, int64_t *rounds_out,
+                    int64_t trace_len, int32_t *trace_ul, double *trace_b, int64_t ws_trace_len,
+                    int32_t *ws_trace) {
+  memset(res, 0, sizeof(*res));
+  if (!X || !y || !alpha || n < 2 || d < 1 || !(C > 0) || !(tol > 0) || (kind == ORACLE_RBF && !(gamma > 0)) ||
+      q < 2 || (q & 1) || !(frac >= 0.0 && frac < 1.0) || max_inner < 1) {
+    res->status = -1;
+    return -1;
+  }
+  int64_t npos = 0, nneg = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (y[i] == 1) npos++;
+    else if (y[i] == -1) nneg++;
+    else { res->status = -1; return -1; }
+  }
+  if (!npos || !nneg) { res->status = -1; return -1; }
+
+  krows kr;
+  if (krows_init(&kr, X, n, d, kind, gamma, cache_bytes, threads)) { krows_free(&kr); res->status = -2; return -2; }
+  double *f = (double *)malloc((size_t)n * sizeof(double));
+  int64_t *up = (int64_t *)malloc((size_t)n * sizeof(int64_t));
+  int64_t *low = (int64_t *)malloc((size_t)n * sizeof(int64_t));
+  int64_t *B = (int64_t *)malloc((size_t)q * sizeof(int64_t));
+  double *KB = (double *)malloc((size_t)(q * q) * sizeof(double));
+  double *fB = (double *)malloc((size_t)q * sizeof(double));
+  double *aB = (double *)malloc((size_t)q * sizeof(double));
+  double *cB = (double *)malloc((size_t)q * sizeof(double));
+  double *s = (double *)malloc((size_t)n * sizeof(double));
+  if (!f || !up || !low || !B || !KB || !fB || !aB || !cB || !s) {
+    free(f); free(up); free(low); free(B); free(KB); free(fB); free(aB); free(cB); free(s);
+    krows_free(&kr);
+    res->status = -2;
+    return -2;
+  }
+  for (int64_t i = 0; i < n; ++i) { alpha[i] = 0.0; f[i] = -(double)y[i]; }
+
+  int64_t t = 0, rounds = 0;
+  double b_up = 0.0, b_low = 0.0;
+  int status = 1;
+  for (;;) {
+    /* 1. maximal violating pair of the whole problem and the stop rule */
+    int64_t u = -1, l = -1;
+    for (int64_t i = 0; i < n; ++i) {
+      if (in_up(y[i], alpha[i], C) && (u < 0 || f[i] < f[u])) u = i;
+      if (in_low(y[i], alpha[i], C) && (l < 0 || f[i] > f[l])) l = i;
+    }
+    if (u < 0 || l < 0) { status = 0; break; }
+    b_up = f[u];
+    b_low = f[l];
+    if (rounds < trace_len) {
+      if (trace_ul) { trace_ul[2 * rounds] = (int32_t)u; trace_ul[2 * rounds + 1] = (int32_t)l; }
+      if (trace_b) { trace_b[2 * rounds] = b_up; trace_b[2 * rounds + 1] = b_low; }
+    }
+    if (b_low - b_up <= tol) { status = 0; break; }
+    if (t >= max_iter) { status = 1; break; }
+
+    /* 2. working set */
+    const int64_t m = ws_select(f, y, alpha, n, C, q, up, low, B);
+    if (rounds < ws_trace_len && ws_trace)
+      for (int64_t k = 0; k < q; ++k) ws_trace[rounds * q + k] = k < m ? (int32_t)B[k] : -1;
+
+    /* 3. sub-problem on B */
+    for (int64_t a = 0; a < m; ++a) {
+      const double *Ka = krows_get(&kr, B[a]);
+      for (int64_t b = 0; b < m; ++b) KB[a * m + b] = Ka[B[b]];
+      fB[a] = f[B[a]];
+      aB[a] = alpha[B[a]];
+    }
+    const double tol_loc = fmax(tol, frac * (b_low - b_up));
+    for (int64_t inner = 0; inner < max_inner && t < max_iter; ++inner) {
+      int64_t pu = -1, pl = -1;
+      for (int64_t a = 0; a < m; ++a) {
+        const int32_t ya = y[B[a]];
+        if (in_up(ya, aB[a], C) && (pu < 0 || fB[a] < fB[pu] || (fB[a] == fB[pu] && B[a] < B[pu]))) pu = a;
+        if (in_low(ya, aB[a], C) && (pl < 0 || fB[a] > fB[pl] || (fB[a] == fB[pl] && B[a] < B[pl]))) pl = a;
+      }
+      if (pu < 0 || pl < 0 || fB[pl] - fB[pu] <= tol_loc) break;
+      double eta = KB[pu * m + pu] + KB[pl * m + pl] - 2.0 * KB[pu * m + pl];
+      if (eta <= 0.0) eta = 1e-12;
+      const double yu = (double)y[B[pu]], yl = (double)y[B[pl]];
+      const double sg = yu * yl;
+      const double au = aB[pu], al = aB[pl];
+      double L, H;
+      if (sg < 0) { L = fmax(0.0, al - au); H = fmin(C, C + al - au); }
+      else { L = fmax(0.0, au + al - C); H = fmin(C, au + al); }
+      double al_new = clampd(al + yl * (fB[pu] - fB[pl]) / eta, L, H);
+      double au_new = clampd(au + sg * (al - al_new), 0.0, C);
+      const double snap = 1e-12 * C;
+      if (fabs(al_new) <= snap) al_new = 0.0;
+      if (fabs(al_new - C) <= snap) al_new = C;
+      if (fabs(au_new) <= snap) au_new = 0.0;
+      if (fabs(au_new - C) <= snap) au_new = C;
+      const double cu = (au_new - au) * yu, cl = (al_new - al) * yl;
+      for (int64_t a = 0; a < m; ++a) fB[a] += cu * KB[pu * m + a] + cl * KB[pl * m + a];
+      aB[pu] = au_new;
+      aB[pl] = al_new;
+      ++t;
+    }
+
+    /* 4. gradient update of every sample from the change of the multipliers in B */
+    for (int64_t a = 0; a < m; ++a) cB[a] = (aB[a] - alpha[B[a]]) * (double)y[B[a]];
+    for (int64_t j = 0; j < n; ++j) s[j] = 0.0;
+    for (int64_t a = 0; a < m; ++a) {
+      if (cB[a] == 0.0) continue;
+      const double *Ka = krows_get(&kr, B[a]);
+      const double c = cB[a];
+#pragma omp parallel for num_threads(threads) schedule(static)
+      for (int64_t j = 0; j < n; ++j) s[j] += c * Ka[j];
+    }
+    for (int64_t j = 0; j < n; ++j) f[j] += s[j];
+    for (int64_t a = 0; a < m; ++a) alpha[B[a]] = aB[a];
+    ++rounds;
+  }
+
+  res->iterations = t;
+  res->status = status;
+  res->b_up = b_up;
+  res->b_low = b_low;
+  res->b = 0.5 * (b_up + b_low);
+  double sa = 0.0, saf = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    sa += alpha[i];
+    saf += alpha[i] * (double)y[i] * f[i];
+    if (alpha[i] > 0.0) { res->n_sv++; if (alpha[i] >= C) res->n_bound++; }
+  }
+  res->dual_obj = 0.5 * sa - 0.5 * saf;
+  if (rounds_out) *rounds_out = rounds;
+  if (f_out) memcpy(f_out, f, (size_t)n * sizeof(double));
+  free(f); free(up); free(low); free(B); free(KB); free(fB); free(aB); free(cB); free(s);
+  krows_free(&kr);
+  return status;
+}
+
 /* Decision values d(x) = sum_{a_i>0} a_i y_i K(x_i, x) - b, summed in index order. */
 void oracle_decision(const float *X, const int32_t *y, const double *alpha, double b, int64_t n, int64_t d, int kind,
                      double gamma, const float *T, int64_t m, double *dec, int threads) {

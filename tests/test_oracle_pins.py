@@ -261,3 +261,101 @@ def test_thread_count_does_not_change_results():
     a = oracle.train(X, y, 1.0, 0.25, 1e-3, threads=1)
     b = oracle.train(X, y, 1.0, 0.25, 1e-3, threads=4)
     np.testing.assert_array_equal(a.alpha, b.alpha)
+
+
+# --- working-set decomposition (rounds of pair steps on q samples) ----------------------
+
+@pytest.mark.parametrize("cid", [0, 2])
+def test_ws_q2_is_the_pair_step(cid):
+    """With q = 2 a round is exactly one maximal-violating-pair step: same pairs, same
+    multipliers to the bit, same bias."""
+    wl = synth.workload(cid)
+    X, y, _, _ = synth.generate(cid, n=600, m=1)
+    a = oracle.train(X, y, wl.C, wl.gamma, wl.tol, trace_len=5000)
+    b = oracle.train_ws(X, y, wl.C, wl.gamma, wl.tol, 2, trace_len=5000)
+    assert a.iterations == b.iterations == b.rounds
+    assert np.array_equal(a.trace_ul, b.trace_ul)
+    assert np.array_equal(a.alpha, b.alpha)
+    assert a.b == b.b
+
+
+def _lex_select(f, y, alpha, C, q):
+    """The working-set rule written with NumPy's stable lexsort."""
+    up = ((y > 0) & (alpha < C)) | ((y < 0) & (alpha > 0))
+    low = ((y > 0) & (alpha > 0)) | ((y < 0) & (alpha < C))
+    idx = np.arange(f.shape[0])
+    fu, fl = f + 0.0, -f + 0.0  # +0.0 folds -0 into +0, as the comparisons do
+    su = idx[up][np.lexsort((idx[up], fu[up]))][: q // 2]
+    sl = idx[low][np.lexsort((idx[low], fl[low]))][: q // 2]
+    return np.array(list(su) + [i for i in sl if i not in set(su)], dtype=np.int64)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_ws_select_rule(seed):
+    """Working sets against the rule evaluated independently, on values with many ties,
+    signed zeros and every membership case."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(5, 400))
+    C = 2.0
+    y = np.where(rng.random(n) < 0.5, 1, -1).astype(np.int32)
+    alpha = rng.choice([0.0, C, 0.7], size=n)
+    f = np.round(rng.standard_normal(n), 1)
+    f[rng.random(n) < 0.1] = -0.0
+    f[rng.random(n) < 0.1] = 0.0
+    for q in (2, 4, 10, 64, 2 * n + 2):
+        assert np.array_equal(oracle.ws_select(f, y, alpha, C, q), _lex_select(f, y, alpha, C, q)), q
+
+
+def test_ws_select_first_round():
+    """From a = 0 every f is -y: B is the q/2 lowest-indexed +1 samples, then the q/2
+    lowest-indexed -1 samples."""
+    X, y = synth.two_blobs(300, 4, seed=9)
+    r = oracle.train_ws(X, y, 1.0, 0.5, 1e-3, 16, ws_trace_len=1)
+    expect = np.concatenate([np.flatnonzero(y == 1)[:8], np.flatnonzero(y == -1)[:8]])
+    assert np.array_equal(r.ws_trace[0], expect)
+
+
+@pytest.mark.parametrize("q", [4, 16, 64, 256])
+def test_ws_same_optimum(q):
+    """Any working-set size reaches the optimum the pair steps reach: KKT to tol with f
+    recomputed from alpha through the kernel directly, the equality constraint, the box,
+    and the dual objective of the maximal-violating-pair solution."""
+    wl = synth.workload(0)
+    X, y, _, _ = synth.generate(0)
+    ref = oracle.train(X, y, wl.C, wl.gamma, wl.tol)
+    r = oracle.train_ws(X, y, wl.C, wl.gamma, wl.tol, q, want_f=True)
+    assert r.status == 0 and r.rounds >= 1
+    assert abs(float(r.alpha @ y)) <= 1e-10 * wl.C * X.shape[0]
+    assert r.alpha.min() >= 0.0 and r.alpha.max() <= wl.C
+    f = oracle.f_from_alpha(X, y, r.alpha, wl.gamma)
+    np.testing.assert_allclose(r.f, f, atol=1e-9)
+    up = ((y > 0) & (r.alpha < wl.C)) | ((y < 0) & (r.alpha > 0))
+    low = ((y > 0) & (r.alpha > 0)) | ((y < 0) & (r.alpha < wl.C))
+    assert f[low].max() - f[up].min() <= wl.tol + 1e-9
+    assert abs(r.dual_obj - ref.dual_obj) <= 1e-6 * abs(ref.dual_obj)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_ws_bruteforce_qp(seed):
+    n = 3 + seed % 8  # 3..10
+    X, y, gamma, C = _tiny_problem(seed + 500, n)
+    K = rbf(X, X, gamma)
+    Q = (y[:, None] * y[None, :]) * K
+    a_star, _, _, _ = bf.solve(Q, y, C)
+    r = oracle.train_ws(X, y, C, gamma, 1e-11, 4)
+    assert r.status == 0
+    np.testing.assert_allclose(r.alpha, a_star, atol=1e-6)
+    assert abs(r.dual_obj - dual_W(K, y, a_star)) <= 1e-9 * max(1.0, abs(r.dual_obj))
+
+
+def test_ws_invariants_between_rounds():
+    """Cut after any number of steps (mid-round included): the round's change is applied
+    in full, so alpha stays feasible and f equals its definition."""
+    X, y = synth.two_blobs(200, 5, seed=4)
+    C, gamma = 1.0, 0.3
+    for t in (1, 5, 17, 40, 90):
+        r = oracle.train_ws(X, y, C, gamma, 1e-3, 16, max_iter=t, want_f=True)
+        assert r.iterations <= t
+        assert abs(float(r.alpha @ y)) <= 1e-12 * 200
+        assert r.alpha.min() >= 0.0 and r.alpha.max() <= C
+        np.testing.assert_allclose(r.f, oracle.f_from_alpha(X, y, r.alpha, gamma), atol=1e-10)
