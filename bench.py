@@ -32,7 +32,7 @@ FP16_MFMA_PEAK_TFLOPS = 2500.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 COUNTERS = os.path.join(ROOT, "profiles", "smo_solve_n20000_d784_hbm_counters.md")
 SOLVER_SOURCES = ("paper_2311_14908_amd/csrc/smo.hip", "paper_2311_14908_amd/csrc/rbf_rows.hpp",
-                  "paper_2311_14908_amd/csrc/solver_params.hpp")
+                  "paper_2311_14908_amd/csrc/solver_params.hpp", "paper_2311_14908_amd/csrc/pair_step.hpp")
 
 
 def counter_bytes_per_step(workload_name):

@@ -84,7 +84,14 @@ typedef struct {
   int32_t exchange_levels;   /* levels of the cross-workgroup exchange: 1, 2, or 0 = automatic
                                 (two levels above 128 workgroups per problem) */
   int32_t gram_mfma;         /* svm_gram_mfma */
-  int32_t reserved;          /* must be 0 */
+  int32_t working_set;       /* 0 = one maximal violating pair per step with f updated every step
+                                (Section III.B).  q = 2..128, even: working-set rounds -- B = the
+                                q/2 smallest f of I_up and the q/2 largest of I_low (ties to the
+                                smaller index), pair steps on B alone until its gap is at most
+                                max(tol, 0.1 x the round's gap) or 100 q steps, then f updated once
+                                from the round's change.  Needs the Gram and n <= 261,120 (255
+                                workgroups of up to 1,024 samples); binary training only.  The
+                                trace then holds the maximal violating pair of every round. */
 } svm_options;
 
 typedef struct {
@@ -100,6 +107,7 @@ typedef struct {
   double t_solve, t_finalize, t_total; /* seconds */
   double t_kernel;      /* seconds the solver kernel ran, summed over its launches (HIP events on
                            the launch stream) */
+  int64_t rounds;       /* working-set rounds (0 for the per-step solver) */
 } svm_stats;
 
 /* Fill *o with the defaults above. */

@@ -59,7 +59,7 @@ def _load():
         lib.oracle_train_ws.restype = C.c_int
         lib.oracle_train_ws.argtypes = [P, P, C.c_int64, C.c_int64, C.c_int, C.c_double, C.c_double, C.c_double,
                                         C.c_int64, C.c_double, C.c_int64, C.c_int64, C.c_int64, C.c_int, P, P,
-                                        C.POINTER(_Res), P, C.c_int64, P, P, C.c_int64, P]
+                                        C.POINTER(_Res), P, C.c_int64, P, P, P, P, C.c_int64, P]
         lib.oracle_ws_select.restype = C.c_int64
         lib.oracle_ws_select.argtypes = [P, P, P, C.c_int64, C.c_double, C.c_int64, P]
         lib.oracle_max_threads.restype = C.c_int
@@ -135,7 +135,9 @@ WS_INNER_PER_Q = 100
 @dataclass
 class WsResult(TrainResult):
     rounds: int = 0
-    ws_trace: np.ndarray | None = None  # [rounds, q] int32 working sets, -1 padded
+    ws_trace: np.ndarray | None = None      # [rounds, q] int32 working sets, -1 padded
+    trace_margin: np.ndarray | None = None  # [rounds] smallest distance of a decision from flipping
+    trace_t: np.ndarray | None = None       # [rounds] steps taken before the round
 
 
 def train_ws(X, y, C_, gamma, tol, q, *, kind=RBF, frac=WS_FRAC, max_inner=None, max_iter=None,
@@ -158,11 +160,13 @@ def train_ws(X, y, C_, gamma, tol, q, *, kind=RBF, frac=WS_FRAC, max_inner=None,
     tl, wl = int(trace_len), int(ws_trace_len)
     tul = np.full((max(tl, 1), 2), -1, dtype=np.int32)
     tb = np.full((max(tl, 1), 2), np.nan, dtype=np.float64)
+    tm = np.full(max(tl, 1), np.nan, dtype=np.float64)
+    tt = np.full(max(tl, 1), -1, dtype=np.int64)
     wst = np.full((max(wl, 1), int(q)), -1, dtype=np.int32)
     rc = lib.oracle_train_ws(_p(X), _p(y), n, d, int(kind), float(C_), float(gamma), float(tol), int(q), float(frac),
                              int(max_inner), int(max_iter), int(cache_bytes), threads, _p(alpha),
-                             _p(f) if f is not None else None, C.byref(res), C.byref(rounds), tl, _p(tul), _p(tb), wl,
-                             _p(wst))
+                             _p(f) if f is not None else None, C.byref(res), C.byref(rounds), tl, _p(tul), _p(tb),
+                             _p(tm), _p(tt), wl, _p(wst))
     if rc < 0:
         raise ValueError(f"oracle_train_ws rejected its input (status {rc})")
     r = int(rounds.value)
@@ -171,7 +175,8 @@ def train_ws(X, y, C_, gamma, tol, q, *, kind=RBF, frac=WS_FRAC, max_inner=None,
                     iterations=int(res.iterations), n_sv=int(res.n_sv), n_bound=int(res.n_bound),
                     status=int(res.status), f=f,
                     trace_ul=tul[:steps].copy() if tl else None, trace_b=tb[:steps].copy() if tl else None,
-                    rounds=r, ws_trace=wst[:min(wl, r)].copy() if wl else None)
+                    rounds=r, ws_trace=wst[:min(wl, r)].copy() if wl else None,
+                    trace_margin=tm[:steps].copy() if tl else None, trace_t=tt[:steps].copy() if tl else None)
 
 
 def ws_select(f, y, alpha, C_, q) -> np.ndarray:

@@ -271,7 +271,13 @@ int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kin
  *      with c_p = (a_new - a_old) y at B_p, accumulated from zero.
  * With q = 2 a round is one step of oracle_train (same pair, same update, same rounding).
  * iterations counts two-multiplier steps; max_iter bounds their total.  For the first
- * ws_trace_len rounds B is written to ws_trace (q entries per round, -1 padded).
+ * ws_trace_len rounds B is written to ws_trace (q entries per round, -1 padded).  For the first
+ * trace_len rounds: the pair (u, l) and (b_up, b_low) of step 1, the steps taken before the
+ * round (trace_t), and the round's margin (trace_margin): the smallest distance of any decision
+ * taken in the round from the value that would flip it -- the stop test, the boundaries of the
+ * two ranked lists at q/2, each pair selection against its runner-up, each local stop test, and
+ * each new multiplier against the bounds of its box (relative to C).  A second solver whose
+ * values differ from these by less than the margin takes the same decisions.
  */
 typedef struct {
   const double *f;
@@ -329,8 +335,8 @@ int64_t oracle_ws_select(const double *f, const int32_t *y, const double *alpha,
 int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int kind, double C, double gamma,
                     double tol, int64_t q, double frac, int64_t max_inner, int64_t max_iter, int64_t cache_bytes,
                     int threads, double *alpha, double *f_out, oracle_result *res, int64_t *rounds_out,
-                    int64_t trace_len, int32_t *trace_ul, double *trace_b, int64_t ws_trace_len,
-                    int32_t *ws_trace) {
+                    int64_t trace_len, int32_t *trace_ul, double *trace_b, double *trace_margin, int64_t *trace_t,
+                    int64_t ws_trace_len, int32_t *ws_trace) {
   memset(res, 0, sizeof(*res));
   if (!X || !y || !alpha || n < 2 || d < 1 || !(C > 0) || !(tol > 0) || (kind == ORACLE_RBF && !(gamma > 0)) ||
       q < 2 || (q & 1) || !(frac >= 0.0 && frac < 1.0) || max_inner < 1) {
@@ -377,9 +383,12 @@ int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int 
     if (u < 0 || l < 0) { status = 0; break; }
     b_up = f[u];
     b_low = f[l];
+    double margin = fabs((b_low - b_up) - tol);
     if (rounds < trace_len) {
       if (trace_ul) { trace_ul[2 * rounds] = (int32_t)u; trace_ul[2 * rounds + 1] = (int32_t)l; }
       if (trace_b) { trace_b[2 * rounds] = b_up; trace_b[2 * rounds + 1] = b_low; }
+      if (trace_t) trace_t[rounds] = t;
+      if (trace_margin) trace_margin[rounds] = margin;
     }
     if (b_low - b_up <= tol) { status = 0; break; }
     if (t >= max_iter) { status = 1; break; }
@@ -388,6 +397,18 @@ int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int 
     const int64_t m = ws_select(f, y, alpha, n, C, q, up, low, B);
     if (rounds < ws_trace_len && ws_trace)
       for (int64_t k = 0; k < q; ++k) ws_trace[rounds * q + k] = k < m ? (int32_t)B[k] : -1;
+    {
+      /* the ranked lists' boundaries (up and low are sorted by ws_select) */
+      int64_t nu = 0, nl = 0;
+      for (int64_t i = 0; i < n; ++i) {
+        nu += in_up(y[i], alpha[i], C);
+        nl += in_low(y[i], alpha[i], C);
+      }
+      const int64_t h = q / 2;
+      /* (from a = 0 every f is exactly -y, so the ties of round 0 are exact in any solver) */
+      if (rounds > 0 && nu > h) margin = fmin(margin, f[up[h]] - f[up[h - 1]]);
+      if (rounds > 0 && nl > h) margin = fmin(margin, f[low[h - 1]] - f[low[h]]);
+    }
 
     /* 3. sub-problem on B */
     for (int64_t a = 0; a < m; ++a) {
@@ -404,6 +425,15 @@ int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int 
         if (in_up(ya, aB[a], C) && (pu < 0 || fB[a] < fB[pu] || (fB[a] == fB[pu] && B[a] < B[pu]))) pu = a;
         if (in_low(ya, aB[a], C) && (pl < 0 || fB[a] > fB[pl] || (fB[a] == fB[pl] && B[a] < B[pl]))) pl = a;
       }
+      if (pu >= 0 && pl >= 0) {
+        margin = fmin(margin, fabs((fB[pl] - fB[pu]) - tol_loc));
+        /* the first step of round 0 sees f = -y exactly: its ties are exact in any solver */
+        for (int64_t a = 0; a < m && !(rounds == 0 && inner == 0); ++a) {
+          const int32_t ya = y[B[a]];
+          if (a != pu && in_up(ya, aB[a], C)) margin = fmin(margin, fabs(fB[a] - fB[pu]));
+          if (a != pl && in_low(ya, aB[a], C)) margin = fmin(margin, fabs(fB[pl] - fB[a]));
+        }
+      }
       if (pu < 0 || pl < 0 || fB[pl] - fB[pu] <= tol_loc) break;
       double eta = KB[pu * m + pu] + KB[pl * m + pl] - 2.0 * KB[pu * m + pl];
       if (eta <= 0.0) eta = 1e-12;
@@ -413,7 +443,9 @@ int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int 
       double L, H;
       if (sg < 0) { L = fmax(0.0, al - au); H = fmin(C, C + al - au); }
       else { L = fmax(0.0, au + al - C); H = fmin(C, au + al); }
-      double al_new = clampd(al + yl * (fB[pu] - fB[pl]) / eta, L, H);
+      const double al_raw = al + yl * (fB[pu] - fB[pl]) / eta;
+      margin = fmin(margin, fmin(fabs(al_raw - L), fabs(al_raw - H)) / C);
+      double al_new = clampd(al_raw, L, H);
       double au_new = clampd(au + sg * (al - al_new), 0.0, C);
       const double snap = 1e-12 * C;
       if (fabs(al_new) <= snap) al_new = 0.0;
@@ -439,6 +471,7 @@ int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int 
     }
     for (int64_t j = 0; j < n; ++j) f[j] += s[j];
     for (int64_t a = 0; a < m; ++a) alpha[B[a]] = aB[a];
+    if (rounds < trace_len && trace_margin) trace_margin[rounds] = margin;
     ++rounds;
   }
 

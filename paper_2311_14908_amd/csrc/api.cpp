@@ -49,6 +49,8 @@ constexpr int32_t CACHE_CAP_MAX = 4096;               // row-cache slots (tags l
 constexpr double SPIN_SECONDS = 2.0;                  // longest a device-side wait may last
 constexpr int64_t LDS_BYTES = 160 * 1024;
 constexpr int32_t MAX_CLASSES = 64;
+constexpr double WS_FRAC = 0.1;           // working-set rounds stop at max(tol, 0.1 x the round's gap)
+constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
@@ -68,6 +70,7 @@ struct Opts {
   int32_t workgroups;
   int32_t levels;
   int32_t gram_mfma;
+  int32_t working_set;
 };
 
 bool resolve(const svm_options *o, int64_t n, Opts *r) {
@@ -88,8 +91,11 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
   r->workgroups = std::max<int32_t>(0, o->workgroups);
   r->levels = o->exchange_levels;
   r->gram_mfma = o->gram_mfma;
+  r->working_set = o->working_set;
+  const bool ws_ok = r->working_set == 0 ||
+                     (r->working_set >= 2 && r->working_set <= ws_q_max() && r->working_set % 2 == 0);
   return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF && r->levels >= 0 && r->levels <= 2 &&
-         (r->gram_mfma == SVM_MFMA_SPLIT_F16 || r->gram_mfma == SVM_MFMA_F32) && o->reserved == 0;
+         (r->gram_mfma == SVM_MFMA_SPLIT_F16 || r->gram_mfma == SVM_MFMA_F32) && ws_ok;
 }
 
 // How a problem of n samples is spread over workgroups.
@@ -138,6 +144,32 @@ bool choose_shape(int64_t n, bool gram, int32_t requested, int32_t levels, Shape
   return true;
 }
 
+// Working-set solver: 64 samples or more per owning workgroup (at most ws_slice_max()), at
+// most 255 owners (plus the solving workgroup), so that every list merge takes at most 16
+// lists: one level up to 16 owners, else groups of ceil(sqrt(nwg)).
+constexpr int32_t WS_MAX_WG = 255;
+
+bool choose_ws_shape(int64_t n, int32_t requested, Shape *s) {
+  int64_t nwg = requested > 0 ? requested : std::min<int64_t>(WS_MAX_WG, (n + 63) / 64);
+  nwg = std::max<int64_t>(1, std::min<int64_t>(nwg, n));
+  const int64_t smax = ws_slice_max();
+  if ((n + nwg - 1) / nwg > smax) nwg = (n + smax - 1) / smax;
+  if (nwg > WS_MAX_WG) return false;
+  const int64_t per_wg = (n + nwg - 1) / nwg;
+  nwg = (n + per_wg - 1) / per_wg;
+  s->nwg = (int32_t)nwg;
+  s->per_wg = (int32_t)per_wg;
+  s->per_thread = 0;
+  if (nwg > 16) {
+    s->g1 = (int32_t)std::ceil(std::sqrt((double)nwg));
+    s->ng = (int32_t)((nwg + s->g1 - 1) / s->g1);
+  } else {
+    s->g1 = 0;
+    s->ng = 0;
+  }
+  return true;
+}
+
 struct Layout {
   int64_t total = 0;
   int64_t add(int64_t bytes) {
@@ -154,7 +186,8 @@ struct TrainPlan {
   Shape shape;
   int32_t cache_cap;
   int64_t off_f, off_gram, off_split, off_sqn, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2,
-      off_tul, off_tb, off_fin, off_err;
+      off_tul, off_tb, off_fin, off_err, off_rounds;
+  int64_t slot_words, slot2_words;
   int64_t total;
 };
 
@@ -171,8 +204,14 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   else
     p->gram = gram_bytes <= (double)o.gram_budget;
   if (p->gram && gram_bytes > 9.0e18) return fail(SVM_ENOMEM, "Gram size overflows");
-  if (!choose_shape(n, p->gram, o.workgroups, o.levels, &p->shape))
+  if (o.working_set > 0) {
+    if (!p->gram) return fail(SVM_EINVAL, "the working-set solver needs the Gram (gram ON, or AUTO within budget)");
+    if (!choose_ws_shape(n, o.workgroups, &p->shape))
+      return fail(SVM_ENOMEM, "n=%lld exceeds the working-set solver's %d x %d samples", (long long)n, WS_MAX_WG,
+                  ws_slice_max());
+  } else if (!choose_shape(n, p->gram, o.workgroups, o.levels, &p->shape)) {
     return fail(SVM_ENOMEM, "problem too large to place");
+  }
   p->cache_cap = 0;
   if (!p->gram) {
     if (o.row_cache_bytes > 0)
@@ -189,13 +228,17 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   p->off_tags = p->cache_cap ? L.add(4LL * p->cache_cap * p->shape.nwg) : -1;
   p->off_ctl = L.add(sizeof(Ctl));
   p->off_prob = L.add(sizeof(Prob));
-  p->off_wgp = L.add(4LL * p->shape.nwg);
-  p->off_slots = L.add(8LL * 2 * p->shape.nwg * SLOT_WORDS);
-  p->off_slots2 = L.add(8LL * 2 * std::max(1, p->shape.ng) * SLOT_WORDS);
+  p->off_wgp = L.add(4LL * (p->shape.nwg + 1));
+  const int64_t per_rec = o.working_set > 0 ? ws_list_words() : SLOT_WORDS;
+  p->slot_words = 2LL * p->shape.nwg * per_rec;
+  p->slot2_words = 2LL * std::max(1, p->shape.ng) * per_rec + (o.working_set > 0 ? ws_bcast_words() : 0);
+  p->off_slots = L.add(8LL * p->slot_words);
+  p->off_slots2 = L.add(8LL * p->slot2_words);
   p->off_tul = L.add(4LL * 2 * o.trace_len);
   p->off_tb = L.add(8LL * 2 * o.trace_len);
   p->off_fin = L.add(8 * 4);
   p->off_err = L.add(16);
+  p->off_rounds = L.add(8);
   p->total = round_up(L.total, ALIGN);
   return SVM_OK;
 }
@@ -226,9 +269,11 @@ struct Timer {
   }
 };
 
-// Launch the solver until no problem is running.  Returns SVM_OK or a negative status.
-svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t per_thread, bool gram, Ctl *d_ctl,
-                      hipStream_t stream, int32_t *launches, std::vector<Ctl> &h, double *t_kernel) {
+// Launch a solver (launch(&max_coresident) enqueues one launch) until no problem is running.
+// Returns SVM_OK or a negative status.
+template <class Launch>
+svm_status run_launches(Launch launch, int32_t *error, int32_t nprob, int32_t total_wg, Ctl *d_ctl, hipStream_t stream,
+                        int32_t *launches, std::vector<Ctl> &h, double *t_kernel) {
   int32_t herr = 0;
   Timer tk;
   HIPCHK(tk.init());
@@ -238,14 +283,14 @@ svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t p
   for (;;) {
     int32_t maxres = 0;
     HIPCHK(hipEventRecord(tk.a, stream));
-    hipError_t e = launch_solver(sp, total_wg, per_thread, gram, stream, &maxres);
+    hipError_t e = launch(&maxres);
     if (e == hipErrorCooperativeLaunchTooLarge)
       return fail(SVM_ENOMEM, "%d solver workgroups do not fit on the device at once (at most %d)", total_wg, maxres);
     if (e != hipSuccess) return fail(SVM_EDEVICE, "solver launch: %s", hipGetErrorString(e));
     ++*launches;
     HIPCHK(hipEventRecord(tk.b, stream));
     HIPCHK(hipMemcpyAsync(h.data(), d_ctl, sizeof(Ctl) * nprob, hipMemcpyDeviceToHost, stream));
-    HIPCHK(hipMemcpyAsync(&herr, sp.error, sizeof(herr), hipMemcpyDeviceToHost, stream));
+    HIPCHK(hipMemcpyAsync(&herr, error, sizeof(herr), hipMemcpyDeviceToHost, stream));
     HIPCHK(hipStreamSynchronize(stream));
     if (herr) return fail(SVM_EDEVICE, "a device-side wait exceeded its %.1f s limit", SPIN_SECONDS);
     *t_kernel += tk.seconds();
@@ -261,6 +306,12 @@ svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t p
     if (!running) return SVM_OK;
     if (!progress) return fail(SVM_EDEVICE, "solver made no progress");
   }
+}
+
+svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t per_thread, bool gram, Ctl *d_ctl,
+                      hipStream_t stream, int32_t *launches, std::vector<Ctl> &h, double *t_kernel) {
+  return run_launches([&](int32_t *maxres) { return launch_solver(sp, total_wg, per_thread, gram, stream, maxres); },
+                      sp.error, nprob, total_wg, d_ctl, stream, launches, h, t_kernel);
 }
 
 svm_status check_labels_pm1(const int32_t *y, int64_t n, hipStream_t stream) {
@@ -462,8 +513,8 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   hp.per_wg = p.shape.per_wg;
   hp.g1 = p.shape.g1;
   hp.ng = p.shape.ng;
-  hp.slots2 = p.shape.g1 ? reinterpret_cast<u64 *>(ws + p.off_slots2) : nullptr;
-  std::vector<int32_t> hwgp(p.shape.nwg, 0);
+  hp.slots2 = (p.shape.g1 || r.working_set > 0) ? reinterpret_cast<u64 *>(ws + p.off_slots2) : nullptr;
+  std::vector<int32_t> hwgp(p.shape.nwg + 1, 0);
   HIPCHK(hipMemcpyAsync(dprob, &hp, sizeof(Prob), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemsetAsync(err, 0, 16, stream));
@@ -507,16 +558,36 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   int32_t launches = 0;
   std::vector<Ctl> hc;
   double t_kernel = 0.0;
-  svm_status s1 = run_solver(sp, 1, p.shape.nwg, p.shape.per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel);
+  int64_t *d_rounds = reinterpret_cast<int64_t *>(ws + p.off_rounds);
+  svm_status s1;
+  if (r.working_set > 0) {
+    HIPCHK(hipMemsetAsync(slots, 0, 8 * p.slot_words, stream));
+    HIPCHK(hipMemsetAsync(ws + p.off_slots2, 0, 8 * p.slot2_words, stream));
+    HIPCHK(hipMemsetAsync(d_rounds, 0, 8, stream));
+    WsParams wp{};
+    wp.sp = sp;
+    wp.rounds = d_rounds;
+    wp.frac = WS_FRAC;
+    wp.q = r.working_set;
+    wp.max_inner = WS_INNER_PER_Q * r.working_set;
+    const int32_t nwg = p.shape.nwg + (p.shape.nwg > 1 ? 1 : 0);  // owners and the solving workgroup
+    s1 = run_launches([&](int32_t *maxres) { return launch_ws_solver(wp, nwg, stream, maxres); }, err, 1, nwg, ctl,
+                      stream, &launches, hc, &t_kernel);
+  } else {
+    s1 = run_solver(sp, 1, p.shape.nwg, p.shape.per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel);
+  }
   if (s1 != SVM_OK) return s1;
+  int64_t h_rounds = 0;
+  HIPCHK(hipMemcpyAsync(&h_rounds, d_rounds, 8, hipMemcpyDeviceToHost, stream));
   HIPCHK(hipEventRecord(ts.b, stream));
 
   HIPCHK(hipEventRecord(tf.a, stream));
   HIPCHK(launch_finalize(dprob, 1, C, fin, stream));
   double hfin[4];
   HIPCHK(hipMemcpyAsync(hfin, fin, sizeof(hfin), hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
   if (r.trace_len) {
-    const int64_t steps = std::min<int64_t>(r.trace_len, hc[0].t + 1);
+    const int64_t steps = std::min<int64_t>(r.trace_len, (r.working_set > 0 ? h_rounds : hc[0].t) + 1);
     if (r.trace_ws) HIPCHK(hipMemcpyAsync(r.trace_ws, tul, 4 * 2 * steps, hipMemcpyDeviceToHost, stream));
     if (r.trace_b) HIPCHK(hipMemcpyAsync(r.trace_b, tb, 8 * 2 * steps, hipMemcpyDeviceToHost, stream));
   }
@@ -540,6 +611,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     st->t_finalize = tf.seconds();
     st->t_total = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
     st->t_kernel = t_kernel;
+    st->rounds = r.working_set > 0 ? h_rounds : 0;
   }
   return c.status == ST_MAXITER ? SVM_NOT_CONVERGED : SVM_OK;
 }

@@ -51,6 +51,25 @@ hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t
                               const PredictScratch &ws, hipStream_t s);
 hipError_t launch_ovo_vote(const double *dec, int64_t m, int32_t k, int32_t *pred, hipStream_t s);
 
+// Working-set solver (ws_smo.hip): one problem per launch, Gram path, nwg sample-owning
+// workgroups plus, when nwg > 1, one solving workgroup (launch nwg + 1).  Prob::slots holds
+// [2][nwg][ws_list_words()] candidate words, Prob::slots2 [2][ng][ws_list_words()] group
+// lists followed by ws_bcast_words() words for the solving workgroup's results; Ctl::t counts
+// pair steps; rounds[problem] counts rounds (ws_slice_max() samples per workgroup at most; q
+// even, 2..ws_q_max(); at most 16 lists per merge, so nwg <= 255 with g1 = ceil(sqrt(nwg))).
+struct WsParams {
+  SolveParams sp;    // steps = pair steps a launch may start rounds within
+  int64_t *rounds;   // [nprob]
+  double frac;       // local tolerance factor
+  int32_t q;         // working-set size
+  int32_t max_inner; // pair steps per round at most
+};
+hipError_t launch_ws_solver(const WsParams &p, int32_t total_wg, hipStream_t s, int32_t *max_coresident);
+int ws_slice_max();
+int ws_q_max();
+int64_t ws_list_words();
+int64_t ws_bcast_words();
+
 int solver_block_size(bool gram);
 int max_per_thread(bool gram);
 

@@ -164,14 +164,20 @@ __global__ void __launch_bounds__(SBS) gram_rbf_f16x3(SplitX s, int64_t n, float
       bh[a] = S[cur].v[2][kq][wn * 64 + a * 16 + r16];
       bl[a] = S[cur].v[3][kq][wn * 64 + a * 16 + r16];
     }
+    // the three products of a block go into one accumulator; each sweep over the 16 blocks
+    // keeps 16 independent MFMAs between two uses of an accumulator
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb) {
-        acc[a][bb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bh[bb], acc[a][bb], 0, 0, 0);
-        acc[a][bb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bl[bb], acc[a][bb], 0, 0, 0);
-        acc[a][bb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[a], bh[bb], acc[a][bb], 0, 0, 0);
-      }
+      for (int bb = 0; bb < 4; ++bb) acc[a][bb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bh[bb], acc[a][bb], 0, 0, 0);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) acc[a][bb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bl[bb], acc[a][bb], 0, 0, 0);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) acc[a][bb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[a], bh[bb], acc[a][bb], 0, 0, 0);
     if (st + 1 < stages) split_store(S[cur ^ 1], r);
     __syncthreads();
   }

@@ -1,0 +1,638 @@
+// ws_smo.hip -- working-set SMO for gfx950: rounds of two-multiplier steps (paper, Section
+// III.B) on a working set B of up to q samples, with the gradient of every sample updated once
+// per round instead of once per step.
+//
+// One cooperative launch serves one problem.  Workgroups 0..nwg-1 own the samples
+// [r*per_wg, (r+1)*per_wg) and keep their f, alpha and label in LDS; with more than one owner,
+// one more workgroup runs the pair steps.  A round:
+//   1. selection.  Every owner ranks its own members of I_up by (f, index) and of I_low by
+//      (-f, index) with bitonic networks inside waves (a sorted list of 64 is one register per
+//      lane) and publishes its 64 best of each side as candidates of three self-stamped words
+//      (ws_record.hpp) -- the stamp-only protocol of the pair solver, so no fence is needed.
+//      With more than 16 owners, group leaders merge their group's lists and publish those;
+//      every workgroup then merges the (group) lists into the same two lists.  B = the first
+//      q/2 of the I_up list, then those of the first q/2 of the I_low list that are not
+//      already in B.
+//   2. stop rule on the heads of the two lists, which are the maximal violating pair.
+//   3. the solving workgroup gathers K_BB from the Gram into LDS, runs the pair steps on B in
+//      one wave until the gap on B is at most max(tol, frac * gap of the round) or the round's
+//      step cap is reached, and publishes the new multipliers of B; meanwhile every owner
+//      loads the Gram rows of B over its own samples into LDS;
+//   4. every owner adds sum_p c_p K(B_p, j) to f_j of its own samples (c_p the change of a y
+//      at B_p, in a fixed grouping of B's order) and stores the new multipliers of its
+//      members of B.
+#include "common.hpp"
+#include "pair_step.hpp"
+#include "ws_record.hpp"
+
+#include <math.h>
+
+namespace svmx {
+
+constexpr int WS_BS = 256;
+constexpr int WS_NW = WS_BS / 64;
+constexpr int WS_QMAX = 128;        // working-set size limit (lists of 64 per side)
+constexpr int WS_SLICE_MAX = 1024;  // samples per workgroup
+constexpr int WS_LISTS_MAX = 16;    // lists merged by one workgroup at a level
+constexpr int WS_LIST_WORDS = 2 * 64 * CAND_WORDS;  // one workgroup's (or group's) two lists
+constexpr int WS_GATHER = 32;      // Gram loads a thread keeps in flight
+constexpr int WS_QUARTERS = 4;     // fixed grouping of the f update's sum
+constexpr int WS_MAXL = WS_LISTS_MAX / 2;     // lists one wave merges at a level
+constexpr int WS_BCAST_PITCH = 2 * WS_QMAX + 8;  // steps word, then two words per multiplier
+constexpr u64 KSENT = ~0ull;
+constexpr unsigned VSENT = 0xffffffffu;
+
+int ws_slice_max() { return WS_SLICE_MAX; }
+int ws_q_max() { return WS_QMAX; }
+int64_t ws_list_words() { return WS_LIST_WORDS; }
+int64_t ws_bcast_words() { return 2LL * WS_BCAST_PITCH; }
+
+// ---------------------------------------------------------------- sorted lists in a wave
+// A list is 64 (key, value) pairs, one per lane, ascending in lexicographic order; value is a
+// position that orders equal keys by sample index.  Empty entries are (KSENT, VSENT).
+
+__device__ __forceinline__ bool kv_lt(u64 ka, unsigned va, u64 kb, unsigned vb) {
+  return ka < kb || (ka == kb && va < vb);
+}
+
+__device__ __forceinline__ u64 shfl_xor_u64(u64 x, int d) {
+  const unsigned hi = (unsigned)__shfl_xor((int)(x >> 32), d);
+  const unsigned lo = (unsigned)__shfl_xor((int)x, d);
+  return ((u64)hi << 32) | lo;
+}
+
+__device__ __forceinline__ u64 shfl_u64(u64 x, int src) {
+  const unsigned hi = (unsigned)__shfl((int)(x >> 32), src);
+  const unsigned lo = (unsigned)__shfl((int)x, src);
+  return ((u64)hi << 32) | lo;
+}
+
+// Compare-exchange with the lane at distance d: in an ascending pair the lower lane keeps the
+// smaller element, in a descending pair the larger one.
+__device__ __forceinline__ void kv_cx(u64 &k, unsigned &v, int d, bool asc) {
+  const int lane = threadIdx.x & 63;
+  const u64 ok = shfl_xor_u64(k, d);
+  const unsigned ov = (unsigned)__shfl_xor((int)v, d);
+  const bool keep_min = ((lane & d) == 0) == asc;
+  const bool take = keep_min ? kv_lt(ok, ov, k, v) : kv_lt(k, v, ok, ov);
+  if (take) {
+    k = ok;
+    v = ov;
+  }
+}
+
+__device__ __forceinline__ void wave_sort64(u64 &k, unsigned &v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int s = 2; s <= 64; s <<= 1)
+#pragma unroll
+    for (int d = s >> 1; d > 0; d >>= 1) kv_cx(k, v, d, (lane & s) == 0);
+}
+
+// (k, v) and (bk, bv) ascending -> the 64 smallest of both, ascending: the element-wise
+// minimum of one list and the other reversed is bitonic and holds them; half-cleaners sort it.
+__device__ __forceinline__ void wave_merge64(u64 &k, unsigned &v, u64 bk, unsigned bv) {
+  const int lane = threadIdx.x & 63;
+  const u64 rk = shfl_u64(bk, 63 - lane);
+  const unsigned rv = (unsigned)__shfl((int)bv, 63 - lane);
+  if (kv_lt(rk, rv, k, v)) {
+    k = rk;
+    v = rv;
+  }
+#pragma unroll
+  for (int d = 32; d > 0; d >>= 1) kv_cx(k, v, d, true);
+}
+
+// s + c k, rounded as written (no contraction), so every placement sums to the same bits.
+__device__ __forceinline__ double ws_acc(double s, double c, float k) {
+#pragma clang fp contract(off)
+  return s + c * (double)k;
+}
+
+__device__ __forceinline__ unsigned ws_aux(int64_t j, int y) { return (unsigned)j | (y < 0 ? 0x80000000u : 0u); }
+__device__ __forceinline__ bool ws_in_up(int y, double a, double C) { return (y > 0 && a < C) || (y < 0 && a > 0.0); }
+__device__ __forceinline__ bool ws_in_low(int y, double a, double C) { return (y > 0 && a > 0.0) || (y < 0 && a < C); }
+
+__device__ __forceinline__ int64_t ws_gmap(const Prob &P, int64_t j) {
+  return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0);
+}
+__device__ __forceinline__ int ws_label(const Prob &P, int64_t j) {
+  return P.y ? P.y[ws_gmap(P, j)] : (j < P.len0 ? 1 : -1);
+}
+
+// Lane `lane` of the calling wave publishes entry `lane` of a list: the three words of the
+// candidate (key, aux, multiplier bits) or of an empty entry.
+__device__ __forceinline__ void put_cand(u64 *list, int lane, u64 key, unsigned aux, u64 abits, unsigned stamp) {
+  u64 w[CAND_WORDS];
+  cand_words(key, aux, abits, stamp, w);
+  u64 *dst = list + (size_t)lane * CAND_WORDS;
+#pragma unroll
+  for (int c = 0; c < CAND_WORDS; ++c) st_word(dst + c, w[c]);
+}
+
+// Wave-level: merge lists first, first + step, ... below last (side `side`, h entries each; at
+// most WS_MAXL lists) of the words at `words` into (k, v); v = (list - first0) * 64 + lane
+// indexes the staging arrays, which receive each taken candidate's aux word and multiplier
+// bits.  Every lane waits for its entry of all lists at once, so the round trips overlap.
+__device__ void merge_lists(const u64 *words, int side, int first0, int first, int last, int step, int h,
+                            unsigned stamp, unsigned *st_aux, u64 *st_ab, u64 &k, unsigned &v, uint64_t spin_limit,
+                            int32_t *err, int *abort_flag) {
+  const int lane = threadIdx.x & 63;
+  const int nl = first < last ? (last - first + step - 1) / step : 0;
+  u64 w[WS_MAXL][CAND_WORDS];
+#pragma unroll
+  for (int i = 0; i < WS_MAXL; ++i)
+#pragma unroll
+    for (int c = 0; c < CAND_WORDS; ++c) w[i][c] = 0;
+  if (lane < h) {
+    unsigned pending = (1u << nl) - 1u;
+    const uint64_t t0 = wall_clock64();
+    while (pending) {
+#pragma unroll
+      for (int i = 0; i < WS_MAXL; ++i) {
+        if (pending & (1u << i)) {
+          const u64 *src = words + ((size_t)(first + i * step) * 2 + side) * 64 * CAND_WORDS + (size_t)lane * CAND_WORDS;
+          bool ok = true;
+#pragma unroll
+          for (int c = 0; c < CAND_WORDS; ++c) {
+            w[i][c] = ld_word(src + c);
+            ok = ok && cand_stamped(w[i][c], stamp);
+          }
+          if (ok) pending &= ~(1u << i);
+        }
+      }
+      if (pending && wall_clock64() - t0 > spin_limit) {
+        __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *abort_flag = 1;
+        break;
+      }
+    }
+  }
+  k = KSENT;
+  v = VSENT;
+#pragma unroll
+  for (int i = 0; i < WS_MAXL; ++i) {
+    if (i >= nl) break;
+    u64 ck = KSENT;
+    unsigned cv = VSENT;
+    if (lane < h) {
+      u64 key, ab;
+      unsigned aux;
+      cand_fields(w[i], key, aux, ab);
+      if (key != KSENT) {
+        ck = key;
+        cv = (unsigned)((first + i * step - first0) * 64 + lane);
+        st_aux[cv] = aux;
+        st_ab[cv] = ab;
+      }
+    }
+    if (i == 0) {
+      k = ck;
+      v = cv;
+    } else {
+      wave_merge64(k, v, ck, cv);
+    }
+  }
+}
+
+// Waits until word `w` carries `stamp`; returns its 60-bit payload.
+__device__ __forceinline__ u64 poll_word(const u64 *w, unsigned stamp, uint64_t spin_limit, int32_t *err,
+                                         int *abort_flag) {
+  const uint64_t t0 = wall_clock64();
+  for (;;) {
+    const u64 x = ld_word(w);
+    if (cand_stamped(x, stamp)) return x & CAND_M60;
+    if (wall_clock64() - t0 > spin_limit) {
+      __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *abort_flag = 1;
+      return 0;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- the solver
+struct WsLds {
+  double f[WS_SLICE_MAX], a[WS_SLICE_MAX];
+  signed char y[WS_SLICE_MAX];
+  u64 lk[WS_NW][64];
+  unsigned lv[WS_NW][64];
+  union {
+    struct {
+      unsigned aux[2][WS_LISTS_MAX * 64];
+      u64 ab[2][WS_LISTS_MAX * 64];
+    } st;
+    float K[WS_QMAX * WS_QMAX];  // solver: K_BB; owners: the Gram rows of B over the own samples
+  } u;
+  double part[WS_QUARTERS][WS_SLICE_MAX];
+  int bi[WS_QMAX];
+  signed char by[WS_QMAX];
+  double bf[WS_QMAX], ba[WS_QMAX], bn[WS_QMAX], bc[WS_QMAX];
+  int nzp[WS_QMAX];
+  int nu, nl, m, nnz, il, abort_flag;
+  double bl;
+  int64_t steps;
+};
+
+// The pair steps on B (wave 0 only; K_BB in S.u.K): S.bn receives the new multipliers,
+// S.steps the number of steps.
+__device__ void local_solve(WsLds &S, const WsParams &p, int m, double b_up, double b_low, int64_t t) {
+  const SolveParams &sp = p.sp;
+  const double C = sp.C;
+  const int lane = threadIdx.x & 63;
+  const int p0 = lane, p1 = lane + 64;
+  const bool v0 = p0 < m, v1 = p1 < m;
+  double f0 = v0 ? S.bf[p0] : 0.0, f1 = v1 ? S.bf[p1] : 0.0;
+  double a0 = v0 ? S.ba[p0] : 0.0, a1 = v1 ? S.ba[p1] : 0.0;
+  const int y0 = v0 ? S.by[p0] : 0, y1 = v1 ? S.by[p1] : 0;
+  const int i0 = v0 ? S.bi[p0] : IBIG, i1 = v1 ? S.bi[p1] : IBIG;
+  const double tl = fmax(sp.tol, p.frac * (b_low - b_up));
+  int64_t tt = t;
+  for (int inner = 0; inner < p.max_inner && tt < sp.max_iter; ++inner) {
+    // this lane's best member of each side
+    double cu_v = INFINITY, cl_v = -INFINITY;
+    int cu_i = IBIG, cl_i = IBIG, cu_p = -1, cl_p = -1;
+    if (ws_in_up(y0, a0, C)) { cu_v = f0; cu_i = i0; cu_p = p0; }
+    if (ws_in_up(y1, a1, C) && lt_min(f1, i1, cu_v, cu_i)) { cu_v = f1; cu_i = i1; cu_p = p1; }
+    if (ws_in_low(y0, a0, C)) { cl_v = f0; cl_i = i0; cl_p = p0; }
+    if (ws_in_low(y1, a1, C) && gt_max(f1, i1, cl_v, cl_i)) { cl_v = f1; cl_i = i1; cl_p = p1; }
+    const int lu = winner_lane<false>(cu_v, cu_i), ll = winner_lane<true>(cl_v, cl_i);
+    const int pu = __builtin_amdgcn_readlane(cu_p, lu), pl = __builtin_amdgcn_readlane(cl_p, ll);
+    if (pu < 0 || pl < 0) break;
+    const double fu = readlane_d(cu_v, lu), fl = readlane_d(cl_v, ll);
+    if (fl - fu <= tl) break;
+    const double au = readlane_d(cu_p == p1 ? a1 : a0, lu), al = readlane_d(cl_p == p1 ? a1 : a0, ll);
+    const double yu = (double)__builtin_amdgcn_readlane(cu_p == p1 ? y1 : y0, lu);
+    const double yl = (double)__builtin_amdgcn_readlane(cl_p == p1 ? y1 : y0, ll);
+    const double kul = (double)S.u.K[pu * WS_QMAX + pl];
+    const PairStep ps = solve_pair(C, fu, fl, au, al, yu, yl, kul);
+    const double cu = (ps.au - au) * yu, cl = (ps.al - al) * yl;
+    if (v0) f0 = f_update(f0, cu, S.u.K[pu * WS_QMAX + p0], cl, S.u.K[pl * WS_QMAX + p0]);
+    if (v1) f1 = f_update(f1, cu, S.u.K[pu * WS_QMAX + p1], cl, S.u.K[pl * WS_QMAX + p1]);
+    if (p0 == pu) a0 = ps.au;
+    if (p0 == pl) a0 = ps.al;
+    if (p1 == pu) a1 = ps.au;
+    if (p1 == pl) a1 = ps.al;
+    ++tt;
+  }
+  if (v0) S.bn[p0] = a0;
+  if (v1) S.bn[p1] = a1;
+  if (lane == 0) S.steps = tt - t;
+}
+
+__global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
+  __shared__ WsLds S;
+  const SolveParams &sp = p.sp;
+  const int32_t pid = sp.wg_prob[blockIdx.x];
+  const Prob P = sp.probs[pid];
+  const int rank = (int)blockIdx.x - P.wg0;
+  Ctl *ctl = P.ctl;
+  if (ctl->status != ST_RUNNING) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const double C = sp.C;
+  const int h = p.q / 2;
+  // Workgroups 0..nwg-1 own the samples; with more than one of them, workgroup nwg runs the
+  // pair steps while the owners fetch the Gram rows of B they will need.
+  const bool solo = P.nwg == 1;
+  const bool solver = solo || rank == P.nwg;
+  const bool owner = rank < P.nwg;
+  const int64_t base = owner ? (int64_t)rank * P.per_wg : 0;
+  const int len = owner ? (int)min<int64_t>(P.per_wg, P.n - base) : 0;
+  u64 *bcast = P.slots2 + 2 * (size_t)P.ng * WS_LIST_WORDS;
+
+  for (int j = tid; j < len; j += WS_BS) {
+    S.f[j] = P.f[base + j];
+    S.a[j] = P.alpha[base + j];
+    S.y[j] = (signed char)ws_label(P, base + j);
+  }
+  if (tid == 0) S.abort_flag = 0;
+  int64_t t = ctl->t;
+  int64_t round = p.rounds[pid];
+  const int64_t t_end = min(t + sp.steps, sp.max_iter);
+  __syncthreads();
+
+  int status = ST_RUNNING;
+  double b_up = 0.0, b_low = 0.0;
+  int iu = IBIG, il = IBIG;
+  for (;;) {
+    const unsigned stamp = (unsigned)(round + 1);
+    const size_t par = (size_t)(round & 1);
+    const int side = wave >> 1, half = wave & 1;
+    // ---- 1a. this workgroup's two lists: waves 0, 1 take I_up, waves 2, 3 take I_low; each
+    // wave sorts every other chunk of 64 samples and merges them, then the two halves meet.
+    u64 k = KSENT;
+    unsigned v = VSENT;
+    {
+      bool have = false;
+      for (int c = half; c * 64 < len; c += 2) {
+        const int pos = c * 64 + lane;
+        u64 ck = KSENT;
+        unsigned cv = VSENT;
+        if (pos < len) {
+          const double fj = S.f[pos], aj = S.a[pos];
+          const int yj = S.y[pos];
+          if (side == 0 ? ws_in_up(yj, aj, C) : ws_in_low(yj, aj, C)) {
+            ck = f_key(side == 0 ? fj : -fj);
+            cv = (unsigned)pos;
+          }
+        }
+        if (__ballot(ck != KSENT) == 0) continue;
+        wave_sort64(ck, cv);
+        if (!have) {
+          k = ck;
+          v = cv;
+          have = true;
+        } else {
+          wave_merge64(k, v, ck, cv);
+        }
+      }
+    }
+    if (half == 1) {
+      S.lk[wave][lane] = k;
+      S.lv[wave][lane] = v;
+    }
+    __syncthreads();
+    if (half == 0) {
+      wave_merge64(k, v, S.lk[wave + 1][lane], S.lv[wave + 1][lane]);
+      if (owner && !solo && lane < h) {
+        unsigned aux = 0;
+        u64 ab = 0;
+        if (k != KSENT) {
+          aux = ws_aux(base + v, S.y[v]);
+          ab = (u64)__double_as_longlong(S.a[v]);
+        }
+        put_cand(P.slots + (par * P.nwg + rank) * WS_LIST_WORDS + (size_t)side * 64 * CAND_WORDS, lane, k, aux, ab,
+                 stamp);
+      }
+    }
+    __syncthreads();  // lk/lv are rewritten below
+    // ---- 1b. group lists (more than 16 owners): group leaders merge their group's lists
+    if (owner && P.g1 > 0 && rank % P.g1 == 0) {
+      const int g = rank / P.g1;
+      const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
+      merge_lists(P.slots + par * P.nwg * WS_LIST_WORDS, side, q0, q0 + half, q1, 2, h, stamp, S.u.st.aux[side],
+                  S.u.st.ab[side], k, v, sp.spin_limit, sp.error, &S.abort_flag);
+      if (half == 1) {
+        S.lk[wave][lane] = k;
+        S.lv[wave][lane] = v;
+      }
+      __syncthreads();
+      if (half == 0) {
+        wave_merge64(k, v, S.lk[wave + 1][lane], S.lv[wave + 1][lane]);
+        if (lane < h) {
+          const bool ok = k != KSENT;
+          put_cand(P.slots2 + (par * P.ng + g) * WS_LIST_WORDS + (size_t)side * 64 * CAND_WORDS, lane, k,
+                   ok ? S.u.st.aux[side][v] : 0u, ok ? S.u.st.ab[side][v] : 0ull, stamp);
+        }
+      }
+      __syncthreads();
+    }
+    // ---- 1c. the problem's two lists, identical in every workgroup
+    if (!solo) {
+      const bool two = P.g1 > 0;
+      const u64 *words = two ? P.slots2 + par * P.ng * WS_LIST_WORDS : P.slots + par * P.nwg * WS_LIST_WORDS;
+      const int nls = two ? P.ng : P.nwg;
+      merge_lists(words, side, 0, half, nls, 2, h, stamp, S.u.st.aux[side], S.u.st.ab[side], k, v, sp.spin_limit,
+                  sp.error, &S.abort_flag);
+      if (half == 1) {
+        S.lk[wave][lane] = k;
+        S.lv[wave][lane] = v;
+      }
+      __syncthreads();
+      if (half == 0) wave_merge64(k, v, S.lk[wave + 1][lane], S.lv[wave + 1][lane]);
+    } else if (half == 0 && k != KSENT) {
+      // one workgroup: its own lists are the problem's; stage them like merged candidates
+      S.u.st.aux[side][v] = ws_aux(base + v, S.y[v]);
+      S.u.st.ab[side][v] = (u64)__double_as_longlong(S.a[v]);
+    }
+    __syncthreads();
+    // ---- 1d. the working set: the I_up list, then the I_low list without repeats
+    if (wave == 0) {
+      const bool ok = lane < h && k != KSENT;
+      if (ok) {
+        const unsigned aux = S.u.st.aux[0][v];
+        S.bi[lane] = (int)(aux & 0x7fffffffu);
+        S.by[lane] = (aux >> 31) ? -1 : 1;
+        S.bf[lane] = key_f(k);
+        S.ba[lane] = __longlong_as_double((long long)S.u.st.ab[0][v]);
+      }
+      const int cnt = __popcll(__ballot(ok));  // every lane votes: outside the lane-0 branch
+      if (lane == 0) S.nu = cnt;
+    }
+    __syncthreads();
+    if (wave == 2) {
+      const int nu = S.nu;
+      const bool ok = lane < h && k != KSENT;
+      const unsigned aux = ok ? S.u.st.aux[1][v] : 0u;
+      const int idx = ok ? (int)(aux & 0x7fffffffu) : -1;
+      const int upi = lane < nu ? S.bi[lane] : -2;
+      bool dup = false;
+      for (int r = 0; r < nu; ++r) dup = dup || (__builtin_amdgcn_readlane(upi, r) == idx);
+      const bool keep = ok && !dup;
+      const u64 mk = __ballot(keep);
+      const int nok = __popcll(__ballot(ok));
+      const int pos = nu + __popcll(mk & ((1ull << lane) - 1ull));
+      if (keep) {
+        S.bi[pos] = idx;
+        S.by[pos] = (aux >> 31) ? -1 : 1;
+        S.bf[pos] = -key_f(k);
+        S.ba[pos] = __longlong_as_double((long long)S.u.st.ab[1][v]);
+      }
+      if (lane == 0) {
+        S.m = nu + __popcll(mk);
+        S.nl = nok;
+        S.il = ok ? idx : IBIG;
+        S.bl = ok ? -key_f(k) : -INFINITY;
+      }
+    }
+    __syncthreads();
+    // ---- 2. stop rule (every workgroup takes the same decision)
+    const int nu = S.nu, m = S.m;
+    iu = nu > 0 ? S.bi[0] : IBIG;
+    b_up = nu > 0 ? S.bf[0] : INFINITY;
+    il = S.nl > 0 ? S.il : IBIG;
+    b_low = S.nl > 0 ? S.bl : -INFINITY;
+    if (rank == 0 && tid == 0 && round < P.trace_len) {
+      if (P.trace_ul) {
+        P.trace_ul[2 * round] = iu;
+        P.trace_ul[2 * round + 1] = il;
+      }
+      if (P.trace_b) {
+        P.trace_b[2 * round] = b_up;
+        P.trace_b[2 * round + 1] = b_low;
+      }
+    }
+    if (S.abort_flag) status = ST_TIMEOUT;
+    else if (nu == 0 || S.nl == 0 || b_low - b_up <= sp.tol) status = ST_CONVERGED;
+    else if (t >= sp.max_iter) status = ST_MAXITER;
+    if (status != ST_RUNNING) break;
+
+    // ---- 3. the pair steps on B: K_BB into LDS, then one wave of the solving workgroup
+    const bool rows_in_lds = owner && !solo && m * len <= WS_QMAX * WS_QMAX;
+    if (solver) {
+      for (int e0 = 0; e0 < m * m; e0 += WS_BS * WS_GATHER) {
+        float kv[WS_GATHER];
+#pragma unroll
+        for (int b = 0; b < WS_GATHER; ++b) {
+          const int e = e0 + b * WS_BS + tid;
+          if (e < m * m) {
+            const int ra = e / m, cb = e - ra * m;
+            kv[b] = sp.gram[ws_gmap(P, S.bi[ra]) * sp.ld + ws_gmap(P, S.bi[cb])];
+          }
+        }
+#pragma unroll
+        for (int b = 0; b < WS_GATHER; ++b) {
+          const int e = e0 + b * WS_BS + tid;
+          if (e < m * m) {
+            const int ra = e / m, cb = e - ra * m;
+            S.u.K[ra * WS_QMAX + cb] = kv[b];
+          }
+        }
+      }
+      __syncthreads();
+      if (wave == 0) local_solve(S, p, m, b_up, b_low, t);
+      __syncthreads();
+      if (!solo) {
+        // publish the new multipliers (two words each) and the step count
+        // every entry is rewritten each round (zero past m): a word left from 16 rounds earlier
+        // would carry the same 4-bit stamp
+        u64 *bw = bcast + par * WS_BCAST_PITCH;
+        const u64 sw = (u64)(stamp & 15u) << 60;
+        if (tid < WS_QMAX) {
+          const u64 b = tid < m ? (u64)__double_as_longlong(S.bn[tid]) : 0ull;
+          st_word(bw + 1 + 2 * tid, sw | (b & 0xffffffffull));
+          st_word(bw + 2 + 2 * tid, sw | (b >> 32));
+        }
+        if (tid == WS_BS - 1) st_word(bw, sw | (u64)S.steps);
+      }
+    } else {
+      // owners: the Gram rows of B over the own samples into LDS while the pair steps run
+      if (rows_in_lds) {
+        for (int e0 = 0; e0 < m * len; e0 += WS_BS * WS_GATHER) {
+          float kv[WS_GATHER];
+#pragma unroll
+          for (int b = 0; b < WS_GATHER; ++b) {
+            const int e = e0 + b * WS_BS + tid;
+            if (e < m * len) {
+              const int ra = e / len, pos = e - ra * len;
+              kv[b] = sp.gram[ws_gmap(P, S.bi[ra]) * sp.ld + ws_gmap(P, base + pos)];
+            }
+          }
+#pragma unroll
+          for (int b = 0; b < WS_GATHER; ++b) {
+            const int e = e0 + b * WS_BS + tid;
+            if (e < m * len) S.u.K[e] = kv[b];
+          }
+        }
+      }
+      const u64 *bw = bcast + par * WS_BCAST_PITCH;
+      if (tid < m) {
+        const u64 lo = poll_word(bw + 1 + 2 * tid, stamp, sp.spin_limit, sp.error, &S.abort_flag);
+        const u64 hi = poll_word(bw + 2 + 2 * tid, stamp, sp.spin_limit, sp.error, &S.abort_flag);
+        S.bn[tid] = __longlong_as_double((long long)((hi << 32) | lo));
+      }
+      if (tid == WS_BS - 1) S.steps = (int64_t)poll_word(bw, stamp, sp.spin_limit, sp.error, &S.abort_flag);
+      __syncthreads();
+    }
+    t += S.steps;
+    // ---- 4. owners: changes of a y in B's order, new multipliers of the own members of B,
+    // and f_j += ((s0 + s1) + s2) + s3, s_g the sum over the g-th quarter of the changes: a
+    // fixed grouping, so the bits do not depend on how many workgroups share the samples.
+    if (owner) {
+      if (wave == 0) {
+        const int p0 = lane, p1 = lane + 64;
+        const bool v0 = p0 < m, v1 = p1 < m;
+        const double c0 = v0 ? (S.bn[p0] - S.ba[p0]) * (double)S.by[p0] : 0.0;
+        const double c1 = v1 ? (S.bn[p1] - S.ba[p1]) * (double)S.by[p1] : 0.0;
+        if (v0) S.bc[p0] = c0;
+        if (v1) S.bc[p1] = c1;
+        const u64 m0 = __ballot(v0 && c0 != 0.0), m1 = __ballot(v1 && c1 != 0.0);
+        const u64 below = (1ull << lane) - 1ull;
+        if (v0 && c0 != 0.0) S.nzp[__popcll(m0 & below)] = p0;
+        if (v1 && c1 != 0.0) S.nzp[__popcll(m0) + __popcll(m1 & below)] = p1;
+        const int nnz = __popcll(m0) + __popcll(m1);
+        if (lane == 0) S.nnz = nnz;
+      }
+      __syncthreads();
+      for (int q = tid; q < m; q += WS_BS) {
+        const int64_t j = S.bi[q] - base;
+        if (j >= 0 && j < len) S.a[j] = S.bn[q];
+      }
+      // threads as (sample, quarters): span samples by 256 / span thread groups, span a power
+      // of two that divides the workgroup, so every thread's group is below ngrp
+      const int nnz = S.nnz;
+      const int span = len <= 64 ? 64 : (len <= 128 ? 128 : WS_BS);
+      const int ngrp = WS_BS / span;  // 4, 2 or 1 thread groups
+      const int grp = tid / span;
+      const int g0 = grp * (WS_QUARTERS / ngrp), g1 = g0 + WS_QUARTERS / ngrp;
+      for (int pos = tid - grp * span; pos < len; pos += WS_BS) {
+        const int64_t gj = ws_gmap(P, base + pos);
+        for (int g = g0; g < g1; ++g) {
+          const int r0 = g * nnz / WS_QUARTERS, r1 = (g + 1) * nnz / WS_QUARTERS;
+          double s = 0.0;
+          if (rows_in_lds) {
+            for (int r = r0; r < r1; ++r) {
+              const int pe = S.nzp[r];
+              s = ws_acc(s, S.bc[pe], S.u.K[pe * len + pos]);
+            }
+          } else {
+            for (int r = r0; r < r1; r += WS_GATHER) {
+              float kk[WS_GATHER];
+#pragma unroll
+              for (int e = 0; e < WS_GATHER; ++e)
+                if (r + e < r1) kk[e] = sp.gram[ws_gmap(P, S.bi[S.nzp[r + e]]) * sp.ld + gj];
+#pragma unroll
+              for (int e = 0; e < WS_GATHER; ++e)
+                if (r + e < r1) s = ws_acc(s, S.bc[S.nzp[r + e]], kk[e]);
+            }
+          }
+          S.part[g][pos] = s;
+        }
+      }
+      __syncthreads();
+      for (int pos = tid; pos < len; pos += WS_BS) {
+        const double s = ((S.part[0][pos] + S.part[1][pos]) + S.part[2][pos]) + S.part[3][pos];
+        S.f[pos] = S.f[pos] + s;
+      }
+    }
+    ++round;
+    __syncthreads();
+    if (S.abort_flag) {
+      status = ST_TIMEOUT;
+      break;
+    }
+    if (t >= t_end) break;  // launch budget spent: the state is whole at a round boundary
+  }
+
+  for (int j = tid; j < len; j += WS_BS) {
+    P.f[base + j] = S.f[j];
+    P.alpha[base + j] = S.a[j];
+  }
+  if (rank == 0 && tid == 0) {
+    ctl->t = t;
+    ctl->status = status;
+    ctl->b_up = b_up;
+    ctl->b_low = b_low;
+    ctl->u = iu;
+    ctl->l = il;
+    p.rounds[pid] = round;
+  }
+}
+
+hipError_t launch_ws_solver(const WsParams &p, int32_t total_wg, hipStream_t s, int32_t *max_coresident) {
+  const void *fn = reinterpret_cast<const void *>(&ws_solve);
+  int dev = 0, cus = 0, per_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, WS_BS, 0);
+  if (e != hipSuccess) return e;
+  if (max_coresident) *max_coresident = per_cu * cus;
+  if (total_wg <= 0) return hipSuccess;
+  if ((int64_t)total_wg > (int64_t)per_cu * cus) return hipErrorCooperativeLaunchTooLarge;
+  WsParams pp = p;
+  void *args[] = {&pp};
+  return hipLaunchCooperativeKernel(fn, dim3((unsigned)total_wg), dim3(WS_BS), args, 0, s);
+}
+
+}  // namespace svmx

@@ -39,7 +39,7 @@ def test_struct_layouts_match_header():
     lib.svm_default_options(C.byref(o))
     assert o.struct_size == C.sizeof(svmx.svm_options) == 88
     assert o.check_every == 65536 and o.gram == svmx.GRAM_AUTO
-    assert C.sizeof(svmx.svm_stats) == 96
+    assert C.sizeof(svmx.svm_stats) == 104
 
 
 def _opts(**kw):
@@ -134,6 +134,26 @@ def test_predict_and_rows_reject():
     assert lib.svm_gram_workspace_bytes(10, 4, C.byref(f32)) == 0
     bad = _opts(gram_mfma=7)
     assert lib.svm_gram_workspace_bytes(10, 4, C.byref(bad)) == -1
+
+
+def test_working_set_options():
+    lib = svmx.load()
+    ws = lambda n, d, **kw: lib.svm_train_workspace_bytes(n, d, C.byref(_opts(**kw)))
+    for q in (1, 3, 130, -2):
+        assert ws(1000, 16, working_set=q) == -1, q
+    for q in (2, 64, 128):
+        assert ws(1000, 16, working_set=q) > 4 * 1000 * 1024, q
+    # the candidate lists of 254 workgroups of 79 samples and 16 groups (two parities, 384 words
+    # per list pair) in place of the pair solver's records
+    w = ws(20_000, 784, working_set=128)
+    assert w - ws(20_000, 784) >= 8 * 2 * (254 + 16) * 384 - 8 * 2 * (40 + 1) * 16
+    # the Gram is required, and n is limited to 255 workgroups of 1024 samples
+    assert ws(20_000, 784, working_set=64, gram=svmx.GRAM_OFF) == -1
+    assert ws(261_120, 4, working_set=64, gram=svmx.GRAM_ON) > 0
+    assert ws(261_121, 4, working_set=64, gram=svmx.GRAM_ON) == -1
+    st = lib.svm_train(FAKE, FAKE, 100, 4, 1.0, 0.5, 1e-3, FAKE, C.byref(C.c_double()), FAKE, 16,
+                       C.byref(_opts(working_set=64, gram=svmx.GRAM_OFF)), None)
+    assert st == svmx.SVM_EINVAL and "Gram" in lib.svm_last_error().decode()
 
 
 def test_predict_workspace_sizes():

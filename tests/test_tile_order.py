@@ -1,6 +1,7 @@
 """Host checks of index and bit arithmetic that the gfx950 kernels use, compiled with hipcc
 for the host: the upper-triangle tile order of the Gram kernels (csrc/tile_order.hpp) hits every
-tile exactly once, and the solver's exchange record (csrc/xchg_record.hpp) round-trips."""
+tile exactly once, the solver's exchange record (csrc/xchg_record.hpp) round-trips, and the
+working-set candidate words (csrc/ws_record.hpp) keep the fp64 order and round-trip."""
 import os
 import subprocess
 
@@ -26,3 +27,8 @@ def test_tile_order_is_bijective(tmp_path):
 @pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
 def test_exchange_record_round_trip(tmp_path):
     assert _run("xchg_record_check.cpp", tmp_path).startswith("ok")
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
+def test_working_set_candidate_words(tmp_path):
+    assert _run("ws_record_check.cpp", tmp_path).startswith("ok")
