@@ -128,7 +128,7 @@ def train(X, y, C_, gamma, tol, *, kind=RBF, max_iter=None, cache_bytes=8 << 30,
 
 
 # Working-set variant: local tolerance factor and per-round step cap used unless given.
-WS_FRAC = 0.1
+WS_FRAC = 0.5
 WS_INNER_PER_Q = 100
 
 

@@ -49,7 +49,7 @@ constexpr int32_t CACHE_CAP_MAX = 4096;               // row-cache slots (tags l
 constexpr double SPIN_SECONDS = 2.0;                  // longest a device-side wait may last
 constexpr int64_t LDS_BYTES = 160 * 1024;
 constexpr int32_t MAX_CLASSES = 64;
-constexpr double WS_FRAC = 0.1;           // working-set rounds stop at max(tol, 0.1 x the round's gap)
+constexpr double WS_FRAC = 0.5;           // working-set rounds stop at max(tol, 0.5 x the round's gap)
 constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }

@@ -55,24 +55,50 @@ __device__ __forceinline__ bool kv_lt(u64 ka, unsigned va, u64 kb, unsigned vb) 
   return ka < kb || (ka == kb && va < vb);
 }
 
-__device__ __forceinline__ u64 shfl_xor_u64(u64 x, int d) {
-  const unsigned hi = (unsigned)__shfl_xor((int)(x >> 32), d);
-  const unsigned lo = (unsigned)__shfl_xor((int)x, d);
-  return ((u64)hi << 32) | lo;
+// Value of lane (lane ^ d) for d = 1, 2, 4, 8, 16, 32 without LDS traffic: DPP quad
+// permutes and row rotations inside rows of 16, and the gfx950 lane swaps across rows and
+// halves (permlane16_swap with both operands x returns x of lane l for even rows and of
+// lane l + 16 for odd ones in its first result, the reverse in its second; permlane32_swap
+// likewise for the two halves).  d is a constant after unrolling.
+__device__ __forceinline__ unsigned xor_lane(unsigned x, int d) {
+  const int lane = threadIdx.x & 63;
+  switch (d) {
+    case 1: return (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+    case 2: return (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+    case 4: {
+      const unsigned a = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x124, 0xF, 0xF, false);  // row_ror:4
+      const unsigned b = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x12C, 0xF, 0xF, false);  // row_ror:12
+      return (lane & 4) ? a : b;
+    }
+    case 8: return (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x128, 0xF, 0xF, false);  // row_ror:8
+    case 16: {
+      const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+      return (lane & 16) ? r[0] : r[1];
+    }
+    default: {
+      const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+      return (lane & 32) ? r[0] : r[1];
+    }
+  }
 }
 
-__device__ __forceinline__ u64 shfl_u64(u64 x, int src) {
-  const unsigned hi = (unsigned)__shfl((int)(x >> 32), src);
-  const unsigned lo = (unsigned)__shfl((int)x, src);
-  return ((u64)hi << 32) | lo;
+__device__ __forceinline__ u64 xor_lane64(u64 x, int d) {
+  return ((u64)xor_lane((unsigned)(x >> 32), d) << 32) | xor_lane((unsigned)x, d);
+}
+
+// Value of lane 63 - lane: the mirror inside each row of 16 (DPP row_mirror), then rows
+// exchanged by xor 48.
+__device__ __forceinline__ unsigned rev_lane(unsigned x) {
+  const unsigned m = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x140, 0xF, 0xF, false);  // row_mirror
+  return xor_lane(xor_lane(m, 16), 32);
 }
 
 // Compare-exchange with the lane at distance d: in an ascending pair the lower lane keeps the
 // smaller element, in a descending pair the larger one.
 __device__ __forceinline__ void kv_cx(u64 &k, unsigned &v, int d, bool asc) {
   const int lane = threadIdx.x & 63;
-  const u64 ok = shfl_xor_u64(k, d);
-  const unsigned ov = (unsigned)__shfl_xor((int)v, d);
+  const u64 ok = xor_lane64(k, d);
+  const unsigned ov = xor_lane(v, d);
   const bool keep_min = ((lane & d) == 0) == asc;
   const bool take = keep_min ? kv_lt(ok, ov, k, v) : kv_lt(k, v, ok, ov);
   if (take) {
@@ -92,9 +118,8 @@ __device__ __forceinline__ void wave_sort64(u64 &k, unsigned &v) {
 // (k, v) and (bk, bv) ascending -> the 64 smallest of both, ascending: the element-wise
 // minimum of one list and the other reversed is bitonic and holds them; half-cleaners sort it.
 __device__ __forceinline__ void wave_merge64(u64 &k, unsigned &v, u64 bk, unsigned bv) {
-  const int lane = threadIdx.x & 63;
-  const u64 rk = shfl_u64(bk, 63 - lane);
-  const unsigned rv = (unsigned)__shfl((int)bv, 63 - lane);
+  const u64 rk = ((u64)rev_lane((unsigned)(bk >> 32)) << 32) | rev_lane((unsigned)bk);
+  const unsigned rv = rev_lane(bv);
   if (kv_lt(rk, rv, k, v)) {
     k = rk;
     v = rv;
@@ -226,16 +251,62 @@ struct WsLds {
   double part[WS_QUARTERS][WS_SLICE_MAX];
   int bi[WS_QMAX];
   signed char by[WS_QMAX];
-  double bf[WS_QMAX], ba[WS_QMAX], bn[WS_QMAX], bc[WS_QMAX];
+  double bf[WS_QMAX], ba[WS_QMAX], bn[WS_QMAX];
   int nzp[WS_QMAX];
+  int64_t roff[WS_QMAX];   // Gram row offset of B_p
+  int64_t nzoff[WS_QMAX];  // Gram row offset and change of the r-th nonzero change
+  double nzc[WS_QMAX];
   int nu, nl, m, nnz, il, abort_flag;
   double bl;
   int64_t steps;
 };
 
+// Wave-wide min of a and max of b, returned to every lane: the DPP pattern of wave_extreme
+// (quad permutes, row rotations, then the row-15 and row-31 broadcasts into lane 63) with
+// compare-and-select (the values are finite or +-inf, so no NaN canonicalization) and the
+// two chains interleaved round by round.
+template <int CTRL>
+__device__ __forceinline__ double dpp_full_d(double v) {  // every lane reads its source lane
+  const long long b = __double_as_longlong(v);
+  const unsigned hi = (unsigned)__builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xF, 0xF, false);
+  const unsigned lo = (unsigned)__builtin_amdgcn_mov_dpp((int)b, CTRL, 0xF, 0xF, false);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+__device__ __forceinline__ void wave_minmax(double &a, double &b) {
+#define SVMX_MM_FULL(CTRL)                       \
+  {                                              \
+    const double oa = dpp_full_d<CTRL>(a);       \
+    const double ob = dpp_full_d<CTRL>(b);       \
+    a = oa < a ? oa : a;                         \
+    b = ob > b ? ob : b;                         \
+  }
+#define SVMX_MM_MASK(CTRL, RM)                   \
+  {                                              \
+    const double oa = dpp_mov_d<CTRL, RM>(a);    \
+    const double ob = dpp_mov_d<CTRL, RM>(b);    \
+    a = oa < a ? oa : a;                         \
+    b = ob > b ? ob : b;                         \
+  }
+  SVMX_MM_FULL(0xB1)      // quad_perm [1,0,3,2]
+  SVMX_MM_FULL(0x4E)      // quad_perm [2,3,0,1]
+  SVMX_MM_FULL(0x124)     // row_ror:4
+  SVMX_MM_FULL(0x128)     // row_ror:8
+  SVMX_MM_MASK(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
+  SVMX_MM_MASK(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
+#undef SVMX_MM_FULL
+#undef SVMX_MM_MASK
+  a = readlane_d(a, 63);
+  b = readlane_d(b, 63);
+}
+
 // The pair steps on B (wave 0 only; K_BB in S.u.K): S.bn receives the new multipliers,
-// S.steps the number of steps.
-__device__ void local_solve(WsLds &S, const WsParams &p, int m, double b_up, double b_low, int64_t t) {
+// S.steps the number of steps.  Lane l holds B positions l and l + 64.  The step is written
+// without lane-divergent branches, and the two wave reductions are independent chains that
+// the scheduler can interleave.  Not inlined: the loop gets registers of its own instead of
+// reloading the kernel's spilled scalars every step.
+__device__ __attribute__((noinline)) void local_solve(WsLds &S, const WsParams &p, int m, double b_up, double b_low,
+                                                     int64_t t) {
   const SolveParams &sp = p.sp;
   const double C = sp.C;
   const int lane = threadIdx.x & 63;
@@ -245,38 +316,61 @@ __device__ void local_solve(WsLds &S, const WsParams &p, int m, double b_up, dou
   double a0 = v0 ? S.ba[p0] : 0.0, a1 = v1 ? S.ba[p1] : 0.0;
   const int y0 = v0 ? S.by[p0] : 0, y1 = v1 ? S.by[p1] : 0;
   const int i0 = v0 ? S.bi[p0] : IBIG, i1 = v1 ? S.bi[p1] : IBIG;
+  const double dy0 = (double)y0, dy1 = (double)y1;
   const double tl = fmax(sp.tol, p.frac * (b_low - b_up));
-  int64_t tt = t;
-  for (int inner = 0; inner < p.max_inner && tt < sp.max_iter; ++inner) {
-    // this lane's best member of each side
-    double cu_v = INFINITY, cl_v = -INFINITY;
-    int cu_i = IBIG, cl_i = IBIG, cu_p = -1, cl_p = -1;
-    if (ws_in_up(y0, a0, C)) { cu_v = f0; cu_i = i0; cu_p = p0; }
-    if (ws_in_up(y1, a1, C) && lt_min(f1, i1, cu_v, cu_i)) { cu_v = f1; cu_i = i1; cu_p = p1; }
-    if (ws_in_low(y0, a0, C)) { cl_v = f0; cl_i = i0; cl_p = p0; }
-    if (ws_in_low(y1, a1, C) && gt_max(f1, i1, cl_v, cl_i)) { cl_v = f1; cl_i = i1; cl_p = p1; }
-    const int lu = winner_lane<false>(cu_v, cu_i), ll = winner_lane<true>(cl_v, cl_i);
+  const int max_inner = (int)min<int64_t>(p.max_inner, sp.max_iter - t);
+  int inner = 0;
+  for (; inner < max_inner; ++inner) {
+    // this lane's best member of each side (positions l and l + 64)
+    const bool u0 = ws_in_up(y0, a0, C), u1 = ws_in_up(y1, a1, C);
+    const bool l0 = ws_in_low(y0, a0, C), l1 = ws_in_low(y1, a1, C);
+    // position l + 64 wins a lane's side on a smaller (larger) f, or an equal f and a smaller
+    // index (bitwise forms: no branches)
+    const bool tie_i = (f1 == f0) & (i1 < i0);
+    const bool up1 = u1 & (!u0 | (f1 < f0) | tie_i);
+    const bool lo1 = l1 & (!l0 | (f1 > f0) | tie_i);
+    const double cu_v = up1 ? f1 : (u0 ? f0 : INFINITY);
+    const int cu_i = up1 ? i1 : (u0 ? i0 : IBIG);
+    const int cu_p = up1 ? p1 : (u0 ? p0 : -1);
+    const double cl_v = lo1 ? f1 : (l0 ? f0 : -INFINITY);
+    const int cl_i = lo1 ? i1 : (l0 ? i0 : IBIG);
+    const int cl_p = lo1 ? p1 : (l0 ? p0 : -1);
+    // wave extremes of both sides, then the smallest index among the lanes holding each
+    double ru = cu_v, rl = cl_v;
+    wave_minmax(ru, rl);
+    const unsigned long long tu = (unsigned long long)__ballot(cu_v == ru);
+    const unsigned long long tw = (unsigned long long)__ballot(cl_v == rl);
+    int lu = __ffsll(tu) - 1, ll = __ffsll(tw) - 1;
+    if (__popcll(tu) > 1) {
+      const int best = wave_min_int(cu_v == ru ? cu_i : IBIG);
+      lu = __ffsll((unsigned long long)__ballot(cu_v == ru && cu_i == best)) - 1;
+    }
+    if (__popcll(tw) > 1) {
+      const int best = wave_min_int(cl_v == rl ? cl_i : IBIG);
+      ll = __ffsll((unsigned long long)__ballot(cl_v == rl && cl_i == best)) - 1;
+    }
+    lu &= 63;
+    ll &= 63;
     const int pu = __builtin_amdgcn_readlane(cu_p, lu), pl = __builtin_amdgcn_readlane(cl_p, ll);
     if (pu < 0 || pl < 0) break;
     const double fu = readlane_d(cu_v, lu), fl = readlane_d(cl_v, ll);
     if (fl - fu <= tl) break;
-    const double au = readlane_d(cu_p == p1 ? a1 : a0, lu), al = readlane_d(cl_p == p1 ? a1 : a0, ll);
-    const double yu = (double)__builtin_amdgcn_readlane(cu_p == p1 ? y1 : y0, lu);
-    const double yl = (double)__builtin_amdgcn_readlane(cl_p == p1 ? y1 : y0, ll);
-    const double kul = (double)S.u.K[pu * WS_QMAX + pl];
+    const bool hu1 = pu >= 64, hl1 = pl >= 64;  // which of its two positions the winner holds
+    const double au = readlane_d(hu1 ? a1 : a0, lu), al = readlane_d(hl1 ? a1 : a0, ll);
+    const double yu = readlane_d(hu1 ? dy1 : dy0, lu), yl = readlane_d(hl1 ? dy1 : dy0, ll);
+    const float *Ku = S.u.K + pu * WS_QMAX, *Kl = S.u.K + pl * WS_QMAX;
+    const double kul = (double)Ku[pl];
+    const float ku0 = Ku[p0], kl0 = Kl[p0], ku1 = Ku[p1], kl1 = Kl[p1];
     const PairStep ps = solve_pair(C, fu, fl, au, al, yu, yl, kul);
     const double cu = (ps.au - au) * yu, cl = (ps.al - al) * yl;
-    if (v0) f0 = f_update(f0, cu, S.u.K[pu * WS_QMAX + p0], cl, S.u.K[pl * WS_QMAX + p0]);
-    if (v1) f1 = f_update(f1, cu, S.u.K[pu * WS_QMAX + p1], cl, S.u.K[pl * WS_QMAX + p1]);
-    if (p0 == pu) a0 = ps.au;
-    if (p0 == pl) a0 = ps.al;
-    if (p1 == pu) a1 = ps.au;
-    if (p1 == pl) a1 = ps.al;
-    ++tt;
+    f0 = f_update(f0, cu, ku0, cl, kl0);
+    f1 = f_update(f1, cu, ku1, cl, kl1);
+    a0 = p0 == pu ? ps.au : (p0 == pl ? ps.al : a0);
+    a1 = p1 == pu ? ps.au : (p1 == pl ? ps.al : a1);
   }
   if (v0) S.bn[p0] = a0;
   if (v1) S.bn[p1] = a1;
-  if (lane == 0) S.steps = tt - t;
+  if (lane == 0) S.steps = inner;
 }
 
 __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
@@ -468,21 +562,24 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
 
     // ---- 3. the pair steps on B: K_BB into LDS, then one wave of the solving workgroup
     const bool rows_in_lds = owner && !solo && m * len <= WS_QMAX * WS_QMAX;
+    if (tid < m) S.roff[tid] = ws_gmap(P, S.bi[tid]) * sp.ld;
+    __syncthreads();
     if (solver) {
-      for (int e0 = 0; e0 < m * m; e0 += WS_BS * WS_GATHER) {
+      // K_BB: flat indices clamped to the last element, so the loads of a batch issue back to
+      // back; only the stores are guarded
+      const int mm = m * m;
+      for (int e0 = 0; e0 < mm; e0 += WS_BS * WS_GATHER) {
         float kv[WS_GATHER];
 #pragma unroll
         for (int b = 0; b < WS_GATHER; ++b) {
-          const int e = e0 + b * WS_BS + tid;
-          if (e < m * m) {
-            const int ra = e / m, cb = e - ra * m;
-            kv[b] = sp.gram[ws_gmap(P, S.bi[ra]) * sp.ld + ws_gmap(P, S.bi[cb])];
-          }
+          const int e = min(e0 + b * WS_BS + tid, mm - 1);
+          const int ra = e / m, cb = e - ra * m;
+          kv[b] = sp.gram[S.roff[ra] + ws_gmap(P, S.bi[cb])];
         }
 #pragma unroll
         for (int b = 0; b < WS_GATHER; ++b) {
           const int e = e0 + b * WS_BS + tid;
-          if (e < m * m) {
+          if (e < mm) {
             const int ra = e / m, cb = e - ra * m;
             S.u.K[ra * WS_QMAX + cb] = kv[b];
           }
@@ -507,20 +604,19 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     } else {
       // owners: the Gram rows of B over the own samples into LDS while the pair steps run
       if (rows_in_lds) {
-        for (int e0 = 0; e0 < m * len; e0 += WS_BS * WS_GATHER) {
+        const int ml = m * len;
+        for (int e0 = 0; e0 < ml; e0 += WS_BS * WS_GATHER) {
           float kv[WS_GATHER];
 #pragma unroll
           for (int b = 0; b < WS_GATHER; ++b) {
-            const int e = e0 + b * WS_BS + tid;
-            if (e < m * len) {
-              const int ra = e / len, pos = e - ra * len;
-              kv[b] = sp.gram[ws_gmap(P, S.bi[ra]) * sp.ld + ws_gmap(P, base + pos)];
-            }
+            const int e = min(e0 + b * WS_BS + tid, ml - 1);
+            const int ra = e / len, pos = e - ra * len;
+            kv[b] = sp.gram[S.roff[ra] + ws_gmap(P, base + pos)];
           }
 #pragma unroll
           for (int b = 0; b < WS_GATHER; ++b) {
             const int e = e0 + b * WS_BS + tid;
-            if (e < m * len) S.u.K[e] = kv[b];
+            if (e < ml) S.u.K[e] = kv[b];
           }
         }
       }
@@ -543,12 +639,20 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         const bool v0 = p0 < m, v1 = p1 < m;
         const double c0 = v0 ? (S.bn[p0] - S.ba[p0]) * (double)S.by[p0] : 0.0;
         const double c1 = v1 ? (S.bn[p1] - S.ba[p1]) * (double)S.by[p1] : 0.0;
-        if (v0) S.bc[p0] = c0;
-        if (v1) S.bc[p1] = c1;
         const u64 m0 = __ballot(v0 && c0 != 0.0), m1 = __ballot(v1 && c1 != 0.0);
         const u64 below = (1ull << lane) - 1ull;
-        if (v0 && c0 != 0.0) S.nzp[__popcll(m0 & below)] = p0;
-        if (v1 && c1 != 0.0) S.nzp[__popcll(m0) + __popcll(m1 & below)] = p1;
+        if (v0 && c0 != 0.0) {
+          const int r = __popcll(m0 & below);
+          S.nzp[r] = p0;
+          S.nzoff[r] = S.roff[p0];
+          S.nzc[r] = c0;
+        }
+        if (v1 && c1 != 0.0) {
+          const int r = __popcll(m0) + __popcll(m1 & below);
+          S.nzp[r] = p1;
+          S.nzoff[r] = S.roff[p1];
+          S.nzc[r] = c1;
+        }
         const int nnz = __popcll(m0) + __popcll(m1);
         if (lane == 0) S.nnz = nnz;
       }
@@ -570,19 +674,15 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
           const int r0 = g * nnz / WS_QUARTERS, r1 = (g + 1) * nnz / WS_QUARTERS;
           double s = 0.0;
           if (rows_in_lds) {
-            for (int r = r0; r < r1; ++r) {
-              const int pe = S.nzp[r];
-              s = ws_acc(s, S.bc[pe], S.u.K[pe * len + pos]);
-            }
+            for (int r = r0; r < r1; ++r) s = ws_acc(s, S.nzc[r], S.u.K[S.nzp[r] * len + pos]);
           } else {
             for (int r = r0; r < r1; r += WS_GATHER) {
               float kk[WS_GATHER];
 #pragma unroll
-              for (int e = 0; e < WS_GATHER; ++e)
-                if (r + e < r1) kk[e] = sp.gram[ws_gmap(P, S.bi[S.nzp[r + e]]) * sp.ld + gj];
+              for (int e = 0; e < WS_GATHER; ++e) kk[e] = sp.gram[S.nzoff[min(r + e, r1 - 1)] + gj];
 #pragma unroll
               for (int e = 0; e < WS_GATHER; ++e)
-                if (r + e < r1) s = ws_acc(s, S.bc[S.nzp[r + e]], kk[e]);
+                if (r + e < r1) s = ws_acc(s, S.nzc[r + e], kk[e]);
             }
           }
           S.part[g][pos] = s;
