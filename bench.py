@@ -15,7 +15,9 @@ path, all pairs in one launch, for a fixed number of steps (4 n_p d + 21 n_p byt
 step).  ``paper_shapes`` times single trainings at the shapes of the paper's own runs (102
 features, 200-800 samples per class, binary and nine-class one-vs-one) for context.
 ``workloads`` trains the other binary workloads (1,000 x 16, 50,000 x 128, 100,000 x 32) end to
-end once each.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
+end once each.  ``working_set`` trains the Gram-path workloads with the working-set solver
+(svm_options.working_set = q: rounds of pair steps on q samples, f updated once a round) beside
+the pair solver; its iterations are pair steps too.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
 (first SMO steps of the same problem, on this host's cores).
 """
 from __future__ import annotations
@@ -69,6 +71,8 @@ def main():
     ap.add_argument("--no-ovo", action="store_true", help="skip the one-vs-one measurement (60000x784, 10 classes)")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the end-to-end trainings of the other binary workloads")
+    ap.add_argument("--ws-q", type=str, default="32,128",
+                    help="working-set sizes of the working-set leg, comma separated ('' = skip)")
     ap.add_argument("--no-paper-shapes", action="store_true",
                     help="skip the context runs at the paper's shapes (d=102, 200-800 per class)")
     ap.add_argument("--ovo-row-steps", type=int, default=300,
@@ -256,6 +260,37 @@ def main():
             del Xkd, ykd, rk
             torch.cuda.empty_cache()
         result["workloads"] = per
+
+    if args.ws_q:
+        # the working-set solver (rounds of pair steps on q samples, f updated once a round)
+        # beside the pair solver, end to end on the Gram-path workloads: one warm-up and one
+        # timed training each; iterations are pair steps, as for the pair solver
+        qs = [int(v) for v in args.ws_q.split(",") if v]
+        wsr = {}
+        for cid in (1, 2, 3):
+            wk = synth.workload(cid)
+            Xk, yk, _, _ = synth.generate(cid, m=1)
+            Xkd, ykd = torch.from_numpy(Xk).cuda(), torch.from_numpy(yk).cuda()
+            ent = {}
+            for q in [0] + qs:
+                svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, gram=svmx.GRAM_ON, working_set=q)
+                torch.cuda.synchronize()
+                t1 = time.perf_counter()
+                rk = svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, gram=svmx.GRAM_ON, working_set=q)
+                torch.cuda.synchronize()
+                tk = time.perf_counter() - t1
+                sk = rk.stats
+                ent["pair" if q == 0 else f"q{q}"] = {
+                    "train_seconds": tk, "smo_iterations": sk["iterations"], "rounds": sk["rounds"],
+                    "iters_per_s": sk["iterations"] / sk["t_solve"], "solver_kernel_seconds": sk["t_kernel"],
+                    "dual_obj": sk["dual_obj"]}
+                del rk
+            for key, e in ent.items():
+                e["speedup_vs_pair"] = ent["pair"]["train_seconds"] / e["train_seconds"]
+            wsr[wk.name] = ent
+            del Xkd, ykd
+            torch.cuda.empty_cache()
+        result["working_set"] = wsr
 
     if not args.no_paper_shapes:
         # context runs of the paper's shapes (102 features, 200-800 samples per class; binary and
