@@ -89,9 +89,11 @@ typedef struct {
                                 q/2 smallest f of I_up and the q/2 largest of I_low (ties to the
                                 smaller index), pair steps on B alone until its gap is at most
                                 max(tol, 0.5 x the round's gap) or 100 q steps, then f updated once
-                                from the round's change.  Needs the Gram and n <= 261,120 (255
-                                workgroups of up to 1,024 samples); binary training only.  The
-                                trace then holds the maximal violating pair of every round. */
+                                from the round's change.  Gram path: n <= 261,120 (255
+                                workgroups of up to 1,024 samples).  Row path: every round
+                                evaluates K(B, .) from X in one pass, n <= 255 x min(1024,
+                                16384 / q).  Binary training only.  The trace then holds the
+                                maximal violating pair of every round. */
 } svm_options;
 
 typedef struct {

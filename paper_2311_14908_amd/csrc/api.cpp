@@ -149,10 +149,13 @@ bool choose_shape(int64_t n, bool gram, int32_t requested, int32_t levels, Shape
 // lists: one level up to 16 owners, else groups of ceil(sqrt(nwg)).
 constexpr int32_t WS_MAX_WG = 255;
 
-bool choose_ws_shape(int64_t n, int32_t requested, Shape *s) {
+bool choose_ws_shape(int64_t n, int32_t requested, int32_t q, bool gram, Shape *s) {
   int64_t nwg = requested > 0 ? requested : std::min<int64_t>(WS_MAX_WG, (n + 63) / 64);
   nwg = std::max<int64_t>(1, std::min<int64_t>(nwg, n));
-  const int64_t smax = ws_slice_max();
+  // row path: at least two owners (the solving workgroup holds K_BB while the owners hold
+  // K(B, own samples)), and q x samples per owner within the LDS row buffer
+  const int64_t smax = gram ? ws_slice_max() : std::min<int64_t>(ws_slice_max(), ws_row_cap() / q);
+  if (!gram) nwg = std::max<int64_t>(nwg, 2);
   if ((n + nwg - 1) / nwg > smax) nwg = (n + smax - 1) / smax;
   if (nwg > WS_MAX_WG) return false;
   const int64_t per_wg = (n + nwg - 1) / nwg;
@@ -205,10 +208,9 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
     p->gram = gram_bytes <= (double)o.gram_budget;
   if (p->gram && gram_bytes > 9.0e18) return fail(SVM_ENOMEM, "Gram size overflows");
   if (o.working_set > 0) {
-    if (!p->gram) return fail(SVM_EINVAL, "the working-set solver needs the Gram (gram ON, or AUTO within budget)");
-    if (!choose_ws_shape(n, o.workgroups, &p->shape))
-      return fail(SVM_ENOMEM, "n=%lld exceeds the working-set solver's %d x %d samples", (long long)n, WS_MAX_WG,
-                  ws_slice_max());
+    if (!choose_ws_shape(n, o.workgroups, o.working_set, p->gram, &p->shape))
+      return fail(SVM_ENOMEM, "n=%lld exceeds the working-set solver's %d workgroups of %d samples", (long long)n,
+                  WS_MAX_WG, p->gram ? ws_slice_max() : std::min(ws_slice_max(), ws_row_cap() / o.working_set));
   } else if (!choose_shape(n, p->gram, o.workgroups, o.levels, &p->shape)) {
     return fail(SVM_ENOMEM, "problem too large to place");
   }
@@ -222,7 +224,9 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   Layout L;
   p->off_f = L.add(8 * n);
   p->off_gram = p->gram ? L.add((int64_t)gram_bytes) : -1;
-  p->off_split = (p->gram && o.gram_mfma == SVM_MFMA_SPLIT_F16) ? L.add(gram_split_scratch_bytes(n, d)) : -1;
+  // split rows: the split-fp16 Gram, or the working-set row path (which evaluates its rows with them)
+  const bool split = (p->gram && o.gram_mfma == SVM_MFMA_SPLIT_F16) || (!p->gram && o.working_set > 0);
+  p->off_split = split ? L.add(gram_split_scratch_bytes(n, d)) : -1;
   p->off_sqn = p->gram ? -1 : L.add(8 * n);
   p->off_cache = p->cache_cap ? L.add(4LL * p->cache_cap * p->ld) : -1;
   p->off_tags = p->cache_cap ? L.add(4LL * p->cache_cap * p->shape.nwg) : -1;
@@ -531,6 +535,8 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     HIPCHK(launch_gram_split(X, n, d, (float)gamma, G, p.ld, ws + p.off_split, stream));
   else if (p.gram)
     HIPCHK(launch_gram(X, n, d, (float)gamma, G, p.ld, stream));
+  else if (r.working_set > 0)
+    HIPCHK(launch_split_rows(X, n, d, split_views(ws + p.off_split, n, d), stream));
   else
     HIPCHK(launch_row_norms(X, n, d, sqn, stream));
   HIPCHK(hipEventRecord(tg.b, stream));
@@ -570,6 +576,10 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     wp.frac = WS_FRAC;
     wp.q = r.working_set;
     wp.max_inner = WS_INNER_PER_Q * r.working_set;
+    if (!p.gram) {
+      wp.split = split_views(ws + p.off_split, n, d);
+      wp.cexp = (float)(-gamma * 1.4426950408889634);
+    }
     const int32_t nwg = p.shape.nwg + (p.shape.nwg > 1 ? 1 : 0);  // owners and the solving workgroup
     s1 = run_launches([&](int32_t *maxres) { return launch_ws_solver(wp, nwg, stream, maxres); }, err, 1, nwg, ctl,
                       stream, &launches, hc, &t_kernel);

@@ -51,8 +51,10 @@ hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t
                               const PredictScratch &ws, hipStream_t s);
 hipError_t launch_ovo_vote(const double *dec, int64_t m, int32_t k, int32_t *pred, hipStream_t s);
 
-// Working-set solver (ws_smo.hip): one problem per launch, Gram path, nwg sample-owning
-// workgroups plus, when nwg > 1, one solving workgroup (launch nwg + 1).  Prob::slots holds
+// Working-set solver (ws_smo.hip): one problem per launch, nwg sample-owning workgroups plus,
+// when nwg > 1, one solving workgroup (launch nwg + 1).  Gram path, or row path (sp.gram NULL:
+// every round each owner evaluates K(B, own samples) from the split rows; needs nwg >= 2 and
+// q * per_wg <= ws_row_cap()).  Prob::slots holds
 // [2][nwg][ws_list_words()] candidate words, Prob::slots2 [2][ng][ws_list_words()] group
 // lists followed by ws_bcast_words() words for the solving workgroup's results; Ctl::t counts
 // pair steps; rounds[problem] counts rounds (ws_slice_max() samples per workgroup at most; q
@@ -63,12 +65,16 @@ struct WsParams {
   double frac;       // local tolerance factor
   int32_t q;         // working-set size
   int32_t max_inner; // pair steps per round at most
+  SplitX split;      // row path (sp.gram == NULL): split-fp16 rows of X, scales and norms
+  float cexp;        // row path: -gamma * log2(e)
+  int32_t pad;
 };
 hipError_t launch_ws_solver(const WsParams &p, int32_t total_wg, hipStream_t s, int32_t *max_coresident);
 int ws_slice_max();
 int ws_q_max();
 int64_t ws_list_words();
 int64_t ws_bcast_words();
+int ws_row_cap();
 
 int solver_block_size(bool gram);
 int max_per_thread(bool gram);

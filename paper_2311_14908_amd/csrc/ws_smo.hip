@@ -29,6 +29,9 @@
 
 namespace svmx {
 
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
 constexpr int WS_BS = 256;
 constexpr int WS_NW = WS_BS / 64;
 constexpr int WS_QMAX = 128;        // working-set size limit (lists of 64 per side)
@@ -45,7 +48,8 @@ constexpr unsigned VSENT = 0xffffffffu;
 int ws_slice_max() { return WS_SLICE_MAX; }
 int ws_q_max() { return WS_QMAX; }
 int64_t ws_list_words() { return WS_LIST_WORDS; }
-int64_t ws_bcast_words() { return 2LL * WS_BCAST_PITCH; }
+int64_t ws_bcast_words() { return 2LL * WS_BCAST_PITCH + 2LL * WS_QMAX * WS_QMAX; }
+int ws_row_cap() { return WS_QMAX * WS_QMAX; }
 
 // ---------------------------------------------------------------- sorted lists in a wave
 // A list is 64 (key, value) pairs, one per lane, ascending in lexicographic order; value is a
@@ -247,13 +251,26 @@ struct WsLds {
       u64 ab[2][WS_LISTS_MAX * 64];
     } st;
     float K[WS_QMAX * WS_QMAX];  // solver: K_BB; owners: the Gram rows of B over the own samples
+    struct {
+      h8 b[2][8][WS_QMAX];  // row path, one block of samples: B rows, [hi, lo][k chunk][row]
+      h8 s[2][8][128];      // and the samples, 64 features a stage
+    } rs64;
   } u;
-  double part[WS_QUARTERS][WS_SLICE_MAX];
+  union {
+    double part[WS_QUARTERS][WS_SLICE_MAX];
+    struct {
+      h8 b[2][4][WS_QMAX];  // row path: B rows, [hi, lo][k chunk of 8][row]
+      h8 s[2][4][128];      // and a block of own samples, [hi, lo][k chunk][column]
+    } rs;
+  } w;
   int bi[WS_QMAX];
   signed char by[WS_QMAX];
   double bf[WS_QMAX], ba[WS_QMAX], bn[WS_QMAX];
   int nzp[WS_QMAX];
   int64_t roff[WS_QMAX];   // Gram row offset of B_p
+  float bsc[WS_QMAX], bnr[WS_QMAX];  // row path: scale and squared norm of B_p
+  int own[WS_QMAX];        // positions of B among this workgroup's samples
+  int nown;
   int64_t nzoff[WS_QMAX];  // Gram row offset and change of the r-th nonzero change
   double nzc[WS_QMAX];
   int nu, nl, m, nnz, il, abort_flag;
@@ -373,6 +390,254 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, const WsParams &
   if (lane == 0) S.steps = inner;
 }
 
+// Row path: K(x_{B_p}, x_j) for p < m and the workgroup's samples j < len into
+// S.u.K[p * len + j] (m * len <= WS_QMAX^2).  The products run on v_mfma_f32_16x16x32_f16 with
+// the split-fp16 rows (hi and lo halves, three products into one fp32 accumulator), the same
+// arithmetic as the Gram kernel's: K = exp2(c max(0, n_p + n_j - 2 s_p s_j acc)), 1 between
+// identical samples.  Samples go in blocks of 128 columns; both operands pass through LDS one
+// chunk of 32 features at a time, with the global loads of the next two chunks in flight while
+// a chunk is multiplied; wave w takes the 16 x 16 tiles w, w + 4, ...  Not inlined: its
+// accumulators and load buffers get registers of their own.
+struct RowLoad {
+  h8 r[8];  // this thread's share of a chunk: [B hi x2, B lo x2, samples hi x2, samples lo x2]
+};
+
+__device__ __forceinline__ void row_chunk_load(RowLoad &L, const SplitX &X, int64_t gb, int64_t gs, int64_t k0,
+                                               int lkq) {
+#pragma unroll
+  for (int sl = 0; sl < 2; ++sl) {
+    const _Float16 *hb = sl ? X.lo : X.hi;
+    if (gb >= 0) {
+      const h8 *q8 = reinterpret_cast<const h8 *>(hb + gb * X.dp + k0) + lkq;
+      L.r[2 * sl] = q8[0];
+      L.r[2 * sl + 1] = q8[1];
+    } else {
+      L.r[2 * sl] = (h8){};
+      L.r[2 * sl + 1] = (h8){};
+    }
+    if (gs >= 0) {
+      const h8 *q8 = reinterpret_cast<const h8 *>(hb + gs * X.dp + k0) + lkq;
+      L.r[4 + 2 * sl] = q8[0];
+      L.r[4 + 2 * sl + 1] = q8[1];
+    } else {
+      L.r[4 + 2 * sl] = (h8){};
+      L.r[4 + 2 * sl + 1] = (h8){};
+    }
+  }
+}
+
+__device__ __forceinline__ void row_chunk_store(WsLds &S, const RowLoad &L, int lrow, int lkq) {
+#pragma unroll
+  for (int sl = 0; sl < 2; ++sl) {
+    S.w.rs.b[sl][lkq][lrow] = L.r[2 * sl];
+    S.w.rs.b[sl][lkq + 1][lrow] = L.r[2 * sl + 1];
+    S.w.rs.s[sl][lkq][lrow] = L.r[4 + 2 * sl];
+    S.w.rs.s[sl][lkq + 1][lrow] = L.r[4 + 2 * sl + 1];
+  }
+}
+
+__device__ __forceinline__ void row_chunk_mma(WsLds &S, v4f (&acc)[16], int ntile, int tj_n) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kq = lane >> 4, r16 = lane & 15;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int tile = wave + 4 * i;
+    if (tile < ntile) {
+      const int tp = tile / tj_n, tj = tile - tp * tj_n;
+      const h8 ah = S.w.rs.b[0][kq][tp * 16 + r16], al = S.w.rs.b[1][kq][tp * 16 + r16];
+      const h8 bh = S.w.rs.s[0][kq][tj * 16 + r16], bl = S.w.rs.s[1][kq][tj * 16 + r16];
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh, acc[i], 0, 0, 0);
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl, acc[i], 0, 0, 0);
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh, acc[i], 0, 0, 0);
+    }
+  }
+}
+
+// One block of at most 128 samples (the usual case): stages of 64 features staged in S.u (the
+// destination of the results, free until the last stage), two stages in flight; every load
+// instruction of a wave reads 8 whole 128-byte lines (16 bytes a lane: thread t takes chunk
+// t % 8 of half (t / 8) % 2 of rows t / 16 + 16 i); wave w takes the row tiles w and w + 4 with
+// every column tile, so each operand read from LDS feeds up to 8 (A) or 2 (B) tiles.
+struct RowLoad64 {
+  h8 b[8], s[8];  // rows t / 16 + 16 i of B and of the samples
+};
+
+__device__ __forceinline__ void row64_load(RowLoad64 &L, const SplitX &X, const int64_t (&gb)[8],
+                                           const int64_t (&gs)[8], int64_t k0, bool full) {
+  const int c = threadIdx.x & 7, half = (threadIdx.x >> 3) & 1;
+  const _Float16 *hb = half ? X.lo : X.hi;
+  const bool in = full || c < 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    L.b[i] = (gb[i] >= 0 && in) ? reinterpret_cast<const h8 *>(hb + gb[i] * X.dp + k0)[c] : (h8){};
+    L.s[i] = (gs[i] >= 0 && in) ? reinterpret_cast<const h8 *>(hb + gs[i] * X.dp + k0)[c] : (h8){};
+  }
+}
+
+__device__ __forceinline__ void row64_store(WsLds &S, const RowLoad64 &L) {
+  const int c = threadIdx.x & 7, half = (threadIdx.x >> 3) & 1, r0 = threadIdx.x >> 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    S.u.rs64.b[half][c][r0 + 16 * i] = L.b[i];
+    S.u.rs64.s[half][c][r0 + 16 * i] = L.s[i];
+  }
+}
+
+__device__ __forceinline__ void row64_mma(WsLds &S, v4f (&acc)[2][8], int tp_n, int tj_n, int ksteps) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kq = lane >> 4, r16 = lane & 15;
+  for (int ks = 0; ks < ksteps; ++ks) {
+    const int c = ks * 4 + kq;
+    h8 ah[2], al[2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      const int tp = wave + 4 * a;
+      ah[a] = S.u.rs64.b[0][c][(tp & 7) * 16 + r16];
+      al[a] = S.u.rs64.b[1][c][(tp & 7) * 16 + r16];
+    }
+#pragma unroll
+    for (int tj = 0; tj < 8; ++tj) {
+      if (tj < tj_n) {
+        const h8 bh = S.u.rs64.s[0][c][tj * 16 + r16], bl = S.u.rs64.s[1][c][tj * 16 + r16];
+#pragma unroll
+        for (int a = 0; a < 2; ++a) {
+          if (wave + 4 * a < tp_n) {
+            acc[a][tj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bh, acc[a][tj], 0, 0, 0);
+            acc[a][tj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[a], bl, acc[a][tj], 0, 0, 0);
+            acc[a][tj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[a], bh, acc[a][tj], 0, 0, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
+__device__ __attribute__((noinline)) void owner_rows_block(WsLds &S, const WsParams &p, const Prob &P, int m,
+                                                          int64_t base, int len) {
+  const SplitX &X = p.split;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kq = lane >> 4, r16 = lane & 15;
+  const int nst = (int)((X.dp + 63) / 64);  // stages; the last one holds 32 features when dp % 64 == 32
+  const int tp_n = (m + 15) / 16, tj_n = (len + 15) / 16;
+  int64_t gb[8], gs[8];  // this thread's rows of B and of the samples (-1: past the end)
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = (tid >> 4) + 16 * i;
+    gb[i] = r < m ? ws_gmap(P, S.bi[r]) : -1;
+    gs[i] = r < len ? ws_gmap(P, base + r) : -1;
+  }
+  v4f acc[2][8];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int tj = 0; tj < 8; ++tj) acc[a][tj] = (v4f){0.f, 0.f, 0.f, 0.f};
+  const auto full = [&](int st) { return (int64_t)st * 64 + 64 <= X.dp; };
+  RowLoad64 la, lb;
+  row64_load(la, X, gb, gs, 0, full(0));
+  if (nst > 1) row64_load(lb, X, gb, gs, 64, full(1));
+  for (int st = 0; st < nst; st += 2) {
+    __syncthreads();  // the previous stage's operands have been read
+    row64_store(S, la);
+    __syncthreads();
+    if (st + 2 < nst) row64_load(la, X, gb, gs, (int64_t)(st + 2) * 64, full(st + 2));
+    row64_mma(S, acc, tp_n, tj_n, full(st) ? 2 : 1);
+    if (st + 1 >= nst) break;
+    __syncthreads();
+    row64_store(S, lb);
+    __syncthreads();
+    if (st + 3 < nst) row64_load(lb, X, gb, gs, (int64_t)(st + 3) * 64, full(st + 3));
+    row64_mma(S, acc, tp_n, tj_n, full(st + 1) ? 2 : 1);
+  }
+  __syncthreads();  // S.u now receives the results
+  // lane l holds rows 4 (l / 16) + e and column l % 16 of each tile
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    const int tp = wave + 4 * a;
+    if (tp < tp_n) {
+#pragma unroll
+      for (int tj = 0; tj < 8; ++tj) {
+        const int j = tj * 16 + r16;
+        if (tj < tj_n && j < len) {
+          const int64_t gj = ws_gmap(P, base + j);
+          const float sj = X.scale[gj], nj = X.nrm[gj];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int pr = tp * 16 + 4 * kq + e;
+            if (pr < m) {
+              const float dot = (acc[a][tj][e] * S.bsc[pr]) * sj;
+              float t = S.bnr[pr] + nj - 2.0f * dot;
+              t = t > 0.f ? t : 0.f;
+              S.u.K[pr * len + j] = (S.bi[pr] == base + j) ? 1.0f : __builtin_amdgcn_exp2f(p.cexp * t);
+            }
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+}
+
+__device__ __attribute__((noinline)) void owner_rows(WsLds &S, const WsParams &p, const Prob &P, int m, int64_t base,
+                                                    int len) {
+  const SplitX &X = p.split;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kq = lane >> 4, r16 = lane & 15;
+  const int stages = (int)(X.dp / 32);
+  const int tp_n = (m + 15) / 16;
+  const int lrow = tid >> 1, lkq = (tid & 1) * 2;  // this thread's share of a chunk
+  const int64_t gb = lrow < m ? ws_gmap(P, S.bi[lrow]) : -1;
+  for (int j0 = 0; j0 < len; j0 += 128) {
+    const int cnt = min(128, len - j0);
+    const int tj_n = (cnt + 15) / 16;
+    const int ntile = tp_n * tj_n;
+    const int64_t gs = lrow < cnt ? ws_gmap(P, base + j0 + lrow) : -1;
+    v4f acc[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = (v4f){0.f, 0.f, 0.f, 0.f};
+    RowLoad la, lb;
+    row_chunk_load(la, X, gb, gs, 0, lkq);
+    if (stages > 1) row_chunk_load(lb, X, gb, gs, 32, lkq);
+    for (int st = 0; st < stages; st += 2) {
+      __syncthreads();  // the previous chunk's operands have been read
+      row_chunk_store(S, la, lrow, lkq);
+      __syncthreads();
+      if (st + 2 < stages) row_chunk_load(la, X, gb, gs, (int64_t)(st + 2) * 32, lkq);
+      row_chunk_mma(S, acc, ntile, tj_n);
+      if (st + 1 >= stages) break;
+      __syncthreads();
+      row_chunk_store(S, lb, lrow, lkq);
+      __syncthreads();
+      if (st + 3 < stages) row_chunk_load(lb, X, gb, gs, (int64_t)(st + 3) * 32, lkq);
+      row_chunk_mma(S, acc, ntile, tj_n);
+    }
+    // lane l holds rows 4 (l / 16) + e and column l % 16 of each tile
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int tile = wave + 4 * i;
+      if (tile < ntile) {
+        const int tp = tile / tj_n, tj = tile - tp * tj_n;
+        const int j = j0 + tj * 16 + r16;
+        if (j < len) {
+          const int64_t gj = ws_gmap(P, base + j);
+          const float sj = X.scale[gj], nj = X.nrm[gj];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int pr = tp * 16 + 4 * kq + e;
+            if (pr < m) {
+              const float dot = (acc[i][e] * S.bsc[pr]) * sj;
+              float t = S.bnr[pr] + nj - 2.0f * dot;
+              t = t > 0.f ? t : 0.f;
+              S.u.K[pr * len + j] = (S.bi[pr] == base + j) ? 1.0f : __builtin_amdgcn_exp2f(p.cexp * t);
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();  // the stage is rewritten by the next block
+  }
+}
+
+template <bool GRAM>
 __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
   __shared__ WsLds S;
   const SolveParams &sp = p.sp;
@@ -392,6 +657,10 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
   const int64_t base = owner ? (int64_t)rank * P.per_wg : 0;
   const int len = owner ? (int)min<int64_t>(P.per_wg, P.n - base) : 0;
   u64 *bcast = P.slots2 + 2 * (size_t)P.ng * WS_LIST_WORDS;
+  // row path: K_BB as published by the owners, [2][WS_QMAX][WS_QMAX] words of (32-bit round
+  // stamp, fp32 bits) -- 32-bit stamps, so a word of an earlier round never passes for a
+  // current one, whichever entries a round leaves untouched
+  u64 *kbuf = bcast + 2 * WS_BCAST_PITCH;
 
   for (int j = tid; j < len; j += WS_BS) {
     S.f[j] = P.f[base + j];
@@ -560,28 +829,85 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     else if (t >= sp.max_iter) status = ST_MAXITER;
     if (status != ST_RUNNING) break;
 
-    // ---- 3. the pair steps on B: K_BB into LDS, then one wave of the solving workgroup
-    const bool rows_in_lds = owner && !solo && m * len <= WS_QMAX * WS_QMAX;
-    if (tid < m) S.roff[tid] = ws_gmap(P, S.bi[tid]) * sp.ld;
+    // ---- 3. the pair steps on B: K_BB into LDS, then one wave of the solving workgroup.
+    // Gram path: the solving workgroup gathers K_BB from the Gram while the owners load the
+    // Gram rows of B over their own samples.  Row path: every owner evaluates K(B, own
+    // samples) and publishes the columns of K_BB of its own members of B; the solving
+    // workgroup collects them.
+    const bool rows_in_lds = GRAM ? owner && !solo && m * len <= WS_QMAX * WS_QMAX : owner;
+    const size_t kpar = par * (size_t)(WS_QMAX * WS_QMAX);
+    const unsigned kstamp = (unsigned)(round + 1);
+    if (tid < m) {
+      const int64_t gb = ws_gmap(P, S.bi[tid]);
+      if (GRAM) {
+        S.roff[tid] = gb * sp.ld;
+      } else {
+        S.bsc[tid] = p.split.scale[gb];
+        S.bnr[tid] = p.split.nrm[gb];
+      }
+    }
+    if (!GRAM && owner && wave == 0) {
+      const int p0 = lane, p1 = lane + 64;
+      const bool o0 = p0 < m && S.bi[p0] >= base && S.bi[p0] < base + len;
+      const bool o1 = p1 < m && S.bi[p1] >= base && S.bi[p1] < base + len;
+      const u64 m0 = __ballot(o0), m1 = __ballot(o1);
+      const u64 below = (1ull << lane) - 1ull;
+      if (o0) S.own[__popcll(m0 & below)] = p0;
+      if (o1) S.own[__popcll(m0) + __popcll(m1 & below)] = p1;
+      const int cnt = __popcll(m0) + __popcll(m1);
+      if (lane == 0) S.nown = cnt;
+    }
     __syncthreads();
-    if (solver) {
-      // K_BB: flat indices clamped to the last element, so the loads of a batch issue back to
-      // back; only the stores are guarded
+    if (solver && !GRAM) {
+      // wait for every published entry of K_BB, WS_GATHER per thread at a time
       const int mm = m * m;
       for (int e0 = 0; e0 < mm; e0 += WS_BS * WS_GATHER) {
-        float kv[WS_GATHER];
+        unsigned pending = 0;
 #pragma unroll
-        for (int b = 0; b < WS_GATHER; ++b) {
-          const int e = min(e0 + b * WS_BS + tid, mm - 1);
-          const int ra = e / m, cb = e - ra * m;
-          kv[b] = sp.gram[S.roff[ra] + ws_gmap(P, S.bi[cb])];
+        for (int b = 0; b < WS_GATHER; ++b)
+          if (e0 + b * WS_BS + tid < mm) pending |= 1u << b;
+        const uint64_t t0 = wall_clock64();
+        while (pending) {
+#pragma unroll
+          for (int b = 0; b < WS_GATHER; ++b) {
+            if (pending & (1u << b)) {
+              const int e = e0 + b * WS_BS + tid;
+              const int ra = e / m, cb = e - ra * m;
+              const u64 w = ld_word(kbuf + kpar + (size_t)ra * WS_QMAX + cb);
+              if ((unsigned)(w >> 32) == kstamp) {
+                S.u.K[ra * WS_QMAX + cb] = __uint_as_float((unsigned)w);
+                pending &= ~(1u << b);
+              }
+            }
+          }
+          if (pending && wall_clock64() - t0 > sp.spin_limit) {
+            __hip_atomic_store(sp.error, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            S.abort_flag = 1;
+            break;
+          }
         }
+      }
+    }
+    if (solver) {
+      if (GRAM) {
+        // K_BB: flat indices clamped to the last element, so the loads of a batch issue back
+        // to back; only the stores are guarded
+        const int mm = m * m;
+        for (int e0 = 0; e0 < mm; e0 += WS_BS * WS_GATHER) {
+          float kv[WS_GATHER];
 #pragma unroll
-        for (int b = 0; b < WS_GATHER; ++b) {
-          const int e = e0 + b * WS_BS + tid;
-          if (e < mm) {
+          for (int b = 0; b < WS_GATHER; ++b) {
+            const int e = min(e0 + b * WS_BS + tid, mm - 1);
             const int ra = e / m, cb = e - ra * m;
-            S.u.K[ra * WS_QMAX + cb] = kv[b];
+            kv[b] = sp.gram[S.roff[ra] + ws_gmap(P, S.bi[cb])];
+          }
+#pragma unroll
+          for (int b = 0; b < WS_GATHER; ++b) {
+            const int e = e0 + b * WS_BS + tid;
+            if (e < mm) {
+              const int ra = e / m, cb = e - ra * m;
+              S.u.K[ra * WS_QMAX + cb] = kv[b];
+            }
           }
         }
       }
@@ -602,8 +928,22 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         if (tid == WS_BS - 1) st_word(bw, sw | (u64)S.steps);
       }
     } else {
+      if (!GRAM) {
+        // row path: K(B, own samples) into LDS, then the columns of K_BB of the own members
+        if (len <= 128)
+          owner_rows_block(S, p, P, m, base, len);
+        else
+          owner_rows(S, p, P, m, base, len);
+        const int nk = S.nown * m;
+        for (int e = tid; e < nk; e += WS_BS) {
+          const int kk = e / m, a = e - kk * m;
+          const int pb = S.own[kk];
+          const float kv = S.u.K[a * len + (int)(S.bi[pb] - base)];
+          st_word(kbuf + kpar + (size_t)a * WS_QMAX + pb, ((u64)kstamp << 32) | (u64)__float_as_uint(kv));
+        }
+      }
       // owners: the Gram rows of B over the own samples into LDS while the pair steps run
-      if (rows_in_lds) {
+      if (GRAM && rows_in_lds) {
         const int ml = m * len;
         for (int e0 = 0; e0 < ml; e0 += WS_BS * WS_GATHER) {
           float kv[WS_GATHER];
@@ -685,12 +1025,12 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
                 if (r + e < r1) s = ws_acc(s, S.nzc[r + e], kk[e]);
             }
           }
-          S.part[g][pos] = s;
+          S.w.part[g][pos] = s;
         }
       }
       __syncthreads();
       for (int pos = tid; pos < len; pos += WS_BS) {
-        const double s = ((S.part[0][pos] + S.part[1][pos]) + S.part[2][pos]) + S.part[3][pos];
+        const double s = ((S.w.part[0][pos] + S.w.part[1][pos]) + S.w.part[2][pos]) + S.w.part[3][pos];
         S.f[pos] = S.f[pos] + s;
       }
     }
@@ -719,7 +1059,8 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
 }
 
 hipError_t launch_ws_solver(const WsParams &p, int32_t total_wg, hipStream_t s, int32_t *max_coresident) {
-  const void *fn = reinterpret_cast<const void *>(&ws_solve);
+  const void *fn = p.sp.gram ? reinterpret_cast<const void *>(&ws_solve<true>)
+                             : reinterpret_cast<const void *>(&ws_solve<false>);
   int dev = 0, cus = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;

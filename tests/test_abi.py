@@ -147,13 +147,18 @@ def test_working_set_options():
     # per list pair) in place of the pair solver's records
     w = ws(20_000, 784, working_set=128)
     assert w - ws(20_000, 784) >= 8 * 2 * (254 + 16) * 384 - 8 * 2 * (40 + 1) * 16
-    # the Gram is required, and n is limited to 255 workgroups of 1024 samples
-    assert ws(20_000, 784, working_set=64, gram=svmx.GRAM_OFF) == -1
+    # Gram path: n up to 255 workgroups of 1024 samples
     assert ws(261_120, 4, working_set=64, gram=svmx.GRAM_ON) > 0
     assert ws(261_121, 4, working_set=64, gram=svmx.GRAM_ON) == -1
+    # row path: q x samples per workgroup <= 16384, and the split rows of X in the workspace
+    for q, nmax in ((128, 255 * 128), (64, 255 * 256), (16, 255 * 1024)):
+        assert ws(nmax, 8, working_set=q, gram=svmx.GRAM_OFF) > 0, q
+        assert ws(nmax + 1, 8, working_set=q, gram=svmx.GRAM_OFF) == -1, q
+    split = 2 * 2 * 20_000 * 800 + 8 * 20_000
+    assert ws(20_000, 784, working_set=64, gram=svmx.GRAM_OFF) >= split
     st = lib.svm_train(FAKE, FAKE, 100, 4, 1.0, 0.5, 1e-3, FAKE, C.byref(C.c_double()), FAKE, 16,
                        C.byref(_opts(working_set=64, gram=svmx.GRAM_OFF)), None)
-    assert st == svmx.SVM_EINVAL and "Gram" in lib.svm_last_error().decode()
+    assert st == svmx.SVM_EWORKSPACE
 
 
 def test_predict_workspace_sizes():

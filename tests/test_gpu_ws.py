@@ -160,3 +160,65 @@ def test_ws_max_iter_not_converged_feasible():
     assert np.all(a >= 0) and np.all(a <= 1.0) and abs(a @ y) <= 1e-12 * len(y)
     np.testing.assert_allclose(a, ref.alpha, atol=1e-5, rtol=0)
     assert np.max(np.abs(f.cpu().numpy() - ref.f)) <= F_ATOL
+
+
+# --- row path: every round evaluates K(B, .) from X ---------------------------------------
+
+@pytest.mark.parametrize("q", [16, 64, 128])
+def test_ws_row_path_c0_against_oracle(c0, q):
+    X, y, Xt = c0
+    ref = oracle.train_ws(X, y, C0.C, C0.gamma, C0.tol, q, trace_len=2000)
+    out = svmx.svm_train(dev(X), dev(y), C0.C, C0.gamma, C0.tol, working_set=q, gram=svmx.GRAM_OFF, trace_len=2000)
+    assert out.status == svmx.SVM_OK and out.stats["gram_used"] == 0
+    k = agree_window(ref)
+    np.testing.assert_array_equal(out.trace_ul[:k], ref.trace_ul[:k])
+    np.testing.assert_allclose(out.trace_b[:k], ref.trace_b[:k], atol=F_ATOL, rtol=0)
+    assert abs(out.stats["dual_obj"] - ref.dual_obj) <= W_RTOL * abs(ref.dual_obj)
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= C0.C) and abs(a @ y) <= 1e-9 * C0.C * len(y)
+    d_gpu = svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, C0.gamma, dev(Xt)).cpu().numpy()
+    check_decisions(d_gpu, oracle.decision(X, y, ref.alpha, ref.b, Xt, C0.gamma))
+
+
+@pytest.mark.parametrize("cid,n,d,q,wgs", [(0, 3, 6, 128, 0), (0, 50, 6, 128, 0), (0, 1001, 6, 16, 5),
+                                           (0, 4000, 6, 64, 0), (0, 5000, 13, 128, 0), (1, 2000, 784, 64, 0),
+                                           (2, 3001, 128, 32, 0)])
+def test_ws_row_path_sizes(cid, n, d, q, wgs):
+    """Two to 63 owners, one and two merge levels, ragged blocks of samples (the MFMA tiles of
+    16 and the blocks of 128 columns), one to 25 feature chunks of 32: the rounds up to the
+    first near tie against the oracle, the optimum, feasibility and decisions (tol 1e-5)."""
+    wl = synth.workload(cid)
+    if cid == 0:
+        X, y = synth.two_blobs(n, d, seed=n + d)
+        if n == 3:
+            y = np.array([1, -1, 1], np.int32)
+        C_, g = 1.0, 0.3
+    else:
+        X, y, _, _ = synth.generate(cid, n=n, m=1, d=d)
+        C_, g = wl.C, wl.gamma
+    ref = oracle.train_ws(X, y, C_, g, 1e-5, q, trace_len=400)
+    out = svmx.svm_train(dev(X), dev(y), C_, g, 1e-5, working_set=q, workgroups=wgs, gram=svmx.GRAM_OFF, trace_len=400)
+    assert out.status == svmx.SVM_OK
+    k = agree_window(ref)
+    np.testing.assert_array_equal(out.trace_ul[:k], ref.trace_ul[:k])
+    np.testing.assert_allclose(out.trace_b[:k], ref.trace_b[:k], atol=F_ATOL, rtol=0)
+    assert abs(out.stats["dual_obj"] - ref.dual_obj) <= W_RTOL * abs(ref.dual_obj)
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= C_) and abs(a @ y) <= 1e-9 * C_ * len(y)
+    T = X[: min(n, 500)]
+    d_gpu = svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, g, dev(T)).cpu().numpy()
+    check_decisions(d_gpu, oracle.decision(X, y, ref.alpha, ref.b, T, g))
+
+
+def test_ws_row_path_configurations_agree():
+    """Every kernel value is computed from its two rows alone, so the owner count changes
+    nothing: bitwise equal results for 2 to 79 owners and any check cadence."""
+    X, y, _, _ = synth.generate(1, n=6000, m=1, d=200)
+    Xd, yd = dev(X), dev(y)
+    kw = dict(working_set=64, gram=svmx.GRAM_OFF, trace_len=300)
+    base = svmx.svm_train(Xd, yd, 10.0, 0.05, 1e-3, workgroups=24, **kw)
+    for wgs, ce in [(2, 0), (16, 0), (17, 0), (0, 0), (0, 300)]:
+        out = svmx.svm_train(Xd, yd, 10.0, 0.05, 1e-3, workgroups=wgs, check_every=ce, **kw)
+        assert out.stats["rounds"] == base.stats["rounds"], (wgs, ce)
+        np.testing.assert_array_equal(out.trace_ul, base.trace_ul)
+        assert torch.equal(out.alpha, base.alpha) and out.b == base.b, (wgs, ce)
