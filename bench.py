@@ -17,7 +17,8 @@ features, 200-800 samples per class, binary and nine-class one-vs-one) for conte
 ``workloads`` trains the other binary workloads (1,000 x 16, 50,000 x 128, 100,000 x 32) end to
 end once each.  ``working_set`` trains the Gram-path workloads with the working-set solver
 (svm_options.working_set = q: rounds of pair steps on q samples, f updated once a round) beside
-the pair solver; its iterations are pair steps too.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
+the pair solver, and the 20,000 x 784 workload once more without a Gram (row path); its
+iterations are pair steps too.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
 (first SMO steps of the same problem, on this host's cores).
 """
 from __future__ import annotations
@@ -288,6 +289,26 @@ def main():
             for key, e in ent.items():
                 e["speedup_vs_pair"] = ent["pair"]["train_seconds"] / e["train_seconds"]
             wsr[wk.name] = ent
+            if cid == 1:
+                # the same problem without a Gram: pair steps evaluate two rows of K from X a
+                # step, working-set rounds evaluate K(B, .) for all of B in one pass a round
+                rent = {}
+                for q in [0] + [v for v in qs if v <= 128]:
+                    kw = dict(gram=svmx.GRAM_OFF, working_set=q)
+                    svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, **kw)
+                    torch.cuda.synchronize()
+                    t1 = time.perf_counter()
+                    rk = svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, **kw)
+                    torch.cuda.synchronize()
+                    tk = time.perf_counter() - t1
+                    sk = rk.stats
+                    rent["pair" if q == 0 else f"q{q}"] = {
+                        "train_seconds": tk, "smo_iterations": sk["iterations"], "rounds": sk["rounds"],
+                        "iters_per_s": sk["iterations"] / sk["t_solve"], "dual_obj": sk["dual_obj"]}
+                    del rk
+                for key, e in rent.items():
+                    e["speedup_vs_pair"] = rent["pair"]["train_seconds"] / e["train_seconds"]
+                wsr[wk.name + " (row path)"] = rent
             del Xkd, ykd
             torch.cuda.empty_cache()
         result["working_set"] = wsr
