@@ -94,6 +94,11 @@ typedef struct {
                                 evaluates K(B, .) from X in one pass, n <= 255 x min(1024,
                                 16384 / q).  Binary training only.  The trace then holds the
                                 maximal violating pair of every round. */
+  int32_t resident_rows;     /* binary training, row path, per-step solver: rows of X each solver
+                                workgroup keeps in LDS for the whole launch (the first rows of its
+                                slice), read from there instead of from HBM at every step; 0 = as
+                                many as fit, -1 = none, k > 0 = at most k.  Results do not depend
+                                on it. */
 } svm_options;
 
 typedef struct {
@@ -110,6 +115,8 @@ typedef struct {
   double t_kernel;      /* seconds the solver kernel ran, summed over its launches (HIP events on
                            the launch stream) */
   int64_t rounds;       /* working-set rounds (0 for the per-step solver) */
+  int32_t resident_rows; /* rows of X each solver workgroup kept in LDS (binary row path) */
+  int32_t reserved;
 } svm_stats;
 
 /* Fill *o with the defaults above. */

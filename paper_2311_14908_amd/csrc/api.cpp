@@ -71,6 +71,7 @@ struct Opts {
   int32_t levels;
   int32_t gram_mfma;
   int32_t working_set;
+  int32_t resident_rows;
 };
 
 bool resolve(const svm_options *o, int64_t n, Opts *r) {
@@ -92,10 +93,11 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
   r->levels = o->exchange_levels;
   r->gram_mfma = o->gram_mfma;
   r->working_set = o->working_set;
+  r->resident_rows = o->resident_rows;
   const bool ws_ok = r->working_set == 0 ||
                      (r->working_set >= 2 && r->working_set <= ws_q_max() && r->working_set % 2 == 0);
   return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF && r->levels >= 0 && r->levels <= 2 &&
-         (r->gram_mfma == SVM_MFMA_SPLIT_F16 || r->gram_mfma == SVM_MFMA_F32) && ws_ok;
+         (r->gram_mfma == SVM_MFMA_SPLIT_F16 || r->gram_mfma == SVM_MFMA_F32) && ws_ok && r->resident_rows >= -1;
 }
 
 // How a problem of n samples is spread over workgroups.
@@ -218,8 +220,8 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   if (!p->gram) {
     if (o.row_cache_bytes > 0)
       p->cache_cap = (int32_t)std::min<int64_t>(CACHE_CAP_MAX, std::min<int64_t>(n, o.row_cache_bytes / (4 * p->ld)));
-    const int64_t lds = 2LL * solver_block_size(false) * p->shape.per_thread * 4 + 4LL * p->cache_cap + 8192;
-    if (lds > LDS_BYTES) return fail(SVM_EINVAL, "row path: row slices and cache tags do not fit the LDS");
+    const int64_t lds = 16LL * p->shape.per_wg + 4LL * p->cache_cap + 8192;
+    if (lds > LDS_BYTES) return fail(SVM_EINVAL, "row path: dot products and cache tags do not fit the LDS");
   }
   Layout L;
   p->off_f = L.add(8 * n);
@@ -559,6 +561,15 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   sp.cache = p.cache_cap ? reinterpret_cast<float *>(ws + p.off_cache) : nullptr;
   sp.cache_tags = p.cache_cap ? reinterpret_cast<int32_t *>(ws + p.off_tags) : nullptr;
   sp.cache_cap = p.cache_cap;
+  sp.max_per_wg = p.shape.per_wg;
+  sp.res_rows = 0;
+  if (!p.gram && r.working_set == 0 && r.resident_rows >= 0) {
+    const int64_t fit = solver_res_rows_max(sp, p.shape.per_thread);
+    if (fit < 0) return fail(SVM_EDEVICE, "row path: LDS capacity query failed");
+    int64_t res = std::min<int64_t>(fit, p.shape.per_wg);
+    if (r.resident_rows > 0) res = std::min<int64_t>(res, r.resident_rows);
+    sp.res_rows = (int32_t)res;
+  }
   sp.spin_limit = spin_ticks();
   sp.error = err;
   int32_t launches = 0;
@@ -622,6 +633,8 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     st->t_total = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
     st->t_kernel = t_kernel;
     st->rounds = r.working_set > 0 ? h_rounds : 0;
+    st->resident_rows = sp.res_rows;
+    st->reserved = 0;
   }
   return c.status == ST_MAXITER ? SVM_NOT_CONVERGED : SVM_OK;
 }
@@ -699,13 +712,14 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   std::vector<Prob> hp(p.P);
   std::vector<int32_t> hwgp;
   int64_t max_n = 0;
-  int32_t per_thread = 1, wg = 0;
+  int32_t per_thread = 1, wg = 0, max_per_wg = 1;
   // Spread a workgroup budget over the pairs; all pairs run in one cooperative launch.
   auto assign = [&](int64_t budget) -> svm_status {
     hwgp.clear();
     int64_t pack = 0;
     max_n = 0;
     per_thread = 1;
+    max_per_wg = 1;
     wg = 0;
     int32_t q = 0;
     for (int32_t a = 0; a < k; ++a)
@@ -732,6 +746,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
         P.nwg = sh.nwg;
         P.per_wg = sh.per_wg;
         per_thread = std::max(per_thread, sh.per_thread);
+        max_per_wg = std::max(max_per_wg, sh.per_wg);
         for (int32_t w = 0; w < sh.nwg; ++w) hwgp.push_back(q);
         wg += sh.nwg;
         pack += P.n;
@@ -750,6 +765,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
     SolveParams probe{};
     probe.X = Xs;
     probe.d = d;
+    probe.max_per_wg = max_per_wg;
     HIPCHK(launch_solver(probe, 0, per_thread, p.gram, stream, &capacity));
     if (capacity <= 0) return fail(SVM_ENOMEM, "the solver does not fit on the device");
     if (wg <= capacity || budget <= p.P) break;
@@ -810,6 +826,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   sp.X = Xs;
   sp.sqn = sqn;
   sp.d = d;
+  sp.max_per_wg = max_per_wg;
   sp.spin_limit = spin_ticks();
   sp.error = err;
   int32_t launches = 0;
@@ -858,6 +875,9 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
       S.t_finalize = tf.seconds();
       S.t_total = t_total;
       S.t_kernel = t_kernel;
+      S.rounds = 0;
+      S.resident_rows = 0;
+      S.reserved = 0;
     }
   }
   return maxed ? SVM_NOT_CONVERGED : SVM_OK;

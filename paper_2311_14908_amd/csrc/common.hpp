@@ -32,6 +32,10 @@ hipError_t launch_solver_init(const Prob *probs, int32_t nprob, int64_t max_n, h
 // total_wg <= 0 only reports in *max_coresident how many workgroups of the variant fit at once.
 hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
                          int32_t *max_coresident);
+// Row path: how many rows of X a solver workgroup can keep resident in LDS next to its other
+// LDS data (p's max_per_wg, cache_cap and d; per_thread as for launch_solver), or -1 on a HIP
+// error.
+int64_t solver_res_rows_max(const SolveParams &p, int32_t per_thread);
 hipError_t launch_finalize(const Prob *probs, int32_t nprob, double C, double *out /*[nprob][4]*/, hipStream_t s);
 // Device scratch of one prediction: compacted support vectors and per-split partial sums.
 struct PredictScratch {

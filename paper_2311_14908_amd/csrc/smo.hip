@@ -36,8 +36,9 @@ namespace svmx {
 // the streaming of X busy without spilling), up to 8 samples per thread.
 constexpr int BS_GRAM = 256, MAXP_GRAM = 16;
 constexpr int BS_ROWS = 512, MAXP_ROWS = 8;
-constexpr int ROW_BATCH = 2;  // samples per lane group and batch in the row evaluation
-constexpr int ROW_MAXM = 4;   // feature positions per lane whose loads are issued together
+constexpr int ROW_BATCH = 2;   // samples per lane group and batch of rows read from LDS
+constexpr int ROW_SBATCH = 2;  // samples per lane group and batch of rows streamed from HBM
+constexpr int ROW_MAXM = 4;    // feature positions per lane whose loads are issued together
 
 int solver_block_size(bool gram) { return gram ? BS_GRAM : BS_ROWS; }
 int max_per_thread(bool gram) { return gram ? MAXP_GRAM : MAXP_ROWS; }
@@ -207,8 +208,9 @@ template <int BS, int PER, bool GRAM, bool VEC4>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   constexpr int NW = BS / 64;
   constexpr int SB = ROW_BATCH;  // a sample's arithmetic does not depend on SB
-  extern __shared__ float4 dyn4[];  // row path: krow[2][per_wg], tags[cap]
-  float *dyn = reinterpret_cast<float *>(dyn4);
+  // Row path, dynamic LDS: dot products against x_u and x_l [2][per_wg] (fp64), cache tags
+  // [cap], then the rows of X this workgroup keeps resident [res][d] (16-byte aligned).
+  extern __shared__ float4 dyn4[];
   __shared__ SelLds<NW> sh;
   __shared__ int s_abort;
   __shared__ double s_kul;
@@ -240,11 +242,30 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
     }
   }
 
-  float *krow = dyn;  // [2][per_wg]
-  int *tags = reinterpret_cast<int *>(krow + 2 * (int64_t)P.per_wg);
+  double *dotu = reinterpret_cast<double *>(dyn4), *dotl = dotu + P.per_wg;
+  int *tags = reinterpret_cast<int *>(dotl + P.per_wg);
+  float *xres = reinterpret_cast<float *>(dyn4 + ((16 * (int64_t)P.per_wg + 4 * (int64_t)p.cache_cap + 15) >> 4));
   const bool use_cache = !GRAM && p.cache != nullptr && p.cache_cap > 0;
-  if (use_cache) {
-    for (int s = threadIdx.x; s < p.cache_cap; s += BS) tags[s] = p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s];
+  // Resident rows: the first `res` samples of the slice, copied once per launch; every step
+  // reads them from LDS instead of HBM.
+  const int64_t res = GRAM ? 0 : min<int64_t>(p.res_rows, max<int64_t>(0, lim - base));
+  double sq[PER];  // squared norms of the own samples (row path)
+  if (!GRAM) {
+    if (use_cache) {
+      for (int s = threadIdx.x; s < p.cache_cap; s += BS) tags[s] = p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s];
+    }
+    typedef typename Lane<VEC4>::T T;
+    const int64_t units = VEC4 ? (p.d >> 2) : p.d;
+    T *xr = reinterpret_cast<T *>(xres);
+    for (int64_t e = threadIdx.x; e < res * units; e += BS) {
+      const int64_t r = e / units, k = e - r * units;
+      xr[e] = reinterpret_cast<const T *>(p.X + gmap(P, base + r) * p.d)[k];
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+      sq[k] = j < lim ? p.sqn[gmap(P, j)] : 0.0;
+    }
   }
   __syncthreads();
 
@@ -333,26 +354,44 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         if (lig == 0) s_kul = (double)rbf_from_dot(nu, nl, pu1[0], p.gamma);
       }
       if (!(hit_u && hit_l)) {
+        typedef typename Lane<VEC4>::T T;
         const int64_t cnt = lim - base;
-        for (int64_t q0 = (int64_t)grp * SB; q0 < cnt; q0 += (int64_t)ngroups * SB) {
-          const int nb = (int)min<int64_t>(SB, cnt - q0);
-          const float *xs[SB];
-          double nj[SB];
+        // Streamed samples [res, cnt) go in batches of SBS per group; the first batch of each
+        // group is loaded before the resident samples are computed, so its HBM latency
+        // overlaps that work.
+        constexpr int SBS = ROW_SBATCH;
+        const int64_t sstride = (int64_t)ngroups * SBS;
+        int64_t qs = res + (int64_t)grp * SBS;
+        int nbs = 0;
+        const float *xs[SBS];
+        T vs[SBS][ROW_MAXM];
+        if (qs < cnt) {
+          nbs = (int)min<int64_t>(SBS, cnt - qs);
 #pragma unroll
-          for (int b = 0; b < SB; ++b) {
-            const int64_t g = gmap(P, base + q0 + min(b, nb - 1));
-            xs[b] = p.X + g * d;
-            nj[b] = p.sqn[g];
-          }
-          double du[SB], dl[SB];
-          dot_batch<VEC4, SB, ROW_MAXM>(xs, nb, xu, xl, d, lig, gs, rp, du, dl);
-          for (int v = lig; v < 2 * SB; v += gs) {
-            const int b = v < SB ? v : v - SB;
-            double njb = nj[0];
+          for (int b = 0; b < SBS; ++b) xs[b] = p.X + gmap(P, base + qs + min(b, nbs - 1)) * d;
+          load_block0<VEC4, SBS, ROW_MAXM>(vs, xs, nbs, d, lig, gs);
+        }
+        for (int64_t q0 = (int64_t)grp * SB; q0 < res; q0 += (int64_t)ngroups * SB) {
+          const int nb = (int)min<int64_t>(SB, res - q0);
+          const float *xr[SB];
 #pragma unroll
-            for (int q = 1; q < SB; ++q) njb = b == q ? nj[q] : njb;
-            if (b < nb)
-              krow[(v < SB ? 0 : P.per_wg) + q0 + b] = rbf_from_dot(v < SB ? nu : nl, njb, batch_value<SB>(du, dl, v), p.gamma);
+          for (int b = 0; b < SB; ++b) xr[b] = xres + (q0 + min(b, nb - 1)) * d;
+          T vr[SB][ROW_MAXM];
+          load_block0<VEC4, SB, ROW_MAXM, true>(vr, xr, nb, d, lig, gs);
+          float fu[SB], fl[SB];
+          dot_partials<VEC4, SB, ROW_MAXM, true>(vr, xr, nb, xu, xl, d, lig, gs, rp, fu, fl);
+          group_sums_store<SB>(fu, fl, nb, gs, lig, dotu + q0, dotl + q0);
+        }
+        while (qs < cnt) {
+          float fu[SBS], fl[SBS];
+          dot_partials<VEC4, SBS, ROW_MAXM>(vs, xs, nbs, xu, xl, d, lig, gs, rp, fu, fl);
+          group_sums_store<SBS>(fu, fl, nbs, gs, lig, dotu + qs, dotl + qs);
+          qs += sstride;
+          if (qs < cnt) {
+            nbs = (int)min<int64_t>(SBS, cnt - qs);
+#pragma unroll
+            for (int b = 0; b < SBS; ++b) xs[b] = p.X + gmap(P, base + qs + min(b, nbs - 1)) * d;
+            load_block0<VEC4, SBS, ROW_MAXM>(vs, xs, nbs, d, lig, gs);
           }
         }
       }
@@ -365,16 +404,18 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         const int64_t j = base + threadIdx.x + (int64_t)k * BS;
         if (j < lim) {
           const int64_t q = j - base;
-          ku[k] = hit_u ? p.cache[(size_t)su * p.ld + j] : krow[q];
-          kl[k] = hit_l ? p.cache[(size_t)sl * p.ld + j] : krow[P.per_wg + q];
+          ku[k] = hit_u ? p.cache[(size_t)su * p.ld + j] : rbf_from_dot(nu, sq[k], dotu[q], p.gamma);
+          kl[k] = hit_l ? p.cache[(size_t)sl * p.ld + j] : rbf_from_dot(nl, sq[k], dotl[q], p.gamma);
           if (store_u) p.cache[(size_t)su * p.ld + j] = ku[k];
           if (store_l) p.cache[(size_t)sl * p.ld + j] = kl[k];
         }
       }
-      __syncthreads();
-      if (threadIdx.x == 0) {
-        if (store_u) tags[su] = (int)gu;
-        if (store_l) tags[sl] = (int)gl;
+      if (use_cache) {
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          if (store_u) tags[su] = (int)gu;
+          if (store_l) tags[sl] = (int)gl;
+        }
       }
     }
     const PairStep ps = solve_pair(C, s.vu, s.vl, s.au, s.al, yu, yl, kul);
@@ -474,6 +515,17 @@ hipError_t launch_finalize(const Prob *probs, int32_t nprob, double C, double *o
   return hipGetLastError();
 }
 
+// Dynamic LDS of the row path: the fp64 dot products [2][per_wg], the cache tags, then `res`
+// resident rows of d floats from a 16-byte boundary.
+static size_t row_path_lds(const SolveParams &p, int64_t res) {
+  const int64_t head = (16 * (int64_t)p.max_per_wg + 4 * (int64_t)p.cache_cap + 15) & ~(int64_t)15;
+  return (size_t)(head + 4 * res * p.d);
+}
+
+static bool row_vec4(const SolveParams &p) {
+  return (p.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(p.X) & 15) == 0);
+}
+
 template <int BS, int PER, bool GRAM, bool VEC4>
 static hipError_t launch_one(const SolveParams &p, int32_t total_wg, size_t shmem, hipStream_t s, int32_t *maxres) {
   const void *fn = reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4>);
@@ -508,10 +560,8 @@ hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thr
       default: return hipErrorInvalidValue;
     }
   }
-  // row path: two row slices of per_wg floats, tags
-  const size_t per_wg = (size_t)BS_ROWS * per_thread;
-  const size_t shmem = 2 * per_wg * sizeof(float) + (size_t)p.cache_cap * sizeof(int) + 16;
-  const bool vec4 = (p.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(p.X) & 15) == 0);
+  const size_t shmem = row_path_lds(p, p.res_rows);
+  const bool vec4 = row_vec4(p);
   switch (per_thread * 2 + (vec4 ? 1 : 0)) {
     case 2: return launch_one<BS_ROWS, 1, false, false>(p, total_wg, shmem, s, max_coresident);
     case 3: return launch_one<BS_ROWS, 1, false, true>(p, total_wg, shmem, s, max_coresident);
@@ -523,6 +573,29 @@ hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thr
     case 17: return launch_one<BS_ROWS, 8, false, true>(p, total_wg, shmem, s, max_coresident);
     default: return hipErrorInvalidValue;
   }
+}
+
+int64_t solver_res_rows_max(const SolveParams &p, int32_t per_thread) {
+  int dev = 0, max_lds = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return -1;
+  const bool vec4 = row_vec4(p);
+  const void *fn = nullptr;
+  switch (per_thread * 2 + (vec4 ? 1 : 0)) {
+    case 2: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 1, false, false>); break;
+    case 3: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 1, false, true>); break;
+    case 4: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 2, false, false>); break;
+    case 5: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 2, false, true>); break;
+    case 8: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 4, false, false>); break;
+    case 9: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 4, false, true>); break;
+    case 16: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 8, false, false>); break;
+    case 17: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 8, false, true>); break;
+    default: return -1;
+  }
+  hipFuncAttributes attr;
+  if (hipFuncGetAttributes(&attr, fn) != hipSuccess) return -1;
+  const int64_t avail = (int64_t)max_lds - (int64_t)attr.sharedSizeBytes - (int64_t)row_path_lds(p, 0);
+  return avail > 0 ? avail / (4 * p.d) : 0;
 }
 
 }  // namespace svmx

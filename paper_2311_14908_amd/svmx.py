@@ -34,14 +34,16 @@ class svm_options(C.Structure):
                 ("row_cache_bytes", C.c_int64), ("max_iter", C.c_int64), ("check_every", C.c_int32),
                 ("trace_len", C.c_int32), ("trace_ws", C.POINTER(C.c_int32)), ("trace_b", C.POINTER(C.c_double)),
                 ("f_out", C.c_void_p), ("stream", C.c_void_p), ("workgroups", C.c_int32),
-                ("exchange_levels", C.c_int32), ("gram_mfma", C.c_int32), ("working_set", C.c_int32)]
+                ("exchange_levels", C.c_int32), ("gram_mfma", C.c_int32), ("working_set", C.c_int32),
+                ("resident_rows", C.c_int32)]
 
 
 class svm_stats(C.Structure):
     _fields_ = [("iterations", C.c_int64), ("n_sv", C.c_int64), ("n_bound_sv", C.c_int64), ("b_up", C.c_double),
                 ("b_low", C.c_double), ("dual_obj", C.c_double), ("gram_used", C.c_int32), ("launches", C.c_int32),
                 ("t_gram", C.c_double), ("t_solve", C.c_double), ("t_finalize", C.c_double), ("t_total", C.c_double),
-                ("t_kernel", C.c_double), ("rounds", C.c_int64)]
+                ("t_kernel", C.c_double), ("rounds", C.c_int64),
+                ("resident_rows", C.c_int32), ("reserved", C.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -108,8 +110,8 @@ def _dev(t: torch.Tensor, dtype, name):
 
 
 def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, check_every=0, trace_len=0,
-            workgroups=0, exchange_levels=0, gram_mfma=0, working_set=0, f_out: torch.Tensor | None = None,
-            stream=None):
+            workgroups=0, exchange_levels=0, gram_mfma=0, working_set=0, resident_rows=0,
+            f_out: torch.Tensor | None = None, stream=None):
     o = svm_options()
     load().svm_default_options(C.byref(o))
     o.gram = gram
@@ -123,6 +125,7 @@ def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, 
     o.exchange_levels = exchange_levels
     o.gram_mfma = gram_mfma
     o.working_set = working_set
+    o.resident_rows = resident_rows
     o.f_out = None if f_out is None else f_out.data_ptr()
     s = stream if stream is not None else torch.cuda.current_stream()
     o.stream = s.cuda_stream

@@ -37,9 +37,9 @@ def test_struct_layouts_match_header():
     lib = svmx.load()
     o = svmx.svm_options()
     lib.svm_default_options(C.byref(o))
-    assert o.struct_size == C.sizeof(svmx.svm_options) == 88
+    assert o.struct_size == C.sizeof(svmx.svm_options) == 96
     assert o.check_every == 65536 and o.gram == svmx.GRAM_AUTO
-    assert C.sizeof(svmx.svm_stats) == 104
+    assert C.sizeof(svmx.svm_stats) == 112
 
 
 def _opts(**kw):
@@ -175,3 +175,15 @@ def test_predict_m0_is_noop():
     lib = svmx.load()
     o = _opts()
     assert lib.svm_predict(FAKE, FAKE, FAKE, 0.0, 10, 4, 0.5, None, 0, None, FAKE, 256, C.byref(o)) == 0
+
+
+def test_resident_rows_option():
+    """resident_rows: -1 (none), 0 (as many as fit) or a positive cap; below -1 is rejected.
+    It does not change the workspace (the rows live in LDS)."""
+    lib = svmx.load()
+    ws = lambda n, d, **kw: lib.svm_train_workspace_bytes(n, d, C.byref(_opts(**kw)))
+    base = ws(20_000, 784, gram=svmx.GRAM_OFF)
+    assert base > 0
+    for r in (-1, 0, 1, 1000):
+        assert ws(20_000, 784, gram=svmx.GRAM_OFF, resident_rows=r) == base, r
+    assert ws(20_000, 784, gram=svmx.GRAM_OFF, resident_rows=-2) == -1

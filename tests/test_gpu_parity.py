@@ -421,3 +421,46 @@ def test_ovo_predict_matches_oracle_given_alpha():
     assert np.max(np.abs(dec.cpu().numpy() - dec_ref)) <= PRED_ATOL
     sure = np.all(np.abs(dec_ref) >= PRED_ATOL, axis=1)
     assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
+
+
+@pytest.mark.parametrize("n,d,res", [(3000, 784, 0), (3000, 784, -1), (3000, 784, 7), (2000, 16, 0), (2000, 100, 0),
+                                     (2000, 301, 0), (1500, 1500, 0), (1500, 1500, 3)])
+def test_row_path_step_uses_the_kernel_row_values(n, d, res):
+    """After one row-path step f equals -y + (c_u K(u, .) + c_l K(l, .)) evaluated on the host from
+    svm_kernel_rows' fp32 values, bit for bit, at every sample: the solver's row values are the
+    entry point's whether its rows of X sit in LDS (all of them, some, or none) or stream from
+    HBM, for lane groups of 64 (784 features), 32 (100) and 4 (16), scalar lanes (301) and rows
+    longer than one register block (301, 1500)."""
+    X, y = synth.two_blobs(n, d, seed=d + 1)
+    Xd, yd = dev(X), dev(y)
+    gamma = 1.0 / d
+    f = torch.empty(n, dtype=torch.float64, device="cuda")
+    out = svmx.svm_train(Xd, yd, 1.0, gamma, 1e-3, gram=svmx.GRAM_OFF, max_iter=1, trace_len=1, resident_rows=res,
+                         f_out=f)
+    assert out.stats["iterations"] == 1
+    st = out.stats["resident_rows"]
+    if res == -1:
+        assert st == 0
+    elif res > 0:
+        assert st == res
+    else:
+        assert st > 0
+    u, l = (int(v) for v in out.trace_ul[0])
+    K = svmx.svm_kernel_rows(Xd, gamma, np.array([u, l])).cpu().numpy().astype(np.float64)
+    a = out.alpha.cpu().numpy()
+    yf = y.astype(np.float64)
+    cu, cl = a[u] * yf[u], a[l] * yf[l]
+    np.testing.assert_array_equal(f.cpu().numpy(), -yf + (cu * K[0] + cl * K[1]))
+
+
+def test_resident_rows_do_not_change_results():
+    """A row-path training to convergence with every row of X streamed, with some resident in
+    LDS and with as many as fit: identical steps, multipliers and bias."""
+    X, y = synth.two_blobs(4000, 784, seed=11)
+    Xd, yd = dev(X), dev(y)
+    runs = [svmx.svm_train(Xd, yd, 1.0, 1.0 / 784, 1e-3, gram=svmx.GRAM_OFF, resident_rows=r) for r in (-1, 9, 0)]
+    assert runs[2].stats["resident_rows"] > 9
+    for r in runs[1:]:
+        assert r.stats["iterations"] == runs[0].stats["iterations"]
+        assert torch.equal(r.alpha, runs[0].alpha)
+        assert r.b == runs[0].b
