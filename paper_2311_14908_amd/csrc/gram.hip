@@ -177,7 +177,7 @@ template <bool VEC4>
 __global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X, int64_t n, int64_t d, double gamma,
                                                       const int64_t *__restrict__ rows, int64_t r,
                                                       float *__restrict__ out) {
-  constexpr int SB = 2, MAXM = 4;
+  constexpr int SB = 2, MAXM = ROW_POSITIONS;
   const int64_t q0 = 2 * (int64_t)blockIdx.y;
   const int64_t q1 = q0 + 1 < r ? q0 + 1 : q0;
   const int64_t ru = rows[q0], rl = rows[q1];

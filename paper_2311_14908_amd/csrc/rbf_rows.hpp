@@ -11,11 +11,18 @@
 
 namespace svmx {
 
-// Lanes per sample: a power of two covering d (float4 units when VEC4), at most 64.
+// Feature positions (float4 units when VEC4) each lane of a group takes in the first register
+// block of a row evaluation.
+constexpr int ROW_POSITIONS = 4;
+
+// Lanes per sample: the smallest power of two gs with ROW_POSITIONS * gs covering the row's
+// units, at most 64 (longer rows continue in later blocks).  So a short row does not leave most
+// of a lane's positions masked: its lanes each take up to ROW_POSITIONS units, and a wave holds
+// 64 / gs samples at once.
 __device__ __forceinline__ int group_size_for(int64_t d, bool vec4) {
   const int64_t units = vec4 ? (d + 3) / 4 : d;
   int gs = 1;
-  while (gs < units && gs < 64) gs <<= 1;
+  while ((int64_t)ROW_POSITIONS * gs < units && gs < 64) gs <<= 1;
   return gs;
 }
 

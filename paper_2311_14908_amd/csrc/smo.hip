@@ -38,7 +38,7 @@ constexpr int BS_GRAM = 256, MAXP_GRAM = 16;
 constexpr int BS_ROWS = 512, MAXP_ROWS = 8;
 constexpr int ROW_BATCH = 2;   // samples per lane group and batch of rows read from LDS
 constexpr int ROW_SBATCH = 2;  // samples per lane group and batch of rows streamed from HBM
-constexpr int ROW_MAXM = 4;    // feature positions per lane whose loads are issued together
+constexpr int ROW_MAXM = ROW_POSITIONS;  // feature positions per lane whose loads are issued together
 
 int solver_block_size(bool gram) { return gram ? BS_GRAM : BS_ROWS; }
 int max_per_thread(bool gram) { return gram ? MAXP_GRAM : MAXP_ROWS; }
