@@ -207,7 +207,9 @@ __device__ __forceinline__ void consider(Sel &s, double f, double a, int y, int 
 template <int BS, int PER, bool GRAM, bool VEC4>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   constexpr int NW = BS / 64;
-  constexpr int SB = ROW_BATCH;  // a sample's arithmetic does not depend on SB
+  // Samples per lane group and batch (a sample's arithmetic does not depend on them): scalar
+  // lanes hold a quarter of the registers per sample, so they take twice as many.
+  constexpr int SB = VEC4 ? ROW_BATCH : 2 * ROW_BATCH;
   // Row path, dynamic LDS: dot products against x_u and x_l [2][per_wg] (fp64), cache tags
   // [cap], then the rows of X this workgroup keeps resident [res][d] (16-byte aligned).
   extern __shared__ float4 dyn4[];
@@ -359,7 +361,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         // Streamed samples [res, cnt) go in batches of SBS per group; the first batch of each
         // group is loaded before the resident samples are computed, so its HBM latency
         // overlaps that work.
-        constexpr int SBS = ROW_SBATCH;
+        constexpr int SBS = VEC4 ? ROW_SBATCH : 2 * ROW_SBATCH;
         const int64_t sstride = (int64_t)ngroups * SBS;
         int64_t qs = res + (int64_t)grp * SBS;
         int nbs = 0;
