@@ -55,17 +55,23 @@ def dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3])
-def test_binary_full_size(cid):
+@pytest.mark.parametrize("cid,gram", [(1, svmx.GRAM_AUTO), (2, svmx.GRAM_AUTO), (3, svmx.GRAM_AUTO),
+                                      (1, svmx.GRAM_OFF), (2, svmx.GRAM_OFF), (3, svmx.GRAM_OFF)])
+def test_binary_full_size(cid, gram):
+    """The default path (the Gram fits at all three sizes) and the row path (rows of X resident
+    in LDS as far as they fit: part of each slice at 784 features, all of it at 128 and 32)."""
     R = ref(cid)
     wl = synth.workload(cid)
     X, y, Xt, _ = synth.generate(cid)
     nt = len(R["test_decisions"])
     assert digest(X, y, Xt[:nt]) == R["inputs_sha256"], "inputs differ from the stored reference"
     Xd, yd = dev(X), dev(y)
-    out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, trace_len=1000)
+    out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, trace_len=1000, gram=gram)
     assert out.status == svmx.SVM_OK
     st = out.stats
+    assert st["gram_used"] == (1 if gram == svmx.GRAM_AUTO else 0)
+    if gram == svmx.GRAM_OFF:
+        assert st["resident_rows"] > 0
     print(f"\nworkload {cid}: gpu {st['iterations']} steps W={st['dual_obj']:.9f} b={out.b:.6f}; "
           f"oracle {R['iterations']} steps W={R['dual_obj']:.9f} b={R['b']:.6f}")
 
