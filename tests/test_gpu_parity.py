@@ -464,3 +464,15 @@ def test_resident_rows_do_not_change_results():
         assert r.stats["iterations"] == runs[0].stats["iterations"]
         assert torch.equal(r.alpha, runs[0].alpha)
         assert r.b == runs[0].b
+
+
+def test_row_path_beyond_one_launch_is_enomem():
+    """A row-path problem needing more solver workgroups than the device holds at once (256 of
+    4,096 samples) is refused on the host before the cooperative launch, with SVM_ENOMEM."""
+    n, d = 1_100_000, 4
+    X = torch.rand(n, d, device="cuda")
+    y = torch.where(torch.arange(n, device="cuda") % 2 == 0, 1, -1).to(torch.int32)
+    with pytest.raises(svmx.SvmError) as e:
+        svmx.svm_train(X, y, 1.0, 0.5, 1e-3, gram=svmx.GRAM_OFF, max_iter=10)
+    assert e.value.status == svmx.SVM_ENOMEM
+    assert "do not fit" in str(e.value)
