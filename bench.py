@@ -403,6 +403,21 @@ def main():
                                   "kind": "oracle",
                                   "sample": f"first {r.iterations} SMO steps of the same {n}x{d} problem, fp64 oracle "
                                             f"with a 1 GiB LRU kernel-row cache, {tc:.1f} s"}
+        # the same oracle on one host thread: a bounded sample of the same problem (about a
+        # fifth of the time above), and the whole 1,000 x 16 training
+        k1 = int(max(10, rate / max(threads, 1) * args.cpu_seconds / 5))
+        t1 = time.perf_counter()
+        r1 = oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=k1, cache_bytes=1 << 30, threads=1)
+        t1c = time.perf_counter() - t1
+        w0 = synth.workload(0)
+        X0, y0, _, _ = synth.generate(0, m=1)
+        t1 = time.perf_counter()
+        r0 = oracle.train(X0, y0, w0.C, w0.gamma, w0.tol, threads=1)
+        t0c = time.perf_counter() - t1
+        result["cpu_baseline_single_thread"] = {
+            "value": r1.iterations / t1c, "unit": "SMO iterations/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {r1.iterations} SMO steps of the same {n}x{d} problem on one thread, {t1c:.1f} s",
+            "small_workload": {"workload": w0.name, "train_seconds": t0c, "smo_iterations": r0.iterations}}
     print(json.dumps(result), flush=True)
 
 
