@@ -18,8 +18,9 @@
 //   3. every workgroup reduces the same nwg records to the same pair (u, l), tests the stop
 //      rule, and solves the 2x2 sub-problem redundantly (identical fp64 arithmetic);
 //   4. every workgroup fetches K(u, j) and K(l, j) for its own samples -- from the Gram, or
-//      computed from X as a GEMV against x_u and x_l with the squared row norms -- and
-//      applies f_j += da_u y_u K_uj + da_l y_l K_lj.
+//      computed from X as a GEMV against x_u and x_l with the squared row norms, the first
+//      rows of its slice of X held in LDS for the whole launch -- and applies
+//      f_j += da_u y_u K_uj + da_l y_l K_lj.
 // Every wait is bounded by a wall-clock limit; on expiry the kernel records an error and
 // all waits end, so a launch always drains.
 #include "common.hpp"
@@ -32,8 +33,8 @@
 namespace svmx {
 
 // Gram path: 256-thread workgroups, up to 16 samples per thread.  Row path: 512-thread
-// workgroups (8 waves per CU, each with 2 samples x the lane's float4 loads in flight, keep
-// the streaming of X busy without spilling), up to 8 samples per thread.
+// workgroups, one per CU (8 waves, each with a batch of samples x the lane's loads in flight,
+// keep the streaming of X busy without spilling), up to 8 samples per thread.
 constexpr int BS_GRAM = 256, MAXP_GRAM = 16;
 constexpr int BS_ROWS = 512, MAXP_ROWS = 8;
 constexpr int ROW_BATCH = 2;   // samples per lane group and batch of rows read from LDS
