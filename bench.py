@@ -174,7 +174,10 @@ def main():
         "roofline": {"kernel": "smo_solve", "bound": "hbm", "achieved": solver_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": solver_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "bytes_per_step": step_bytes, "launch_avg_ms": 1e3 * t_kernel / launches,
-                     "us_per_smo_step": 1e6 * t_kernel / iters},
+                     "us_per_smo_step": 1e6 * t_kernel / iters,
+                     "note": "a step moves 25n algorithmic bytes but is bound by latency: the "
+                             "cross-workgroup exchange of the selections and the dependent read of "
+                             "the two Gram rows"},
         # the default Gram runs the fp32 contraction as three fp16 MFMA products per fp32 product
         # (split halves), so its own peak is the dense fp16 one; n^2 d is the fp32-equivalent count
         "gram_build": {"kernel": "gram_rbf_f16x3 (fp32 inputs split into fp16 halves)", "bound": "mfma",
