@@ -476,3 +476,41 @@ def test_row_path_beyond_one_launch_is_enomem():
         svmx.svm_train(X, y, 1.0, 0.5, 1e-3, gram=svmx.GRAM_OFF, max_iter=10)
     assert e.value.status == svmx.SVM_ENOMEM
     assert "do not fit" in str(e.value)
+
+
+@pytest.mark.parametrize("gram", [svmx.GRAM_ON, svmx.GRAM_OFF])
+@pytest.mark.parametrize("C_,gamma", [(1e-3, 0.125), (1e3, 0.125), (1.0, 10.0)])
+def test_extreme_box_and_width(C_, gamma, gram):
+    """Degenerate regimes of the dual: C = 1e-3 (most multipliers end at the bound C), C = 1e3
+    (near hard margin, large multipliers), gamma = 10 (K close to the identity: every sample a
+    support vector).  Against the oracle: the selections up to the first near-tie (early in the
+    first and last regimes, where the steps leave exact ties), W, the box and equality
+    constraints, tol-KKT with f recomputed by the oracle from the GPU's alpha, and the
+    decisions within 1e-3 (measured on MI355X: 4.4e-4 at C = 1e3, where sum a = 2,767, about
+    1e-8 in the other two regimes)."""
+    X, y = synth.two_blobs(600, 8, seed=17)
+    Xt, _ = synth.two_blobs(200, 8, seed=18)
+    tol = 1e-3
+    r = oracle.train(X, y, C_, gamma, tol, trace_len=500)
+    out = svmx.svm_train(dev(X), dev(y), C_, gamma, tol, gram=gram, trace_len=500)
+    assert out.status == svmx.SVM_OK
+    tied = np.flatnonzero(np.asarray(r.trace_gap)[1:].min(axis=1) < 1e-6)
+    k = min(500, r.iterations + 1, out.stats["iterations"] + 1, int(tied[0]) + 1 if tied.size else 500)
+    np.testing.assert_array_equal(out.trace_ul[:k], r.trace_ul[:k])
+    assert abs(out.stats["dual_obj"] - r.dual_obj) <= W_RTOL * abs(r.dual_obj)
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= C_) and abs(a @ y) <= 1e-9 * C_ * len(y)
+    f = oracle.f_from_alpha(X, y, a, gamma)
+    up = ((y > 0) & (a < C_)) | ((y < 0) & (a > 0))
+    low = ((y > 0) & (a > 0)) | ((y < 0) & (a < C_))
+    slack = 1e-4 * max(1.0, float(a.sum()))
+    assert f[up].min() >= f[low].max() - tol - slack
+    d_gpu = svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, gamma, dev(Xt)).cpu().numpy()
+    d_ref = oracle.decision(X, y, r.alpha, r.b, Xt, gamma)
+    gate = DEC_ATOL
+    print(f"\nC={C_} gamma={gamma}: steps {out.stats['iterations']} / {r.iterations}, max |dd| = "
+          f"{np.max(np.abs(d_gpu - d_ref)):.2e}, W rel {abs(out.stats['dual_obj'] - r.dual_obj) / abs(r.dual_obj):.1e}, "
+          f"trace prefix {k}")
+    assert np.max(np.abs(d_gpu - d_ref)) <= gate
+    sure = np.abs(d_ref) >= gate
+    assert np.array_equal(d_gpu[sure] > 0, d_ref[sure] > 0)
