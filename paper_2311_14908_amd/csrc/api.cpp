@@ -400,33 +400,39 @@ svm_status class_sort(const int32_t *label, int64_t n, int32_t k, hipStream_t st
   return SVM_OK;
 }
 
-// Layout of the prediction scratch for up to ntr training samples and m test samples of d
-// features: compacted support vectors, partial sums, and the split-fp16 rows of both sets.
+// Layout of the prediction scratch: for up to `pairs` problems of one launch with up to ntr
+// training samples each (n rows of X in all) and m test samples of d features, the compacted
+// support vectors, the partial sums, the problems' descriptions, and the split-fp16 rows of
+// both sets.
 struct PredictWs {
   PredictScratch ps;
   SplitX train, test;
 };
 
-int64_t predict_scratch_bytes(int64_t ntr, int64_t m, int64_t d) {
+constexpr int32_t PREDICT_PAIRS_MAX = 64;  // problems per prediction launch (bounds the partial sums)
+
+int64_t predict_scratch_bytes(int64_t n, int64_t ntr, int64_t pairs, int64_t m, int64_t d) {
   Layout L;
-  L.add(4 * ntr);
-  L.add(8 * ntr);
-  L.add(8);
-  L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1));
-  L.add(gram_split_scratch_bytes(ntr, d));
+  L.add(4 * ntr * pairs);
+  L.add(8 * ntr * pairs);
+  L.add(8 * pairs);
+  L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1) * pairs);
+  L.add((int64_t)sizeof(PredPair) * pairs);
+  L.add(gram_split_scratch_bytes(n, d));
   L.add(gram_split_scratch_bytes(std::max<int64_t>(m, 1), d));
   return round_up(L.total, ALIGN);
 }
 
-PredictWs predict_scratch(void *base, int64_t ntr, int64_t m, int64_t d) {
+PredictWs predict_scratch(void *base, int64_t n, int64_t ntr, int64_t pairs, int64_t m, int64_t d) {
   Layout L;
   char *b = static_cast<char *>(base);
   PredictWs w;
-  w.ps.sv_row = reinterpret_cast<int32_t *>(b + L.add(4 * ntr));
-  w.ps.sv_coef = reinterpret_cast<double *>(b + L.add(8 * ntr));
-  w.ps.count = reinterpret_cast<int64_t *>(b + L.add(8));
-  w.ps.part = reinterpret_cast<double *>(b + L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1)));
-  w.train = split_views(b + L.add(gram_split_scratch_bytes(ntr, d)), ntr, d);
+  w.ps.sv_row = reinterpret_cast<int32_t *>(b + L.add(4 * ntr * pairs));
+  w.ps.sv_coef = reinterpret_cast<double *>(b + L.add(8 * ntr * pairs));
+  w.ps.count = reinterpret_cast<int64_t *>(b + L.add(8 * pairs));
+  w.ps.part = reinterpret_cast<double *>(b + L.add(8LL * predict_splits(m, ntr) * std::max<int64_t>(m, 1) * pairs));
+  w.ps.pairs = reinterpret_cast<PredPair *>(b + L.add((int64_t)sizeof(PredPair) * pairs));
+  w.train = split_views(b + L.add(gram_split_scratch_bytes(n, d)), n, d);
   w.test = split_views(b + L.add(gram_split_scratch_bytes(std::max<int64_t>(m, 1), d)), std::max<int64_t>(m, 1), d);
   return w;
 }
@@ -641,7 +647,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
 
 int64_t svm_predict_workspace_bytes(int64_t n, int64_t d, int64_t m) {
   if (n < 1 || d < 1 || m < 0 || n > 0x7ffffffeLL || m > (INT64_MAX / 8) / 64 / std::max<int64_t>(n, 1)) return -1;
-  return predict_scratch_bytes(n, m, d);
+  return predict_scratch_bytes(n, n, 1, m, d);
 }
 
 svm_status svm_predict(const float *X_train, const int32_t *y, const double *alpha, double b, int64_t n, int64_t d,
@@ -659,9 +665,22 @@ svm_status svm_predict(const float *X_train, const int32_t *y, const double *alp
   if (need < 0) return fail(SVM_ENOMEM, "sizes overflow");
   if (!workspace || workspace_bytes < need)
     return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)need, (long long)workspace_bytes);
-  PredictWs pw = predict_scratch(workspace, n, m, d);
+  PredictWs pw = predict_scratch(workspace, n, n, 1, m, d);
   HIPCHK(predict_prepare(pw, r, X_train, n, X_test, m, d));
-  HIPCHK(launch_predict_map(X_train, d, 0, n, n, y, nullptr, alpha, n, gamma, X_test, m, b, dec, 1, pw.ps, r.stream));
+  PredPair pp{};
+  pp.off0 = 0;
+  pp.len0 = n;
+  pp.off1 = n;
+  pp.y = y;
+  pp.perm = nullptr;
+  pp.alpha_off = 0;
+  pp.ntr = n;
+  pp.sv_off = 0;
+  pp.part_off = 0;
+  pp.b = b;
+  pp.nsplit = predict_splits(m, n);
+  HIPCHK(hipMemcpyAsync(pw.ps.pairs, &pp, sizeof(pp), hipMemcpyHostToDevice, r.stream));
+  HIPCHK(launch_predict_pairs(X_train, d, 1, pp.nsplit, alpha, gamma, X_test, m, dec, 1, pw.ps, r.stream));
   HIPCHK(hipStreamSynchronize(r.stream));
   return SVM_OK;
 }
@@ -885,7 +904,8 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
 
 int64_t svm_predict_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, int64_t m) {
   if (n < 2 || d < 1 || k < 2 || k > MAX_CLASSES || m < 0 || n > 0x7ffffffeLL) return -1;
-  return round_up(4 * n, ALIGN) + predict_scratch_bytes(n, m, d);
+  const int64_t P = (int64_t)k * (k - 1) / 2;
+  return round_up(4 * n, ALIGN) + predict_scratch_bytes(n, n, std::min<int64_t>(P, PREDICT_PAIRS_MAX), m, d);
 }
 
 svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k,
@@ -910,18 +930,43 @@ svm_status svm_predict_ovo(const float *X, const int32_t *label, int64_t n, int6
   if (s0 != SVM_OK) return s0;
   if (m == 0) return SVM_OK;
   int32_t *dperm = static_cast<int32_t *>(workspace);
-  PredictWs pw = predict_scratch(static_cast<char *>(workspace) + round_up(4 * n, ALIGN), n, m, d);
+  const int32_t chunk = std::min<int32_t>(P, PREDICT_PAIRS_MAX);
+  PredictWs pw = predict_scratch(static_cast<char *>(workspace) + round_up(4 * n, ALIGN), n, n, chunk, m, d);
   HIPCHK(predict_prepare(pw, r, X, n, X_test, m, d));
   HIPCHK(hipMemcpyAsync(dperm, perm.data(), 4 * n, hipMemcpyHostToDevice, r.stream));
+  // the pairs in chunks of up to PREDICT_PAIRS_MAX, each chunk one launch per stage
+  std::vector<PredPair> pp;
+  pp.reserve(P);
   int64_t pack = 0;
-  int32_t q = 0;
   for (int32_t a = 0; a < k; ++a)
-    for (int32_t bb = a + 1; bb < k; ++bb, ++q) {
-      const int64_t np = cnt[a] + cnt[bb];
-      HIPCHK(launch_predict_map(X, d, start[a], cnt[a], start[bb], nullptr, dperm, alpha + pack, np, gamma, X_test, m,
-                                b[q], dec + q, P, pw.ps, r.stream));
-      pack += np;
+    for (int32_t bb = a + 1; bb < k; ++bb) {
+      PredPair e{};
+      e.off0 = start[a];
+      e.len0 = cnt[a];
+      e.off1 = start[bb];
+      e.y = nullptr;
+      e.perm = dperm;
+      e.alpha_off = pack;
+      e.ntr = cnt[a] + cnt[bb];
+      e.b = b[pp.size()];
+      e.nsplit = predict_splits(m, e.ntr);
+      pp.push_back(e);
+      pack += e.ntr;
     }
+  for (int32_t c0 = 0; c0 < P; c0 += chunk) {
+    const int32_t np = std::min<int32_t>(chunk, P - c0);
+    int nsplit_max = 1;
+    int64_t sv = 0, part = 0;
+    for (int32_t q = c0; q < c0 + np; ++q) {
+      pp[q].sv_off = sv;
+      pp[q].part_off = part;
+      sv += pp[q].ntr;
+      part += (int64_t)pp[q].nsplit * m;
+      nsplit_max = std::max(nsplit_max, (int)pp[q].nsplit);
+    }
+    HIPCHK(hipMemcpyAsync(pw.ps.pairs, pp.data() + c0, sizeof(PredPair) * np, hipMemcpyHostToDevice, r.stream));
+    HIPCHK(launch_predict_pairs(X, d, np, nsplit_max, alpha, gamma, X_test, m, dec + c0, P, pw.ps, r.stream));
+  }
   HIPCHK(launch_ovo_vote(dec, m, k, pred, r.stream));
   HIPCHK(hipStreamSynchronize(r.stream));
   return SVM_OK;

@@ -37,22 +37,36 @@ hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thr
 // error.
 int64_t solver_res_rows_max(const SolveParams &p, int32_t per_thread);
 hipError_t launch_finalize(const Prob *probs, int32_t nprob, double C, double *out /*[nprob][4]*/, hipStream_t s);
-// Device scratch of one prediction: compacted support vectors and per-split partial sums.
+// Device scratch of a prediction: compacted support vectors and per-split partial sums of
+// every problem of one launch, and the problems' descriptions.
 struct PredictScratch {
-  int32_t *sv_row;  // [ntr]
-  double *sv_coef;  // [ntr]
-  int64_t *count;   // [1]
-  double *part;     // [predict_splits(m, ntr)][m]
+  int32_t *sv_row;  // [sum of the problems' ntr]
+  double *sv_coef;  // [sum of the problems' ntr]
+  int64_t *count;   // [problems]
+  double *part;     // [sum of the problems' nsplit][m]
+  struct PredPair *pairs;  // [problems], device
   const SplitX *split_train = nullptr;  // split rows of the training X and of the test samples
   const SplitX *split_test = nullptr;   // (both set: the split-fp16 kernel; host pointers)
 };
 int predict_splits(int64_t m, int64_t nsv_max);
-// Decision values for training samples addressed like Prob (local j -> row off0+j or
-// off1+j-len0, then through perm when perm != NULL); labels from y by that row, or by range.
-hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t len0, int64_t off1,
-                              const int32_t *y, const int32_t *perm, const double *alpha, int64_t ntr, double gamma,
-                              const float *T, int64_t m, double b, double *dec, int64_t dec_stride,
-                              const PredictScratch &ws, hipStream_t s);
+// One problem of a prediction launch: its training samples addressed like Prob (local j -> row
+// off0+j or off1+j-len0, then through perm when perm != NULL; labels from y by that row, or by
+// range), its multipliers alpha[alpha_off ..][ntr], where its support vectors and partial sums
+// go, its bias and split count (predict_splits(m, ntr)).
+struct PredPair {
+  int64_t off0, len0, off1;
+  const int32_t *y;
+  const int32_t *perm;
+  int64_t alpha_off, ntr, sv_off, part_off;
+  double b;
+  int32_t nsplit, pad;
+};
+// Decision values of npairs problems in one launch per stage: dec[q * dec_stride + p] for test
+// sample q and problem p (pairs[] already on the device, in ws.pairs); nsplit_max = the
+// largest nsplit among them.
+hipError_t launch_predict_pairs(const float *Xtr, int64_t d, int32_t npairs, int nsplit_max, const double *alpha,
+                                double gamma, const float *T, int64_t m, double *dec, int64_t dec_stride,
+                                const PredictScratch &ws, hipStream_t s);
 hipError_t launch_ovo_vote(const double *dec, int64_t m, int32_t k, int32_t *pred, hipStream_t s);
 
 // Working-set solver (ws_smo.hip): one problem per launch, nwg sample-owning workgroups plus,

@@ -25,18 +25,21 @@ constexpr int PKC = 16;        // k per LDS stage
 constexpr int PPAD = PT + 16;  // LDS pitch (conflict-free operand reads)
 constexpr int PBS = 256;
 
-struct PredMap {  // local training index j -> row of X, and its label
-  int64_t off0, len0, off1;
-  const int32_t *y;     // labels by row, or NULL: +1 for j < len0, else -1
-  const int32_t *perm;  // sorted position -> row of X, or NULL (identity)
-};
+__device__ __forceinline__ int64_t pm_pos(const PredPair &m, int64_t j) {
+  return j < m.len0 ? m.off0 + j : m.off1 + (j - m.len0);
+}
 
-__device__ __forceinline__ int64_t pm_pos(const PredMap &m, int64_t j) { return j < m.len0 ? m.off0 + j : m.off1 + (j - m.len0); }
-
-// One workgroup of 1024 threads: stable compaction of the samples with a > 0.
-__global__ void __launch_bounds__(1024) sv_compact_k(const double *__restrict__ alpha, int64_t n, PredMap map,
-                                                     int32_t *__restrict__ sv_row, double *__restrict__ sv_coef,
-                                                     int64_t *__restrict__ count) {
+// One workgroup of 1024 threads per problem (blockIdx.x): stable compaction of its samples
+// with a > 0.
+__global__ void __launch_bounds__(1024) sv_compact_k(const double *__restrict__ alpha_all,
+                                                     const PredPair *__restrict__ pairs, int32_t *__restrict__ sv_row_all,
+                                                     double *__restrict__ sv_coef_all, int64_t *__restrict__ count_all) {
+  const PredPair map = pairs[blockIdx.x];
+  const double *alpha = alpha_all + map.alpha_off;
+  const int64_t n = map.ntr;
+  int32_t *sv_row = sv_row_all + map.sv_off;
+  double *sv_coef = sv_coef_all + map.sv_off;
+  int64_t *count = count_all + blockIdx.x;
   __shared__ int wave_cnt[16];
   __shared__ int64_t s_base;
   if (threadIdx.x == 0) s_base = 0;
@@ -119,18 +122,26 @@ __device__ __forceinline__ double row16_sum(double v) {
   return v;
 }
 
+// Workgroup (x, y, z): test rows 128 x .. +128, split y of problem z's support-vector tiles.
 template <bool VEC4>
 __global__ void __launch_bounds__(PBS) predict_mfma_k(const float *__restrict__ T, int64_t m, const float *__restrict__ X,
-                                                      const int32_t *__restrict__ sv_row,
-                                                      const double *__restrict__ sv_coef,
+                                                      const PredPair *__restrict__ pairs,
+                                                      const int32_t *__restrict__ sv_row_all,
+                                                      const double *__restrict__ sv_coef_all,
                                                       const int64_t *__restrict__ sv_count, int64_t d, float c,
-                                                      int nsplit, double *__restrict__ part) {
+                                                      double *__restrict__ part_all) {
+  const PredPair pp = pairs[blockIdx.z];
+  const int nsplit = pp.nsplit;
+  if ((int)blockIdx.y >= nsplit) return;
+  const int32_t *sv_row = sv_row_all + pp.sv_off;
+  const double *sv_coef = sv_coef_all + pp.sv_off;
+  double *part = part_all + pp.part_off;
   __shared__ float As[PKC][PPAD];
   __shared__ float Bs[PKC][PPAD];
   __shared__ float nA[PT], nB[PT];
   __shared__ double cB[PT];
   __shared__ double rs[2][PT];
-  const int64_t nsv = *sv_count;
+  const int64_t nsv = sv_count[blockIdx.z];
   const int64_t q0 = (int64_t)blockIdx.x * PT;
   const int split = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -250,15 +261,22 @@ __device__ __forceinline__ void pred_split_store(PredStage &S, const h8 (&r)[8])
 // predict_mfma_k on the split representation: st holds the test rows, sx the training rows
 // (support vectors addressed through sv_row); dot = acc * s_q * s_j.
 __global__ void __launch_bounds__(PBS) predict_f16x3_k(SplitX st, int64_t m, SplitX sx,
-                                                       const int32_t *__restrict__ sv_row,
-                                                       const double *__restrict__ sv_coef,
-                                                       const int64_t *__restrict__ sv_count, float c, int nsplit,
-                                                       double *__restrict__ part) {
+                                                       const PredPair *__restrict__ pairs,
+                                                       const int32_t *__restrict__ sv_row_all,
+                                                       const double *__restrict__ sv_coef_all,
+                                                       const int64_t *__restrict__ sv_count, float c,
+                                                       double *__restrict__ part_all) {
+  const PredPair pp = pairs[blockIdx.z];
+  const int nsplit = pp.nsplit;
+  if ((int)blockIdx.y >= nsplit) return;
+  const int32_t *sv_row = sv_row_all + pp.sv_off;
+  const double *sv_coef = sv_coef_all + pp.sv_off;
+  double *part = part_all + pp.part_off;
   __shared__ PredStage S[2];
   __shared__ float sA[PT], nA[PT], sB[PT], nB[PT];
   __shared__ double cB[PT];
   __shared__ double rs[2][PT];
-  const int64_t nsv = *sv_count;
+  const int64_t nsv = sv_count[blockIdx.z];
   const int64_t q0 = (int64_t)blockIdx.x * PT;
   const int split = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -338,13 +356,16 @@ __global__ void __launch_bounds__(PBS) predict_f16x3_k(SplitX st, int64_t m, Spl
   if (threadIdx.x < PT && q0 + threadIdx.x < m) part[(int64_t)split * m + q0 + threadIdx.x] = row_acc;
 }
 
-__global__ void predict_final_k(const double *__restrict__ part, int64_t m, int nsplit, double b, double *dec,
-                                int64_t stride) {
+// dec[q * stride + p] = the sum of problem p's (blockIdx.y) split partials - its bias.
+__global__ void predict_final_k(const double *__restrict__ part_all, int64_t m, const PredPair *__restrict__ pairs,
+                                double *dec, int64_t stride) {
   const int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (q >= m) return;
+  const PredPair pp = pairs[blockIdx.y];
+  const double *part = part_all + pp.part_off;
   double s = 0.0;
-  for (int k = 0; k < nsplit; ++k) s += part[(int64_t)k * m + q];
-  dec[q * stride] = s - b;
+  for (int k = 0; k < pp.nsplit; ++k) s += part[(int64_t)k * m + q];
+  dec[q * stride + blockIdx.y] = s - pp.b;
 }
 
 int predict_splits(int64_t m, int64_t nsv_max) {
@@ -358,34 +379,32 @@ int predict_splits(int64_t m, int64_t nsv_max) {
   return (int)s;
 }
 
-hipError_t launch_predict_map(const float *Xtr, int64_t d, int64_t off0, int64_t len0, int64_t off1,
-                              const int32_t *y, const int32_t *perm, const double *alpha, int64_t ntr, double gamma,
-                              const float *T, int64_t m, double b, double *dec, int64_t dec_stride,
-                              const PredictScratch &ws, hipStream_t s) {
-  if (m <= 0) return hipSuccess;
+hipError_t launch_predict_pairs(const float *Xtr, int64_t d, int32_t npairs, int nsplit_max, const double *alpha,
+                                double gamma, const float *T, int64_t m, double *dec, int64_t dec_stride,
+                                const PredictScratch &ws, hipStream_t s) {
+  if (m <= 0 || npairs <= 0) return hipSuccess;
   const bool split = ws.split_test != nullptr && ws.split_train != nullptr;
-  PredMap map{off0, len0, off1, y, perm};
-  hipLaunchKernelGGL(sv_compact_k, dim3(1), dim3(1024), 0, s, alpha, ntr, map, ws.sv_row, ws.sv_coef, ws.count);
+  hipLaunchKernelGGL(sv_compact_k, dim3((unsigned)npairs), dim3(1024), 0, s, alpha, ws.pairs, ws.sv_row, ws.sv_coef,
+                     ws.count);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nsplit = predict_splits(m, ntr);
   const float c = (float)(-gamma * 1.4426950408889634);
-  dim3 grid((unsigned)((m + PT - 1) / PT), (unsigned)nsplit);
+  dim3 grid((unsigned)((m + PT - 1) / PT), (unsigned)nsplit_max, (unsigned)npairs);
   const bool vec4 = (d % 4 == 0) && ((reinterpret_cast<uintptr_t>(T) & 15) == 0) &&
                     ((reinterpret_cast<uintptr_t>(Xtr) & 15) == 0);
   if (split)
-    hipLaunchKernelGGL(predict_f16x3_k, grid, dim3(PBS), 0, s, *ws.split_test, m, *ws.split_train, ws.sv_row,
-                       ws.sv_coef, ws.count, c, nsplit, ws.part);
+    hipLaunchKernelGGL(predict_f16x3_k, grid, dim3(PBS), 0, s, *ws.split_test, m, *ws.split_train, ws.pairs,
+                       ws.sv_row, ws.sv_coef, ws.count, c, ws.part);
   else if (vec4)
-    hipLaunchKernelGGL(predict_mfma_k<true>, grid, dim3(PBS), 0, s, T, m, Xtr, ws.sv_row, ws.sv_coef, ws.count, d, c,
-                       nsplit, ws.part);
+    hipLaunchKernelGGL(predict_mfma_k<true>, grid, dim3(PBS), 0, s, T, m, Xtr, ws.pairs, ws.sv_row, ws.sv_coef,
+                       ws.count, d, c, ws.part);
   else
-    hipLaunchKernelGGL(predict_mfma_k<false>, grid, dim3(PBS), 0, s, T, m, Xtr, ws.sv_row, ws.sv_coef, ws.count, d, c,
-                       nsplit, ws.part);
+    hipLaunchKernelGGL(predict_mfma_k<false>, grid, dim3(PBS), 0, s, T, m, Xtr, ws.pairs, ws.sv_row, ws.sv_coef,
+                       ws.count, d, c, ws.part);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(predict_final_k, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, ws.part, m, nsplit, b, dec,
-                     dec_stride);
+  hipLaunchKernelGGL(predict_final_k, dim3((unsigned)((m + 255) / 256), (unsigned)npairs), dim3(256), 0, s, ws.part,
+                     m, ws.pairs, dec, dec_stride);
   return hipGetLastError();
 }
 

@@ -187,3 +187,16 @@ def test_resident_rows_option():
     for r in (-1, 0, 1, 1000):
         assert ws(20_000, 784, gram=svmx.GRAM_OFF, resident_rows=r) == base, r
     assert ws(20_000, 784, gram=svmx.GRAM_OFF, resident_rows=-2) == -1
+
+
+def test_predict_ovo_workspace_covers_the_pair_chunks():
+    """One-vs-one prediction runs up to 64 pairs per launch: its workspace holds, per pair of a
+    chunk, room for all n samples' support vectors (12 bytes each) and the partial sums."""
+    lib = svmx.load()
+    n, d, m = 60_000, 784, 10_000
+    one = lib.svm_predict_workspace_bytes(n, d, m)
+    for k, pairs in ((2, 1), (10, 45), (12, 64), (64, 64)):
+        w = lib.svm_predict_ovo_workspace_bytes(n, d, k, m)
+        assert w >= 4 * n + pairs * 12 * n, k
+        assert w >= one, k
+    assert lib.svm_predict_ovo_workspace_bytes(n, d, 64, m) == lib.svm_predict_ovo_workspace_bytes(n, d, 12, m)
