@@ -530,8 +530,41 @@ static bool row_vec4(const SolveParams &p) {
 }
 
 template <int BS, int PER, bool GRAM, bool VEC4>
-static hipError_t launch_one(const SolveParams &p, int32_t total_wg, size_t shmem, hipStream_t s, int32_t *maxres) {
-  const void *fn = reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4>);
+static const void *kernel_of() {
+  return reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4>);
+}
+
+// The solver variant for a path, samples per thread and (row path) float4 lanes; NULL if none.
+static const void *solver_kernel(bool gram, int32_t per_thread, bool vec4) {
+  if (gram) {
+    switch (per_thread) {
+      case 1: return kernel_of<BS_GRAM, 1, true, false>();
+      case 2: return kernel_of<BS_GRAM, 2, true, false>();
+      case 4: return kernel_of<BS_GRAM, 4, true, false>();
+      case 8: return kernel_of<BS_GRAM, 8, true, false>();
+      case 16: return kernel_of<BS_GRAM, 16, true, false>();
+      default: return nullptr;
+    }
+  }
+  switch (per_thread * 2 + (vec4 ? 1 : 0)) {
+    case 2: return kernel_of<BS_ROWS, 1, false, false>();
+    case 3: return kernel_of<BS_ROWS, 1, false, true>();
+    case 4: return kernel_of<BS_ROWS, 2, false, false>();
+    case 5: return kernel_of<BS_ROWS, 2, false, true>();
+    case 8: return kernel_of<BS_ROWS, 4, false, false>();
+    case 9: return kernel_of<BS_ROWS, 4, false, true>();
+    case 16: return kernel_of<BS_ROWS, 8, false, false>();
+    case 17: return kernel_of<BS_ROWS, 8, false, true>();
+    default: return nullptr;
+  }
+}
+
+hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
+                         int32_t *max_coresident) {
+  const void *fn = solver_kernel(gram, per_thread, !gram && row_vec4(p));
+  if (!fn) return hipErrorInvalidValue;
+  const int bs = gram ? BS_GRAM : BS_ROWS;
+  const size_t shmem = gram ? 0 : row_path_lds(p, p.res_rows);
   if (shmem > 48 * 1024) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return e;
@@ -541,60 +574,22 @@ static hipError_t launch_one(const SolveParams &p, int32_t total_wg, size_t shme
   if (e != hipSuccess) return e;
   e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, BS, shmem);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, bs, shmem);
   if (e != hipSuccess) return e;
-  if (maxres) *maxres = per_cu * cus;
+  if (max_coresident) *max_coresident = per_cu * cus;
   if (total_wg <= 0) return hipSuccess;  // capacity query only
   if ((int64_t)total_wg > (int64_t)per_cu * cus) return hipErrorCooperativeLaunchTooLarge;
   SolveParams pp = p;
   void *args[] = {&pp};
-  return hipLaunchCooperativeKernel(fn, dim3((unsigned)total_wg), dim3(BS), args, (unsigned)shmem, s);
-}
-
-hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
-                         int32_t *max_coresident) {
-  if (gram) {
-    switch (per_thread) {
-      case 1: return launch_one<BS_GRAM, 1, true, false>(p, total_wg, 0, s, max_coresident);
-      case 2: return launch_one<BS_GRAM, 2, true, false>(p, total_wg, 0, s, max_coresident);
-      case 4: return launch_one<BS_GRAM, 4, true, false>(p, total_wg, 0, s, max_coresident);
-      case 8: return launch_one<BS_GRAM, 8, true, false>(p, total_wg, 0, s, max_coresident);
-      case 16: return launch_one<BS_GRAM, 16, true, false>(p, total_wg, 0, s, max_coresident);
-      default: return hipErrorInvalidValue;
-    }
-  }
-  const size_t shmem = row_path_lds(p, p.res_rows);
-  const bool vec4 = row_vec4(p);
-  switch (per_thread * 2 + (vec4 ? 1 : 0)) {
-    case 2: return launch_one<BS_ROWS, 1, false, false>(p, total_wg, shmem, s, max_coresident);
-    case 3: return launch_one<BS_ROWS, 1, false, true>(p, total_wg, shmem, s, max_coresident);
-    case 4: return launch_one<BS_ROWS, 2, false, false>(p, total_wg, shmem, s, max_coresident);
-    case 5: return launch_one<BS_ROWS, 2, false, true>(p, total_wg, shmem, s, max_coresident);
-    case 8: return launch_one<BS_ROWS, 4, false, false>(p, total_wg, shmem, s, max_coresident);
-    case 9: return launch_one<BS_ROWS, 4, false, true>(p, total_wg, shmem, s, max_coresident);
-    case 16: return launch_one<BS_ROWS, 8, false, false>(p, total_wg, shmem, s, max_coresident);
-    case 17: return launch_one<BS_ROWS, 8, false, true>(p, total_wg, shmem, s, max_coresident);
-    default: return hipErrorInvalidValue;
-  }
+  return hipLaunchCooperativeKernel(fn, dim3((unsigned)total_wg), dim3(bs), args, (unsigned)shmem, s);
 }
 
 int64_t solver_res_rows_max(const SolveParams &p, int32_t per_thread) {
   int dev = 0, max_lds = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return -1;
-  const bool vec4 = row_vec4(p);
-  const void *fn = nullptr;
-  switch (per_thread * 2 + (vec4 ? 1 : 0)) {
-    case 2: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 1, false, false>); break;
-    case 3: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 1, false, true>); break;
-    case 4: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 2, false, false>); break;
-    case 5: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 2, false, true>); break;
-    case 8: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 4, false, false>); break;
-    case 9: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 4, false, true>); break;
-    case 16: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 8, false, false>); break;
-    case 17: fn = reinterpret_cast<const void *>(&smo_solve<BS_ROWS, 8, false, true>); break;
-    default: return -1;
-  }
+  const void *fn = solver_kernel(false, per_thread, row_vec4(p));
+  if (!fn) return -1;
   hipFuncAttributes attr;
   if (hipFuncGetAttributes(&attr, fn) != hipSuccess) return -1;
   const int64_t avail = (int64_t)max_lds - (int64_t)attr.sharedSizeBytes - (int64_t)row_path_lds(p, 0);
