@@ -138,7 +138,8 @@ int64_t svm_train_workspace_bytes(int64_t n, int64_t d, const svm_options *o);
  *   workspace/workspace_bytes          device scratch of at least svm_train_workspace_bytes
  *   o      options or NULL;  st  host stats out or NULL
  * EINVAL: n<2, d<1, non-finite or non-positive C/gamma/tol, NULL pointers, a label not in
- * {+1,-1} or only one class present.
+ * {+1,-1} or only one class present, a value of X that is not finite (checked on the device
+ * before any other work).
  */
 svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma, double tol,
                      double *alpha, double *b, void *workspace, int64_t workspace_bytes, const svm_options *o,
@@ -168,6 +169,8 @@ int64_t svm_train_ovo_workspace_bytes(int64_t n, int64_t d, int32_t k, const svm
  *   alpha  device fp64 [(k-1)*n] out: the pairs' multipliers packed in pair order, each pair
  *          in its local sample order (pair p occupies n_a + n_b entries)
  *   b      host double [P] out;  st  host svm_stats [P] out or NULL
+ * EINVAL as for svm_train (a label outside 0..k-1, a class without samples and a value of X
+ * that is not finite included).
  */
 svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_t d, int32_t k, double C,
                          double gamma, double tol, double *alpha, double *b, void *workspace,

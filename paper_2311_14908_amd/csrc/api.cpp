@@ -320,6 +320,17 @@ svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t p
                       sp.error, nprob, total_wg, d_ctl, stream, launches, h, t_kernel);
 }
 
+// EINVAL unless every value of X[0 .. count) is finite (a NaN or an infinity would leave no
+// stop test true, and the solver would run to max_iter).  flag: a cleared device word.
+svm_status check_finite(const float *X, int64_t count, int32_t *flag, hipStream_t stream) {
+  HIPCHK(launch_check_finite(X, count, flag, stream));
+  int32_t bad = 0;
+  HIPCHK(hipMemcpyAsync(&bad, flag, sizeof(bad), hipMemcpyDeviceToHost, stream));
+  HIPCHK(hipStreamSynchronize(stream));
+  if (bad) return fail(SVM_EINVAL, "X holds a value that is not finite");
+  return SVM_OK;
+}
+
 svm_status check_labels_pm1(const int32_t *y, int64_t n, hipStream_t stream) {
   std::vector<int32_t> h(n);
   HIPCHK(hipMemcpyAsync(h.data(), y, 4 * n, hipMemcpyDeviceToHost, stream));
@@ -530,6 +541,8 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   HIPCHK(hipMemcpyAsync(dprob, &hp, sizeof(Prob), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemsetAsync(err, 0, 16, stream));
+  s0 = check_finite(X, n * d, err + 2, stream);
+  if (s0 != SVM_OK) return s0;
   if (p.cache_cap)
     HIPCHK(hipMemsetAsync(ws + p.off_tags, 0xff, 4LL * p.cache_cap * p.shape.nwg, stream));
 
@@ -815,6 +828,8 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   HIPCHK(hipMemcpyAsync(dprob, hp.data(), sizeof(Prob) * hp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemsetAsync(err, 0, 16, stream));
+  s0 = check_finite(X, n * d, err + 2, stream);
+  if (s0 != SVM_OK) return s0;
   HIPCHK(launch_gather_rows(X, d, dperm, n, Xs, stream));
 
   Timer tg, ts, tf;

@@ -27,6 +27,8 @@ int64_t gram_split_scratch_bytes(int64_t n, int64_t d);
 hipError_t launch_gram_split(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, void *scratch,
                              hipStream_t st);
 hipError_t launch_row_norms(const float *X, int64_t n, int64_t d, double *sqn, hipStream_t s);
+// flag[0] = 1 when a value of X[0 .. count) is not finite (flag left as it is otherwise).
+hipError_t launch_check_finite(const float *X, int64_t count, int32_t *flag, hipStream_t s);
 hipError_t launch_gather_rows(const float *X, int64_t d, const int32_t *perm, int64_t n, float *Xs, hipStream_t s);
 hipError_t launch_solver_init(const Prob *probs, int32_t nprob, int64_t max_n, hipStream_t s);
 // total_wg <= 0 only reports in *max_coresident how many workgroups of the variant fit at once.

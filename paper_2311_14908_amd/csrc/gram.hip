@@ -213,6 +213,23 @@ __global__ void __launch_bounds__(256) kernel_rows_k(const float *__restrict__ X
   }
 }
 
+// flag[0] = 1 if any of the count values at X is not finite (a plain store: every writer
+// stores the same value, so no atomic is needed).
+__global__ void __launch_bounds__(256) nonfinite_k(const float *__restrict__ X, int64_t count, int32_t *flag) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  bool bad = false;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) bad |= !__builtin_isfinite(X[i]);
+  if (bad) *flag = 1;
+}
+
+hipError_t launch_check_finite(const float *X, int64_t count, int32_t *flag, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  int64_t blocks = (count + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(nonfinite_k, dim3((unsigned)blocks), dim3(256), 0, s, X, count, flag);
+  return hipGetLastError();
+}
+
 // sqn[j] = |x_j|^2, one group of lanes per row (the routine kernel_rows_k uses).
 template <bool VEC4>
 __global__ void __launch_bounds__(256) row_norms_k(const float *__restrict__ X, int64_t n, int64_t d,

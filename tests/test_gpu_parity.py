@@ -514,3 +514,19 @@ def test_extreme_box_and_width(C_, gamma, gram):
     assert np.max(np.abs(d_gpu - d_ref)) <= gate
     sure = np.abs(d_ref) >= gate
     assert np.array_equal(d_gpu[sure] > 0, d_ref[sure] > 0)
+
+
+@pytest.mark.parametrize("bad", [float("nan"), float("inf"), -float("inf")])
+def test_non_finite_x_is_rejected(bad):
+    """A NaN or an infinity in X would keep every stop test false until max_iter; training
+    refuses it up front with SVM_EINVAL (binary, either path, and one-vs-one)."""
+    X, y = synth.two_blobs(300, 6, seed=2)
+    X[123, 4] = bad
+    for gram in (svmx.GRAM_ON, svmx.GRAM_OFF):
+        with pytest.raises(svmx.SvmError) as e:
+            svmx.svm_train(dev(X), dev(y), 1.0, 0.5, 1e-3, gram=gram)
+        assert e.value.status == svmx.SVM_EINVAL and "not finite" in str(e.value)
+    lab = (y > 0).astype(np.int32)
+    with pytest.raises(svmx.SvmError) as e:
+        svmx.svm_train_ovo(dev(X), dev(lab), 2, 1.0, 0.5, 1e-3)
+    assert e.value.status == svmx.SVM_EINVAL and "not finite" in str(e.value)
