@@ -146,3 +146,40 @@ def test_ovo_row_path_full_size_pairs_equal_binary():
         r = svmx.svm_train(dev(X[idx]), dev(y), wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=steps)
         assert out.stats[p]["iterations"] == r.stats["iterations"]
         assert torch.equal(out.alpha[offs[p]:offs[p] + sizes[p]], r.alpha), f"pair {p}"
+
+
+@pytest.mark.parametrize("cid,q,gram", [(1, 128, svmx.GRAM_AUTO), (1, 128, svmx.GRAM_OFF), (2, 32, svmx.GRAM_AUTO),
+                                        (3, 32, svmx.GRAM_AUTO)])
+def test_working_set_full_size(cid, q, gram):
+    """The working-set solver at the full sizes reaches the optimum of the stored oracle
+    solve (its trajectory differs from the pair steps', so the gates are those of the optimum):
+    W within 1e-4, the stored test decisions within 1e-3 with their labels, the box and
+    equality constraints, and tol-KKT on 128 rows whose f the oracle recomputes."""
+    R = ref(cid)
+    wl = synth.workload(cid)
+    X, y, Xt, _ = synth.generate(cid)
+    nt = len(R["test_decisions"])
+    assert digest(X, y, Xt[:nt]) == R["inputs_sha256"], "inputs differ from the stored reference"
+    Xd, yd = dev(X), dev(y)
+    out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, working_set=q, gram=gram)
+    assert out.status == svmx.SVM_OK
+    st = out.stats
+    print(f"\nworkload {cid}, q={q}, gram_used={st['gram_used']}: {st['rounds']} rounds, {st['iterations']} pair "
+          f"steps, W={st['dual_obj']:.9f} (oracle {R['dual_obj']:.9f})")
+    assert abs(st["dual_obj"] - R["dual_obj"]) <= 1e-4 * abs(R["dual_obj"])
+    d_gpu = svmx.svm_predict(Xd, yd, out.alpha, out.b, wl.gamma, dev(Xt[:nt])).cpu().numpy()
+    d_ref = np.array(R["test_decisions"])
+    assert np.max(np.abs(d_gpu - d_ref)) <= 1e-3
+    sure = np.abs(d_ref) >= 1e-3
+    assert np.array_equal(d_gpu[sure] > 0, d_ref[sure] > 0)
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= wl.C)
+    assert abs(float(a @ y)) <= 1e-9 * wl.C * len(y)
+    rows = np.random.default_rng(100 + cid).choice(len(y), 128, replace=False)
+    f = oracle.f_from_alpha(X, y, a, wl.gamma, rows=rows)
+    ar, yr = a[rows], y[rows]
+    up = ((yr > 0) & (ar < wl.C)) | ((yr < 0) & (ar > 0))
+    low = ((yr > 0) & (ar > 0)) | ((yr < 0) & (ar < wl.C))
+    slack = 1e-4
+    assert np.all(f[up] >= out.b - wl.tol / 2 - slack)
+    assert np.all(f[low] <= out.b + wl.tol / 2 + slack)
