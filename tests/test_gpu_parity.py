@@ -424,13 +424,15 @@ def test_ovo_predict_matches_oracle_given_alpha():
 
 
 @pytest.mark.parametrize("n,d,res", [(3000, 784, 0), (3000, 784, -1), (3000, 784, 7), (2000, 16, 0), (2000, 100, 0),
-                                     (2000, 301, 0), (1500, 1500, 0), (1500, 1500, 3)])
+                                     (2000, 301, 0), (1500, 1500, 0), (1500, 1500, 3), (700, 4100, 0),
+                                     (700, 4100, -1), (600, 3001, 0)])
 def test_row_path_step_uses_the_kernel_row_values(n, d, res):
     """After one row-path step f equals -y + (c_u K(u, .) + c_l K(l, .)) evaluated on the host from
     svm_kernel_rows' fp32 values, bit for bit, at every sample: the solver's row values are the
     entry point's whether its rows of X sit in LDS (all of them, some, or none) or stream from
-    HBM, for lane groups of 64 (784 features), 32 (100) and 4 (16), scalar lanes (301) and rows
-    longer than one register block (301, 1500)."""
+    HBM, for lane groups of 64 (784 features), 32 (100) and 4 (16), scalar lanes (301, 3001) and
+    rows longer than one register block (301, 1500, and 4100 and 3001 with 7 and 11 later
+    blocks)."""
     X, y = synth.two_blobs(n, d, seed=d + 1)
     Xd, yd = dev(X), dev(y)
     gamma = 1.0 / d
