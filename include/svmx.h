@@ -30,7 +30,11 @@
  *    leaks; svm_last_error() explains.  SVM_NOT_CONVERGED (positive) means the iteration
  *    limit was reached: alpha is feasible (0 <= a <= C, sum a y = 0) and b is the current
  *    midpoint.
- *  - Calls on one device that overlap in time must use distinct workspaces.
+ *  - Calls on one device that overlap in time must use distinct workspaces.  Training calls
+ *    (svm_train, svm_train_ovo) should not overlap in time on one device: each solver launch
+ *    expects all of its workgroups to run at once, and one that has to wait longer than the
+ *    device-side wait limit (2 s) for workgroups held back by another call's launch ends with
+ *    SVM_EDEVICE.
  */
 #ifndef SVMX_H
 #define SVMX_H
