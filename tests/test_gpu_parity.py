@@ -423,6 +423,25 @@ def test_ovo_predict_matches_oracle_given_alpha():
     assert np.array_equal(pred.cpu().numpy()[sure], pred_ref[sure])
 
 
+@pytest.mark.parametrize("k", [5, 12])
+@pytest.mark.parametrize("mfma", [svmx.MFMA_SPLIT_F16, svmx.MFMA_F32])
+def test_ovo_predict_pairs_equal_binary_predict(k, mfma):
+    """One-vs-one prediction runs the pairs together (up to 64 per launch; 12 classes give 66
+    pairs, so two launches of each stage), but every pair keeps its own support vectors, split
+    count and summation order: its decision values are those of svm_predict on that pair's
+    samples alone, bit for bit."""
+    X, lab, Xt, _ = synth.generate(4, n=60 * k, m=300, d=20, classes=k)
+    out = svmx.svm_train_ovo(dev(X), dev(lab), k, 10.0, 0.05, 1e-3)
+    assert out.status == svmx.SVM_OK
+    dec, _ = svmx.svm_predict_ovo(dev(X), dev(lab), k, out.alpha, out.b, 0.05, dev(Xt), gram_mfma=mfma)
+    offs, sizes = svmx.ovo_offsets(lab, k)
+    for p, (a, b) in enumerate(oracle.ovo_pairs(k)):
+        idx, y = oracle.ovo_local(lab, a, b)
+        d1 = svmx.svm_predict(dev(X[idx]), dev(y), out.alpha[offs[p]:offs[p] + sizes[p]].contiguous(), float(out.b[p]),
+                              0.05, dev(Xt), gram_mfma=mfma)
+        assert torch.equal(dec[:, p].contiguous(), d1), f"pair {p} ({a}, {b})"
+
+
 @pytest.mark.parametrize("n,d,res", [(3000, 784, 0), (3000, 784, -1), (3000, 784, 7), (2000, 16, 0), (2000, 100, 0),
                                      (2000, 301, 0), (1500, 1500, 0), (1500, 1500, 3), (700, 4100, 0),
                                      (700, 4100, -1), (600, 3001, 0)])
