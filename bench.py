@@ -239,19 +239,10 @@ def main():
     if args.row_large_n > 0 and args.row_large_steps > 0:
         # The same recipe at a size where X (4 n d bytes) exceeds LDS, L2 and the 256 MB Infinity
         # Cache together, so every step streams most of X from HBM.
-        # Drawn on the device with torch's seeded generator (workload 1's recipe: U[0, 1] entries
-        # zeroed with probability 0.8, labels from the sign of a random projection about its
-        # median, 5% flipped); a timing leg only, so the host generator's exact values are not
-        # needed.
+        # Drawn on the device with torch's seeded generator (workload 1's recipe; the parity tests
+        # draw the same inputs).
         nl = args.row_large_n
-        g = torch.Generator(device="cuda").manual_seed(1)
-        XLd = torch.rand(nl, d, generator=g, device="cuda")
-        XLd.masked_fill_(torch.rand(nl, d, generator=g, device="cuda") < 0.8, 0.0)
-        proj = XLd.double() @ torch.randn(d, generator=g, device="cuda", dtype=torch.float64)
-        yLd = torch.where(proj >= proj.median(), 1, -1).to(torch.int32)
-        flip = torch.randperm(nl, generator=g, device="cuda")[:round(0.05 * nl)]
-        yLd[flip] = -yLd[flip]
-        del proj, flip
+        XLd, yLd = synth.sparse_projection_on_device(nl, d, seed=1)
         svmx.svm_train(XLd, yLd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=16)
         torch.cuda.synchronize()
         r = svmx.svm_train(XLd, yLd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=args.row_large_steps)

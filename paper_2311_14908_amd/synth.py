@@ -202,3 +202,20 @@ def paper_shaped(per_class: int, classes: int, seed: int = 0):
     X = np.clip(mu[lab] + 0.1 * rng.standard_normal((n, d)), 0.0, 1.0).astype(np.float32)
     return np.ascontiguousarray(X), np.ascontiguousarray(lab)
 
+
+def sparse_projection_on_device(n: int, d: int, seed: int = 1):
+    """Workload 1's recipe drawn on the current GPU with torch's seeded generator, for sizes at
+    which drawing on the host is slow (300,000 x 784: about a minute with NumPy): entries U[0,1]
+    zeroed with probability 0.8, label = sign of a random Gaussian projection about its median
+    (0 counts as +1), 5% of the labels flipped.  Same distribution as ``generate(1, n=n, d=d)``,
+    other values.  Returns device tensors (X float32 [n, d], y int32 [n])."""
+    import torch
+
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    X = torch.rand(n, d, generator=g, device="cuda")
+    X.masked_fill_(torch.rand(n, d, generator=g, device="cuda") < 0.8, 0.0)
+    proj = X.double() @ torch.randn(d, generator=g, device="cuda", dtype=torch.float64)
+    y = torch.where(proj >= proj.median(), 1, -1).to(torch.int32)
+    flip = torch.randperm(n, generator=g, device="cuda")[:round(0.05 * n)]
+    y[flip] = -y[flip]
+    return X, y

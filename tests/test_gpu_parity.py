@@ -109,6 +109,29 @@ def test_row_path_largest_placement():
         np.testing.assert_allclose(out.alpha.cpu().numpy(), r.alpha, atol=1e-5, rtol=0)
 
 
+def test_row_path_streamed_large_configuration():
+    """The row path as the 300,000 x 784 measurement runs it: default options, so each
+    workgroup keeps the first rows of its slice in LDS and the rest of X (940 MB, more than
+    LDS, L2 and the Infinity Cache hold) streams from HBM at every step.  The first 20 steps
+    against the oracle on the same bytes: selections, b_up/b_low and the multipliers moved."""
+    wl = synth.workload(1)
+    Xd, yd = synth.sparse_projection_on_device(300_000, 784, seed=1)
+    steps = 20
+    out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=steps, trace_len=steps)
+    assert out.status == svmx.SVM_NOT_CONVERGED and out.stats["iterations"] == steps
+    assert out.stats["gram_used"] == 0 and out.stats["resident_rows"] > 0
+    X, y = Xd.cpu().numpy(), yd.cpu().numpy()
+    del Xd, yd
+    r = oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=steps, trace_len=steps)
+    tied = np.flatnonzero(np.asarray(r.trace_gap)[1:].min(axis=1) < 1e-6)
+    k = min(steps, int(tied[0]) + 1 if tied.size else steps)
+    assert k >= 5
+    np.testing.assert_array_equal(out.trace_ul[:k], r.trace_ul[:k])
+    np.testing.assert_allclose(out.trace_b[:k], r.trace_b[:k], atol=F_ATOL, rtol=0)
+    if k == steps:
+        np.testing.assert_allclose(out.alpha.cpu().numpy(), r.alpha, atol=1e-5, rtol=0)
+
+
 @pytest.mark.parametrize("mfma", MFMAS)
 @pytest.mark.parametrize("cid,n,d", [(0, 1000, 16), (2, 1300, 128), (1, 700, 784), (3, 3001, 32), (0, 333, 13),
                                      (0, 129, 5)])
