@@ -19,7 +19,7 @@ constexpr int ROW_POSITIONS = 4;
 // units, at most 64 (longer rows continue in later blocks).  So a short row does not leave most
 // of a lane's positions masked: its lanes each take up to ROW_POSITIONS units, and a wave holds
 // 64 / gs samples at once.
-__device__ __forceinline__ int group_size_for(int64_t d, bool vec4) {
+__host__ __device__ __forceinline__ int group_size_for(int64_t d, bool vec4) {
   const int64_t units = vec4 ? (d + 3) / 4 : d;
   int gs = 1;
   while ((int64_t)ROW_POSITIONS * gs < units && gs < 64) gs <<= 1;

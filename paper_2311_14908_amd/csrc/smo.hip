@@ -205,12 +205,13 @@ __device__ __forceinline__ void consider(Sel &s, double f, double a, int y, int 
 }
 
 // ---------------------------------------------------------------------------------------
-template <int BS, int PER, bool GRAM, bool VEC4>
+template <int BS, int PER, bool GRAM, bool VEC4, bool ONE = false>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   constexpr int NW = BS / 64;
   // Samples per lane group and batch (a sample's arithmetic does not depend on them): scalar
-  // lanes hold a quarter of the registers per sample, so they take twice as many.
-  constexpr int SB = VEC4 ? ROW_BATCH : 2 * ROW_BATCH;
+  // lanes hold a quarter of the registers per sample, so they take twice as many; ONE: one at
+  // a time (row_batch_one).
+  constexpr int SB = ONE ? 1 : VEC4 ? ROW_BATCH : 2 * ROW_BATCH;
   // Row path, dynamic LDS: dot products against x_u and x_l [2][per_wg] (fp64), cache tags
   // [cap], then the rows of X this workgroup keeps resident [res][d] (16-byte aligned).
   extern __shared__ float4 dyn4[];
@@ -362,7 +363,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         // Streamed samples [res, cnt) go in batches of SBS per group; the first batch of each
         // group is loaded before the resident samples are computed, so its HBM latency
         // overlaps that work.
-        constexpr int SBS = VEC4 ? ROW_SBATCH : 2 * ROW_SBATCH;
+        constexpr int SBS = ONE ? 1 : VEC4 ? ROW_SBATCH : 2 * ROW_SBATCH;
         const int64_t sstride = (int64_t)ngroups * SBS;
         int64_t qs = res + (int64_t)grp * SBS;
         int nbs = 0;
@@ -529,13 +530,23 @@ static bool row_vec4(const SolveParams &p) {
   return (p.d % 4 == 0) && ((reinterpret_cast<uintptr_t>(p.X) & 15) == 0);
 }
 
-template <int BS, int PER, bool GRAM, bool VEC4>
-static const void *kernel_of() {
-  return reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4>);
+// Row path, float4 lanes with 8 samples a thread: there batches of two samples spill registers.
+// For lane groups of up to 8 lanes (rows of up to 128 features) batches of one are faster
+// (1,000,000 x 16: 25.8 -> 17.5 us a step; 1,000,000 x 64: 55.0 -> 46.0; 600,000 x 128: 55.2 ->
+// 49.1); for wider groups the loads one batch keeps in flight matter more than the spill
+// (batches of one: 600,000 x 256 115 -> 120 us, x 512 214 -> 238, x 784 326 -> 362).
+static bool row_batch_one(const SolveParams &p, int32_t per_thread) {
+  return per_thread == 8 && row_vec4(p) && group_size_for(p.d, true) <= 8;
 }
 
-// The solver variant for a path, samples per thread and (row path) float4 lanes; NULL if none.
-static const void *solver_kernel(bool gram, int32_t per_thread, bool vec4) {
+template <int BS, int PER, bool GRAM, bool VEC4, bool ONE = false>
+static const void *kernel_of() {
+  return reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4, ONE>);
+}
+
+// The solver variant for a path, samples per thread, (row path) float4 lanes and batches of
+// one; NULL if none.
+static const void *solver_kernel(bool gram, int32_t per_thread, bool vec4, bool one = false) {
   if (gram) {
     switch (per_thread) {
       case 1: return kernel_of<BS_GRAM, 1, true, false>();
@@ -554,14 +565,14 @@ static const void *solver_kernel(bool gram, int32_t per_thread, bool vec4) {
     case 8: return kernel_of<BS_ROWS, 4, false, false>();
     case 9: return kernel_of<BS_ROWS, 4, false, true>();
     case 16: return kernel_of<BS_ROWS, 8, false, false>();
-    case 17: return kernel_of<BS_ROWS, 8, false, true>();
+    case 17: return one ? kernel_of<BS_ROWS, 8, false, true, true>() : kernel_of<BS_ROWS, 8, false, true>();
     default: return nullptr;
   }
 }
 
 hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
                          int32_t *max_coresident) {
-  const void *fn = solver_kernel(gram, per_thread, !gram && row_vec4(p));
+  const void *fn = solver_kernel(gram, per_thread, !gram && row_vec4(p), !gram && row_batch_one(p, per_thread));
   if (!fn) return hipErrorInvalidValue;
   const int bs = gram ? BS_GRAM : BS_ROWS;
   const size_t shmem = gram ? 0 : row_path_lds(p, p.res_rows);
@@ -588,7 +599,7 @@ int64_t solver_res_rows_max(const SolveParams &p, int32_t per_thread) {
   int dev = 0, max_lds = 0;
   if (hipGetDevice(&dev) != hipSuccess) return -1;
   if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return -1;
-  const void *fn = solver_kernel(false, per_thread, row_vec4(p));
+  const void *fn = solver_kernel(false, per_thread, row_vec4(p), row_batch_one(p, per_thread));
   if (!fn) return -1;
   hipFuncAttributes attr;
   if (hipFuncGetAttributes(&attr, fn) != hipSuccess) return -1;
