@@ -467,14 +467,16 @@ def test_ovo_predict_pairs_equal_binary_predict(k, mfma):
 
 @pytest.mark.parametrize("n,d,res", [(3000, 784, 0), (3000, 784, -1), (3000, 784, 7), (2000, 16, 0), (2000, 100, 0),
                                      (2000, 301, 0), (1500, 1500, 0), (1500, 1500, 3), (700, 4100, 0),
-                                     (700, 4100, -1), (600, 3001, 0)])
+                                     (700, 4100, -1), (600, 3001, 0), (600_000, 16, 0), (600_000, 16, -1),
+                                     (600_000, 64, 0), (540_000, 200, 0), (540_000, 33, 0)])
 def test_row_path_step_uses_the_kernel_row_values(n, d, res):
     """After one row-path step f equals -y + (c_u K(u, .) + c_l K(l, .)) evaluated on the host from
     svm_kernel_rows' fp32 values, bit for bit, at every sample: the solver's row values are the
     entry point's whether its rows of X sit in LDS (all of them, some, or none) or stream from
-    HBM, for lane groups of 64 (784 features), 32 (100) and 4 (16), scalar lanes (301, 3001) and
-    rows longer than one register block (301, 1500, and 4100 and 3001 with 7 and 11 later
-    blocks)."""
+    HBM, for lane groups of 64 (784 features), 32 (100), 16 (200), 4 (64) and 1 (16), scalar lanes
+    (33, 301, 3001), rows longer than one register block (301, 1500, and 4100 and 3001 with 7 and
+    11 later blocks), and with 8 samples a thread (more than 524,288 samples), where rows of up
+    to 128 features go in batches of one sample and wider ones in batches of two."""
     X, y = synth.two_blobs(n, d, seed=d + 1)
     Xd, yd = dev(X), dev(y)
     gamma = 1.0 / d
