@@ -263,6 +263,25 @@ def svm_gram(X, gamma: float, ld: int | None = None, **opt) -> torch.Tensor:
     return G
 
 
+
+def svm_train_host(X: np.ndarray, y: np.ndarray, C_: float, gamma: float, tol: float, **opt):
+    """Host-array convenience around svm_train: X (float32 [n, d]) and y (int32 [n]) are copied
+    to the current device, trained there by the same call, and alpha comes back as a NumPy fp64
+    array.  Returns (alpha, b, status, stats); the copies are the only difference."""
+    Xd = torch.from_numpy(np.ascontiguousarray(X, dtype=np.float32)).cuda()
+    yd = torch.from_numpy(np.ascontiguousarray(y, dtype=np.int32)).cuda()
+    out = svm_train(Xd, yd, C_, gamma, tol, **opt)
+    return out.alpha.cpu().numpy(), out.b, out.status, out.stats
+
+
+def svm_predict_host(X_train: np.ndarray, y: np.ndarray, alpha: np.ndarray, b: float, gamma: float,
+                     X_test: np.ndarray, **opt) -> np.ndarray:
+    """Host-array convenience around svm_predict: the arrays are copied to the current device,
+    the decision values (fp64 [m]) come back as a NumPy array."""
+    dev = lambda a, t: torch.from_numpy(np.ascontiguousarray(a, dtype=t)).cuda()
+    return svm_predict(dev(X_train, np.float32), dev(y, np.int32), dev(alpha, np.float64), b, gamma,
+                       dev(X_test, np.float32), **opt).cpu().numpy()
+
 def ovo_offsets(label: np.ndarray, k: int):
     """Start of each pair's block in the packed alpha of svm_train_ovo, and its size."""
     cnt = np.bincount(np.asarray(label), minlength=k)

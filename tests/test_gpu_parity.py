@@ -109,6 +109,20 @@ def test_row_path_largest_placement():
         np.testing.assert_allclose(out.alpha.cpu().numpy(), r.alpha, atol=1e-5, rtol=0)
 
 
+
+def test_host_array_conveniences_are_the_device_calls():
+    """svm_train_host and svm_predict_host only copy around svm_train and svm_predict: the same
+    alpha, b and decision values, bit for bit."""
+    X, y, Xt, _ = synth.generate(0)
+    a_h, b_h, status, st = svmx.svm_train_host(X, y, C0.C, C0.gamma, C0.tol)
+    out = svmx.svm_train(dev(X), dev(y), C0.C, C0.gamma, C0.tol)
+    assert status == svmx.SVM_OK and st["iterations"] == out.stats["iterations"]
+    np.testing.assert_array_equal(a_h, out.alpha.cpu().numpy())
+    assert b_h == out.b
+    d_h = svmx.svm_predict_host(X, y, a_h, b_h, C0.gamma, Xt)
+    d = svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, C0.gamma, dev(Xt)).cpu().numpy()
+    np.testing.assert_array_equal(d_h, d)
+
 def test_row_path_streamed_large_configuration():
     """The row path as the 300,000 x 784 measurement runs it: default options, so each
     workgroup keeps the first rows of its slice in LDS and the rest of X (940 MB, more than
