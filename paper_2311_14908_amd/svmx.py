@@ -282,6 +282,25 @@ def svm_predict_host(X_train: np.ndarray, y: np.ndarray, alpha: np.ndarray, b: f
     return svm_predict(dev(X_train, np.float32), dev(y, np.int32), dev(alpha, np.float64), b, gamma,
                        dev(X_test, np.float32), **opt).cpu().numpy()
 
+
+def svm_train_ovo_host(X: np.ndarray, label: np.ndarray, k: int, C_: float, gamma: float, tol: float, **opt):
+    """Host-array convenience around svm_train_ovo: returns (packed alpha as NumPy fp64, b [P],
+    status, per-pair stats)."""
+    Xd = torch.from_numpy(np.ascontiguousarray(X, dtype=np.float32)).cuda()
+    ld = torch.from_numpy(np.ascontiguousarray(label, dtype=np.int32)).cuda()
+    out = svm_train_ovo(Xd, ld, k, C_, gamma, tol, **opt)
+    return out.alpha.cpu().numpy(), out.b, out.status, out.stats
+
+
+def svm_predict_ovo_host(X: np.ndarray, label: np.ndarray, k: int, alpha: np.ndarray, b: np.ndarray, gamma: float,
+                         X_test: np.ndarray, **opt):
+    """Host-array convenience around svm_predict_ovo: returns (decision values [m, P], predicted
+    classes [m]) as NumPy arrays."""
+    dev = lambda a, t: torch.from_numpy(np.ascontiguousarray(a, dtype=t)).cuda()
+    dec, pred = svm_predict_ovo(dev(X, np.float32), dev(label, np.int32), k, dev(alpha, np.float64), b, gamma,
+                                dev(X_test, np.float32), **opt)
+    return dec.cpu().numpy(), pred.cpu().numpy()
+
 def ovo_offsets(label: np.ndarray, k: int):
     """Start of each pair's block in the packed alpha of svm_train_ovo, and its size."""
     cnt = np.bincount(np.asarray(label), minlength=k)

@@ -122,6 +122,17 @@ def test_host_array_conveniences_are_the_device_calls():
     d_h = svmx.svm_predict_host(X, y, a_h, b_h, C0.gamma, Xt)
     d = svmx.svm_predict(dev(X), dev(y), out.alpha, out.b, C0.gamma, dev(Xt)).cpu().numpy()
     np.testing.assert_array_equal(d_h, d)
+    k = 4
+    Xo, lab, Xto, _ = synth.generate(4, n=400, m=50, d=12, classes=k)
+    a_o, b_o, s_o, _ = svmx.svm_train_ovo_host(Xo, lab, k, 1.0, 0.1, 1e-3)
+    oo = svmx.svm_train_ovo(dev(Xo), dev(lab), k, 1.0, 0.1, 1e-3)
+    assert s_o == svmx.SVM_OK
+    np.testing.assert_array_equal(a_o, oo.alpha.cpu().numpy())
+    np.testing.assert_array_equal(b_o, oo.b)
+    dh, ph = svmx.svm_predict_ovo_host(Xo, lab, k, a_o, b_o, 0.1, Xto)
+    dd, pd = svmx.svm_predict_ovo(dev(Xo), dev(lab), k, oo.alpha, oo.b, 0.1, dev(Xto))
+    np.testing.assert_array_equal(dh, dd.cpu().numpy())
+    np.testing.assert_array_equal(ph, pd.cpu().numpy())
 
 def test_row_path_streamed_large_configuration():
     """The row path as the 300,000 x 784 measurement runs it: default options, so each
