@@ -105,7 +105,11 @@ def test_binary_full_size(cid, gram):
     assert np.all(f[low] <= out.b + wl.tol / 2 + slack)
 
 
-def test_ovo_full_size():
+@pytest.mark.parametrize("gram", [svmx.GRAM_AUTO, svmx.GRAM_OFF])
+def test_ovo_full_size(gram):
+    """All 45 pairs of the 60,000 x 784 workload to convergence, from the class-sorted global Gram
+    (default) or on the row path: every pair's W against the stored oracle optimum, decisions and
+    votes on the stored test points."""
     R = ref(4)
     wl = synth.workload(4)
     k = wl.classes
@@ -113,15 +117,16 @@ def test_ovo_full_size():
     nt = len(R["test_pred"])
     assert digest(X, lab, Xt[:nt]) == R["inputs_sha256"], "inputs differ from the stored reference"
     Xd, ld = dev(X), dev(lab)
-    out = svmx.svm_train_ovo(Xd, ld, k, wl.C, wl.gamma, wl.tol)
+    out = svmx.svm_train_ovo(Xd, ld, k, wl.C, wl.gamma, wl.tol, gram=gram)
     assert out.status == svmx.SVM_OK
+    assert all(st["gram_used"] == (1 if gram == svmx.GRAM_AUTO else 0) for st in out.stats)
     for p, rp in enumerate(R["pairs"]):
         assert abs(out.stats[p]["dual_obj"] - rp["dual_obj"]) <= 1e-4 * abs(rp["dual_obj"])
     dec, pred = svmx.svm_predict_ovo(Xd, ld, k, out.alpha, out.b, wl.gamma, dev(Xt[:nt]))
     d_ref = np.array(R["test_decisions"])
     dec = dec.cpu().numpy()
     err = np.max(np.abs(dec - d_ref))
-    print(f"\none-vs-one: max |d_gpu - d_oracle| = {err:.2e}")
+    print(f"\none-vs-one (gram {gram}): max |d_gpu - d_oracle| = {err:.2e}")
     assert err <= 1e-3
     sure = np.all(np.abs(d_ref) >= 1e-3, axis=1)
     assert np.array_equal(pred.cpu().numpy()[sure], np.array(R["test_pred"])[sure])
