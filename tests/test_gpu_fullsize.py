@@ -154,7 +154,7 @@ def test_ovo_row_path_full_size_pairs_equal_binary():
 
 
 @pytest.mark.parametrize("cid,q,gram", [(1, 128, svmx.GRAM_AUTO), (1, 128, svmx.GRAM_OFF), (2, 32, svmx.GRAM_AUTO),
-                                        (3, 32, svmx.GRAM_AUTO)])
+                                        (2, 32, svmx.GRAM_OFF), (3, 32, svmx.GRAM_AUTO), (3, 32, svmx.GRAM_OFF)])
 def test_working_set_full_size(cid, q, gram):
     """The working-set solver at the full sizes reaches the optimum of the stored oracle
     solve (its trajectory differs from the pair steps', so the gates are those of the optimum):
