@@ -294,13 +294,22 @@ def test_max_iter_not_converged_feasible():
     assert abs(out.b - r.b) <= F_ATOL
 
 
-def test_results_independent_of_check_cadence():
-    X, y = synth.two_blobs(3000, 8, seed=8)
-    ref = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3)
+@pytest.mark.parametrize("n,d,gram,steps", [(3000, 8, svmx.GRAM_AUTO, 0), (3000, 8, svmx.GRAM_OFF, 0),
+                                           (600_000, 16, svmx.GRAM_OFF, 60)])
+def test_results_independent_of_check_cadence(n, d, gram, steps):
+    """The same steps, multipliers and bias whether the solve runs in launches of 1, 7, 256 or
+    the default number of steps: on the Gram path, on the row path (its resident rows of X are
+    loaded into LDS again at every launch) and on the row path with 8 samples a thread (60
+    steps)."""
+    X, y = synth.two_blobs(n, d, seed=8)
+    kw = dict(gram=gram, max_iter=steps) if steps else dict(gram=gram)
+    ref = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3, **kw)
+    assert ref.stats["gram_used"] == (1 if gram == svmx.GRAM_AUTO else 0)
     for ce in (1, 7, 256):
-        out = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3, check_every=ce)
+        out = svmx.svm_train(dev(X), dev(y), 1.0, 0.1, 1e-3, check_every=ce, **kw)
         assert torch.equal(out.alpha, ref.alpha) and out.b == ref.b
         assert out.stats["iterations"] == ref.stats["iterations"]
+        assert out.stats["launches"] >= ref.stats["iterations"] // ce
 
 
 def test_row_cache_does_not_change_results():
