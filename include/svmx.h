@@ -49,7 +49,8 @@ typedef enum {
   SVM_OK = 0,
   SVM_NOT_CONVERGED = 1,
   SVM_EINVAL = -1,     /* invalid argument */
-  SVM_ENOMEM = -2,     /* problem too large for the device or for 64-bit sizes */
+  SVM_ENOMEM = -2,     /* problem too large for the device, or n beyond the 32-bit sample index
+                          (n > 2^31 - 2) */
   SVM_EDEVICE = -3,    /* a HIP call failed, or a device-side wait exceeded its time limit */
   SVM_EWORKSPACE = -4  /* workspace NULL or smaller than the size query returned */
 } svm_status;
@@ -121,6 +122,12 @@ typedef struct {
   int64_t rounds;       /* working-set rounds (0 for the per-step solver) */
   int32_t resident_rows; /* rows of X each solver workgroup kept in LDS (binary row path) */
   int32_t reserved;
+  double t_upload;      /* seconds of input validation and staging before the precompute: the
+                           labels copied to the host and checked (one-vs-one: and class-sorted),
+                           the problem descriptors copied to the device, the device-side scan of X
+                           for values that are not finite (one-vs-one: and the class-sorted copy of
+                           X).  The inputs themselves are device buffers, so no copy of X over
+                           PCIe is part of any call. */
 } svm_stats;
 
 /* Fill *o with the defaults above. */
@@ -143,7 +150,7 @@ int64_t svm_train_workspace_bytes(int64_t n, int64_t d, const svm_options *o);
  *   o      options or NULL;  st  host stats out or NULL
  * EINVAL: n<2, d<1, non-finite or non-positive C/gamma/tol, NULL pointers, a label not in
  * {+1,-1} or only one class present, a value of X that is not finite (checked on the device
- * before any other work).
+ * before any other work), byte counts of n*d or of the n^2 Gram that overflow int64.
  */
 svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma, double tol,
                      double *alpha, double *b, void *workspace, int64_t workspace_bytes, const svm_options *o,

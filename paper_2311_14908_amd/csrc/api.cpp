@@ -199,7 +199,7 @@ struct TrainPlan {
 svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   if (n < 2 || d < 1) return fail(SVM_EINVAL, "need n >= 2 and d >= 1 (got n=%lld, d=%lld)", (long long)n, (long long)d);
   if (n > 0x7ffffffeLL) return fail(SVM_ENOMEM, "n=%lld exceeds the 32-bit sample index", (long long)n);
-  if (d > (INT64_MAX / 8) / n) return fail(SVM_ENOMEM, "n*d overflows");
+  if (d > (INT64_MAX / 8) / n) return fail(SVM_EINVAL, "n*d overflows 64-bit byte counts");
   p->ld = round_up(n, 64);
   const double gram_bytes = 4.0 * (double)n * (double)p->ld;
   if (o.gram == SVM_GRAM_ON)
@@ -208,7 +208,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
     p->gram = false;
   else
     p->gram = gram_bytes <= (double)o.gram_budget;
-  if (p->gram && gram_bytes > 9.0e18) return fail(SVM_ENOMEM, "Gram size overflows");
+  if (p->gram && gram_bytes > 9.0e18) return fail(SVM_EINVAL, "the Gram's n^2 size overflows 64-bit byte counts");
   if (o.working_set > 0) {
     if (!choose_ws_shape(n, o.workgroups, o.working_set, p->gram, &p->shape))
       return fail(SVM_ENOMEM, "n=%lld exceeds the working-set solver's %d workgroups of %d samples", (long long)n,
@@ -367,7 +367,7 @@ svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) 
   if (n < 2 || d < 1) return fail(SVM_EINVAL, "need n >= 2 and d >= 1");
   if (k < 2 || k > MAX_CLASSES) return fail(SVM_EINVAL, "k=%d must be in [2, %d]", k, MAX_CLASSES);
   if (n > 0x7ffffffeLL) return fail(SVM_ENOMEM, "n too large");
-  if (d > (INT64_MAX / 8) / n) return fail(SVM_ENOMEM, "n*d overflows");
+  if (d > (INT64_MAX / 8) / n) return fail(SVM_EINVAL, "n*d overflows 64-bit byte counts");
   p->P = k * (k - 1) / 2;
   p->ld = round_up(n, 64);
   const double gram_bytes = 4.0 * (double)n * (double)p->ld;
@@ -545,6 +545,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   if (s0 != SVM_OK) return s0;
   if (p.cache_cap)
     HIPCHK(hipMemsetAsync(ws + p.off_tags, 0xff, 4LL * p.cache_cap * p.shape.nwg, stream));
+  const double t_upload = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
 
   Timer tg, ts, tf;
   HIPCHK(tg.init());
@@ -654,6 +655,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     st->rounds = r.working_set > 0 ? h_rounds : 0;
     st->resident_rows = sp.res_rows;
     st->reserved = 0;
+    st->t_upload = t_upload;
   }
   return c.status == ST_MAXITER ? SVM_NOT_CONVERGED : SVM_OK;
 }
@@ -670,12 +672,13 @@ svm_status svm_predict(const float *X_train, const int32_t *y, const double *alp
   if (n < 1 || d < 1 || m < 0) return fail(SVM_EINVAL, "need n >= 1, d >= 1, m >= 0");
   if (!X_train || !y || !alpha || (m > 0 && (!X_test || !dec))) return fail(SVM_EINVAL, "NULL pointer argument");
   if (!finite_pos(gamma) || !std::isfinite(b)) return fail(SVM_EINVAL, "gamma must be finite and > 0, b finite");
-  if (n > 0x7ffffffeLL || d > (INT64_MAX / 8) / std::max<int64_t>(n, m)) return fail(SVM_ENOMEM, "sizes overflow");
+  if (n > 0x7ffffffeLL) return fail(SVM_ENOMEM, "n=%lld exceeds the 32-bit sample index", (long long)n);
+  if (d > (INT64_MAX / 8) / std::max<int64_t>(n, m)) return fail(SVM_EINVAL, "sizes overflow 64-bit byte counts");
   Opts r;
   if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options");
   if (m == 0) return SVM_OK;
   const int64_t need = svm_predict_workspace_bytes(n, d, m);
-  if (need < 0) return fail(SVM_ENOMEM, "sizes overflow");
+  if (need < 0) return fail(SVM_EINVAL, "sizes overflow 64-bit byte counts");
   if (!workspace || workspace_bytes < need)
     return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)need, (long long)workspace_bytes);
   PredictWs pw = predict_scratch(workspace, n, n, 1, m, d);
@@ -828,9 +831,10 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   HIPCHK(hipMemcpyAsync(dprob, hp.data(), sizeof(Prob) * hp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemsetAsync(err, 0, 16, stream));
-  s0 = check_finite(X, n * d, err + 2, stream);
-  if (s0 != SVM_OK) return s0;
   HIPCHK(launch_gather_rows(X, d, dperm, n, Xs, stream));
+  s0 = check_finite(X, n * d, err + 2, stream);  // its synchronisation also ends the class-sorted copy
+  if (s0 != SVM_OK) return s0;
+  const double t_upload = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
 
   Timer tg, ts, tf;
   HIPCHK(tg.init());
@@ -912,6 +916,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
       S.rounds = 0;
       S.resident_rows = 0;
       S.reserved = 0;
+      S.t_upload = t_upload;
     }
   }
   return maxed ? SVM_NOT_CONVERGED : SVM_OK;
@@ -993,7 +998,7 @@ svm_status svm_kernel_rows(const float *X, int64_t n, int64_t d, double gamma, c
   if (!X || !rows || !out) return fail(SVM_EINVAL, "NULL pointer argument");
   if (n < 1 || d < 1 || r < 1) return fail(SVM_EINVAL, "need n, d, r >= 1");
   if (!finite_pos(gamma)) return fail(SVM_EINVAL, "gamma must be finite and > 0");
-  if (d > (INT64_MAX / 8) / n || r > INT64_MAX / 8 / n) return fail(SVM_ENOMEM, "sizes overflow");
+  if (d > (INT64_MAX / 8) / n || r > INT64_MAX / 8 / n) return fail(SVM_EINVAL, "sizes overflow 64-bit byte counts");
   if (2 * 4 * d > LDS_BYTES) return fail(SVM_EINVAL, "d too large for the staged rows");
   Opts op;
   if (!resolve(o, n, &op)) return fail(SVM_EINVAL, "bad options");
@@ -1019,7 +1024,7 @@ svm_status svm_gram(const float *X, int64_t n, int64_t d, double gamma, float *G
   if (!X || !G) return fail(SVM_EINVAL, "NULL pointer argument");
   if (n < 1 || d < 1 || ld < n) return fail(SVM_EINVAL, "need n, d >= 1 and ld >= n");
   if (!finite_pos(gamma)) return fail(SVM_EINVAL, "gamma must be finite and > 0");
-  if (d > (INT64_MAX / 8) / n || ld > (INT64_MAX / 8) / n) return fail(SVM_ENOMEM, "sizes overflow");
+  if (d > (INT64_MAX / 8) / n || ld > (INT64_MAX / 8) / n) return fail(SVM_EINVAL, "sizes overflow 64-bit byte counts");
   Opts op;
   if (!resolve(o, n, &op)) return fail(SVM_EINVAL, "bad options");
   if (op.gram_mfma == SVM_MFMA_SPLIT_F16) {

@@ -43,7 +43,7 @@ class svm_stats(C.Structure):
                 ("b_low", C.c_double), ("dual_obj", C.c_double), ("gram_used", C.c_int32), ("launches", C.c_int32),
                 ("t_gram", C.c_double), ("t_solve", C.c_double), ("t_finalize", C.c_double), ("t_total", C.c_double),
                 ("t_kernel", C.c_double), ("rounds", C.c_int64),
-                ("resident_rows", C.c_int32), ("reserved", C.c_int32)]
+                ("resident_rows", C.c_int32), ("reserved", C.c_int32), ("t_upload", C.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

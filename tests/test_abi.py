@@ -39,7 +39,7 @@ def test_struct_layouts_match_header():
     lib.svm_default_options(C.byref(o))
     assert o.struct_size == C.sizeof(svmx.svm_options) == 96
     assert o.check_every == 65536 and o.gram == svmx.GRAM_AUTO
-    assert C.sizeof(svmx.svm_stats) == 112
+    assert C.sizeof(svmx.svm_stats) == 120
 
 
 def _opts(**kw):
@@ -92,7 +92,8 @@ FAKE = C.c_void_p(0x1000)  # never dereferenced: every case below fails validati
     (dict(tol=float("nan")), svmx.SVM_EINVAL),
     (dict(wsb=16), svmx.SVM_EWORKSPACE),
     (dict(ws=None), svmx.SVM_EWORKSPACE),
-    (dict(n=1 << 40, d=1 << 30), svmx.SVM_ENOMEM),
+    (dict(n=1 << 40, d=1 << 30), svmx.SVM_ENOMEM),  # n beyond the 32-bit sample index
+    (dict(n=1 << 30, d=1 << 34), svmx.SVM_EINVAL),  # n*d bytes overflow int64
 ])
 def test_train_rejects(case, expect):
     lib = svmx.load()
