@@ -3,23 +3,27 @@
 
 One step is one pass of the whole hot path over one synthetic workload: RBF Gram build
 (MFMA), the SMO solve to tol, the finalize reduction, and decision values for the test
-split.  Inputs are resident in HBM before the timed region starts.
+split.  Inputs are resident in HBM before the timed region starts.  The default workload is
+the largest single-GPU binary one, 100,000 x 32 with its 40 GB fp32 Gram resident in HBM.
 
 Prints ONE JSON line.  ``value`` is SMO iterations per second over the timed steps;
 ``train_seconds`` is the mean svm_train wall time.  ``roofline`` describes the dominant
 kernel (the persistent SMO solver) against the HBM roofline with the algorithmic bytes of
-an SMO step (two kernel rows 8n, f read+write 16n, status n = 25n bytes); ``row_path``
-reports the same solve with kernel rows evaluated from X at every step (4nd + 21n bytes a
-step).  ``ovo_row_path`` runs the 45 one-vs-one pairs of the 10-class workload on the row
-path, all pairs in one launch, for a fixed number of steps (4 n_p d + 21 n_p bytes per pair
-step).  ``paper_shapes`` times single trainings at the shapes of the paper's own runs (102
-features, 200-800 samples per class, binary and nine-class one-vs-one) for context.
-``workloads`` trains the other binary workloads (1,000 x 16, 50,000 x 128, 100,000 x 32) end to
-end once each.  ``working_set`` trains the Gram-path workloads with the working-set solver
+an SMO step (two kernel rows 8n, f read+write 16n, status n = 25n bytes).  ``gram_build``
+reports the Gram precompute against the dense fp16 MFMA peak (its contraction runs as
+split-fp16 products) with the method's n^2 d flops.  ``row_path`` reports the 20,000 x 784
+solve with kernel rows evaluated from X at every step (4nd + 21n bytes a step), and
+``row_path_large`` the same recipe at 300,000 x 784.  ``ovo`` trains the 10-class one-vs-one
+workload end to end, with rooflines for its global Gram and for the launch that advances all
+45 pairs; ``ovo_row_path`` runs the 45 pairs on the row path for a fixed number of steps
+(4 n_p d + 21 n_p bytes per pair step).  ``paper_shapes`` times single trainings at the
+shapes of the paper's own runs (102 features, 200-800 samples per class, binary and nine-class
+one-vs-one) for context.  ``workloads`` trains the other binary workloads end to end once
+each.  ``working_set`` trains the Gram-path workloads with the working-set solver
 (svm_options.working_set = q: rounds of pair steps on q samples, f updated once a round) beside
 the pair solver, and the 20,000 x 784 workload once more without a Gram (row path); its
-iterations are pair steps too.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample of the same workload
-(first SMO steps of the same problem, on this host's cores).
+iterations are pair steps too.  ``cpu_baseline`` times the fp64 CPU oracle on the same problem
+on this host's cores: the whole training when it fits the time budget, else its first steps.
 """
 from __future__ import annotations
 
@@ -33,18 +37,21 @@ HBM_PEAK_GBPS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 FP16_MFMA_PEAK_TFLOPS = 2500.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
-COUNTERS = os.path.join(ROOT, "profiles", "smo_solve_n20000_d784_hbm_counters.md")
 SOLVER_SOURCES = ("paper_2311_14908_amd/csrc/smo.hip", "paper_2311_14908_amd/csrc/rbf_rows.hpp",
                   "paper_2311_14908_amd/csrc/solver_params.hpp", "paper_2311_14908_amd/csrc/pair_step.hpp")
 
 
-def counter_bytes_per_step(workload_name):
+def counters_path(n, d):
+    return os.path.join(ROOT, "profiles", f"smo_solve_n{n}_d{d}_hbm_counters.md")
+
+
+def counter_bytes_per_step(workload_name, n, d):
     """HBM bytes per SMO step measured with rocprofv3 FETCH_SIZE/WRITE_SIZE (scaled by a copy of
     known size), as recorded in profiles/; None when missing, for another workload, or when the
     solver sources changed after the counters were taken."""
     import hashlib
     try:
-        line = [l for l in open(COUNTERS) if "solver_sources_sha256" in l][0]
+        line = [l for l in open(counters_path(n, d)) if "solver_sources_sha256" in l][0]
         rec = json.loads(line.strip())
     except (OSError, IndexError, ValueError):
         return None
@@ -56,6 +63,18 @@ def counter_bytes_per_step(workload_name):
     return rec
 
 
+def gram_roofline(n, d, seconds):
+    """The Gram precompute against the dense fp16 MFMA peak, with the method's n^2 d flops."""
+    flops = float(n) * n * d
+    tf = flops / seconds / 1e12 if seconds > 0 else None
+    return {"kernel": "gram_rbf_f16x3 (fp32 inputs split into fp16 halves, 3 products per fp32 product)",
+            "bound": "mfma", "flops": flops, "seconds": seconds, "achieved": tf, "peak": FP16_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": tf / FP16_MFMA_PEAK_TFLOPS if tf else None,
+            "executed_fp16_tflops": 3.0 * tf if tf else None,
+            "fp32_equivalent_vs_fp32_mfma_peak": tf / FP32_MFMA_PEAK_TFLOPS if tf else None,
+            "gram_bytes": 4.0 * n * n, "write_GBps": 4.0 * n * n / seconds / 1e9 if seconds > 0 else None}
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -65,14 +84,16 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", type=int, default=1, help="synthetic workload id (0..3 binary)")
+    ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (0..3 binary)")
     ap.add_argument("--gram", choices=["auto", "on", "off"], default="auto")
     ap.add_argument("--row-path-steps", type=int, default=4000, help="SMO steps of the row-path measurement (0 = skip)")
     ap.add_argument("--row-large-n", type=int, default=300_000,
                     help="samples of the large row-path measurement (workload 1's recipe, X far larger than the "
                          "on-chip memories and the Infinity Cache; 0 = skip)")
     ap.add_argument("--row-large-steps", type=int, default=200, help="SMO steps of the large row-path measurement")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle sample time (0 = skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=45.0,
+                    help="CPU-oracle time budget: the whole training when its predicted time fits, else the first "
+                         "steps that fit (0 = skip)")
     ap.add_argument("--no-ovo", action="store_true", help="skip the one-vs-one measurement (60000x784, 10 classes)")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the end-to-end trainings of the other binary workloads")
@@ -143,12 +164,10 @@ def main():
     t_kernel = sum(s["t_kernel"] for s in st)
     step_bytes = 25.0 * n
     solver_gbps = step_bytes * iters / t_kernel / 1e9
-    counters = counter_bytes_per_step(wl.name)
+    counters = counter_bytes_per_step(wl.name, n, d)
     gram_used = bool(st[0]["gram_used"])
     traffic = (counters["gram_path_hbm_bytes_per_smo_step"] * iters / launches
                if counters and gram_used else None)
-    gram_flops = float(n) * n * d
-    gram_tflops = gram_flops / mean("t_gram") / 1e12 if mean("t_gram") > 0 else None
 
     result = {
         "metric": "SMO iterations/sec + train seconds; kernel-row HBM GB/s vs peak",
@@ -161,13 +180,13 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32 kernel values, f64 solve",
+        "dtype": "f32 kernel values (Gram contraction: split-fp16 x3 MFMA products, fp32 accumulation), f64 solve",
         "data": "synthetic (seeded), resident in HBM",
         "config": {"workload": f"{wl.name}: binary RBF-SVM, C={wl.C:g}, gamma={wl.gamma:g}, tol={wl.tol:g}",
                    "n": n, "d": d, "m_test": m, "gram": bool(st[0]["gram_used"])},
         "train_seconds": mean("t_total"),
         "iterations_per_step": iters / args.steps,
-        "phases_s": {"gram": mean("t_gram"), "solve": mean("t_solve"), "solver_kernel": t_kernel / args.steps,
+        "phases_s": {"upload": mean("t_upload"), "gram": mean("t_gram"), "solve": mean("t_solve"), "solver_kernel": t_kernel / args.steps,
                      "finalize": mean("t_finalize"), "predict": float(np.mean(t_pred))},
         "n_sv": st[-1]["n_sv"], "n_bound_sv": st[-1]["n_bound_sv"], "dual_obj": st[-1]["dual_obj"],
         "test_accuracy": acc,
@@ -179,13 +198,9 @@ def main():
                              "cross-workgroup exchange of the selections and the dependent read of "
                              "the two Gram rows"},
         # the default Gram runs the fp32 contraction as three fp16 MFMA products per fp32 product
-        # (split halves), so its own peak is the dense fp16 one; n^2 d is the fp32-equivalent count
-        "gram_build": {"kernel": "gram_rbf_f16x3 (fp32 inputs split into fp16 halves)", "bound": "mfma",
-                       "flops": gram_flops, "achieved_tflops": gram_tflops,
-                       "executed_fp16_tflops": 3.0 * gram_tflops if gram_tflops else None,
-                       "peak_tflops": FP16_MFMA_PEAK_TFLOPS,
-                       "frac": (3.0 * gram_tflops / FP16_MFMA_PEAK_TFLOPS) if gram_tflops else None,
-                       "fp32_equivalent_vs_fp32_mfma_peak": (gram_tflops / FP32_MFMA_PEAK_TFLOPS) if gram_tflops else None},
+        # (split halves) on the fp16 MFMA instruction, so its peak is the dense fp16 one; the
+        # achieved rate counts the method's n^2 d flops (symmetric), not the executed products
+        "gram_build": gram_roofline(n, d, mean("t_gram")),
     }
 
     # The same training from host arrays: X and y in pinned host memory, copied to the device,
@@ -212,21 +227,29 @@ def main():
                                      "included; not the headline value"}
     del Xd2, yd2, Xh, yh, ah
 
+    # The row path on the 20,000 x 784 workload (where the kernel-row GEMV is the step's work) and on
+    # the same recipe at 300,000 x 784.
+    w1 = synth.workload(1)
+    counters1 = counter_bytes_per_step(w1.name, w1.n, w1.d)
     if args.row_path_steps > 0:
         k = args.row_path_steps
-        svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=64)
+        X1, y1, _, _ = synth.generate(1, m=1)
+        n1, d1 = X1.shape
+        X1d, y1d = torch.from_numpy(X1).cuda(), torch.from_numpy(y1).cuda()
+        svmx.svm_train(X1d, y1d, w1.C, w1.gamma, w1.tol, gram=svmx.GRAM_OFF, max_iter=64)
         torch.cuda.synchronize()
-        rb = 4.0 * n * d + 21.0 * n
+        rb = 4.0 * n1 * d1 + 21.0 * n1
         # default (the first rows of every workgroup's slice resident in LDS), then every row
         # streamed from HBM at every step
         for key, res, ckey in (("row_path", 0, "row_path_hbm_bytes_per_smo_step"),
                                ("row_path_streamed", -1, "row_path_streamed_hbm_bytes_per_smo_step")):
-            r = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=k, resident_rows=res)
+            r = svmx.svm_train(X1d, y1d, w1.C, w1.gamma, w1.tol, gram=svmx.GRAM_OFF, max_iter=k, resident_rows=res)
             s = r.stats
             gbps = rb * s["iterations"] / s["t_kernel"] / 1e9
-            rtraffic = (counters[ckey] * s["iterations"] / s["launches"] if counters and ckey in counters else None)
-            result[key] = {"kernel": "smo_solve (row path)", "bound": "hbm", "smo_steps": s["iterations"],
-                           "iters_per_s": s["iterations"] / s["t_kernel"], "bytes_per_step": rb,
+            rtraffic = (counters1[ckey] * s["iterations"] / s["launches"] if counters1 and ckey in counters1 else None)
+            result[key] = {"kernel": "smo_solve (row path)", "workload": w1.name, "bound": "hbm",
+                           "smo_steps": s["iterations"], "iters_per_s": s["iterations"] / s["t_kernel"],
+                           "us_per_step": 1e6 * s["t_kernel"] / s["iterations"], "bytes_per_step": rb,
                            "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS,
                            "traffic": rtraffic, "resident_rows_per_workgroup": s["resident_rows"]}
             if res == 0:
@@ -235,29 +258,31 @@ def main():
                 result[key].update({"bound": "on-chip (X in LDS and L2)",
                                     "note": "achieved counts the algorithmic bytes 4nd+21n; X is not re-read from "
                                             "HBM at this size, so frac is an effective rate, not HBM use"})
+        del X1d, y1d
 
     if args.row_large_n > 0 and args.row_large_steps > 0:
         # The same recipe at a size where X (4 n d bytes) exceeds LDS, L2 and the 256 MB Infinity
         # Cache together, so every step streams most of X from HBM.
         # Drawn on the device with torch's seeded generator (workload 1's recipe; the parity tests
         # draw the same inputs).
-        nl = args.row_large_n
-        XLd, yLd = synth.sparse_projection_on_device(nl, d, seed=1)
-        svmx.svm_train(XLd, yLd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=16)
+        nl, dl = args.row_large_n, w1.d
+        XLd, yLd = synth.sparse_projection_on_device(nl, dl, seed=1)
+        svmx.svm_train(XLd, yLd, w1.C, w1.gamma, w1.tol, gram=svmx.GRAM_OFF, max_iter=16)
         torch.cuda.synchronize()
-        r = svmx.svm_train(XLd, yLd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_OFF, max_iter=args.row_large_steps)
+        r = svmx.svm_train(XLd, yLd, w1.C, w1.gamma, w1.tol, gram=svmx.GRAM_OFF, max_iter=args.row_large_steps)
         s = r.stats
-        rbl = 4.0 * nl * d + 21.0 * nl
+        rbl = 4.0 * nl * dl + 21.0 * nl
         gbps = rbl * s["iterations"] / s["t_kernel"] / 1e9
         ckey = "row_path_large_hbm_bytes_per_smo_step"
-        rtraffic = (counters[ckey] * s["iterations"] / s["launches"] if counters and ckey in counters else None)
+        rtraffic = (counters1[ckey] * s["iterations"] / s["launches"] if counters1 and ckey in counters1 else None)
         result["row_path_large"] = {"kernel": "smo_solve (row path)", "bound": "hbm",
-                                    "workload": f"sparse-proj-n{nl}-d{d} (recipe of {wl.name})",
+                                    "workload": f"sparse-proj-n{nl}-d{dl} (recipe of {w1.name})",
                                     "smo_steps": s["iterations"], "us_per_step": 1e6 * s["t_kernel"] / s["iterations"],
                                     "bytes_per_step": rbl, "achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                                     "frac": gbps / HBM_PEAK_GBPS, "traffic": rtraffic,
                                     "resident_rows_per_workgroup": s["resident_rows"]}
         del XLd, yLd
+        torch.cuda.empty_cache()
 
     if not args.no_ovo:
         wo = synth.workload(4)
@@ -275,13 +300,24 @@ def main():
         t_pred = time.perf_counter() - t1
         it = sum(p["iterations"] for p in oo.stats)
         no = Xo.shape[0]
+        _, osz = svmx.ovo_offsets(lo, wo.classes)
+        # the launch that advances all 45 pairs: 25 n_p algorithmic bytes per pair step (two
+        # Gram row slices, f read and write, status), over the solver kernel's time
+        obytes = sum(25.0 * float(sz) * p["iterations"] for sz, p in zip(osz, oo.stats))
+        otk = oo.stats[0]["t_kernel"]
         result["ovo"] = {"workload": f"{wo.name}: {wo.classes}-class one-vs-one RBF-SVM, 45 pairs, C={wo.C:g}, "
                                      f"gamma={wo.gamma:g}, tol={wo.tol:g}",
                          "train_seconds": t_train, "smo_iterations": it, "iters_per_s": it / t_train,
-                         "gram_seconds": oo.stats[0]["t_gram"],
-                         "gram_tflops": float(no) * no * Xo.shape[1] / oo.stats[0]["t_gram"] / 1e12,
-                         "solver_kernel_seconds": oo.stats[0]["t_kernel"], "predict_seconds": t_pred,
-                         "test_accuracy": float(np.mean(pred.cpu().numpy() == lto))}
+                         "upload_seconds": oo.stats[0]["t_upload"], "gram_seconds": oo.stats[0]["t_gram"],
+                         "solver_kernel_seconds": otk, "predict_seconds": t_pred,
+                         "test_accuracy": float(np.mean(pred.cpu().numpy() == lto)),
+                         "gram_build": gram_roofline(no, Xo.shape[1], oo.stats[0]["t_gram"]),
+                         "roofline": {"kernel": "smo_solve (Gram path, 45 pairs in one launch)", "bound": "hbm",
+                                      "bytes": obytes, "bytes_per_pair_step": "25*n_p", "kernel_seconds": otk,
+                                      "launches": oo.stats[0]["launches"], "achieved": obytes / otk / 1e9,
+                                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                      "frac": obytes / otk / 1e9 / HBM_PEAK_GBPS,
+                                      "us_per_pair_step": 1e6 * otk / it * len(osz)}}
         if args.ovo_row_steps > 0:
             # the same 45 pairs on the row path: every pair evaluates its kernel rows from X at
             # every step, all pairs in one launch (batched one-vs-one steps)
@@ -309,7 +345,7 @@ def main():
     if not args.no_workloads:
         # the other binary workloads, end to end (one warm-up and one timed training each)
         per = {}
-        for cid in (0, 2, 3):
+        for cid in (0, 1, 2, 3):
             if cid == args.workload:
                 continue
             wk = synth.workload(cid)
@@ -322,9 +358,14 @@ def main():
             torch.cuda.synchronize()
             tk = time.perf_counter() - t1
             sk = rk.stats
+            nk = Xk.shape[0]
+            gb = 25.0 * nk * sk["iterations"] / sk["t_kernel"] / 1e9
             per[wk.name] = {"train_seconds": tk, "smo_iterations": sk["iterations"],
                             "iters_per_s": sk["iterations"] / sk["t_solve"], "gram_seconds": sk["t_gram"],
-                            "us_per_smo_step": 1e6 * sk["t_kernel"] / sk["iterations"], "gram_used": sk["gram_used"]}
+                            "us_per_smo_step": 1e6 * sk["t_kernel"] / sk["iterations"], "gram_used": sk["gram_used"],
+                            "solver_GBps": gb, "solver_frac_of_hbm_peak": gb / HBM_PEAK_GBPS}
+            if sk["gram_used"] and nk > 4096:
+                per[wk.name]["gram_build"] = gram_roofline(nk, Xk.shape[1], sk["t_gram"])
             del Xkd, ykd, rk
             torch.cuda.empty_cache()
         result["workloads"] = per
@@ -407,25 +448,33 @@ def main():
         result["paper_shapes"] = {"d": ps["d"], "per_class": [200, 400, 600, 800], **shapes}
 
     if args.cpu_seconds > 0:
+        # The fp64 oracle on the same problem: the whole training when its time, predicted from
+        # a probe of its first steps and the GPU's step count, fits the budget; else the first
+        # steps that fit.  All host threads (OpenMP over the per-sample loops).
         import oracle
         threads = oracle.max_threads()
+        cache = 16 << 30  # the full fp64 Gram when it fits, else a least-recently-used row cache
         probe = 20
         t1 = time.perf_counter()
-        oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=probe, cache_bytes=1 << 30)
+        oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=probe, cache_bytes=cache)
         rate = probe / max(time.perf_counter() - t1, 1e-6)
-        k = int(min(200_000, max(probe, rate * args.cpu_seconds)))
+        expect = 1.2 * iters / args.steps
+        full = expect <= rate * args.cpu_seconds
+        k = None if full else int(max(probe, rate * args.cpu_seconds))
         t1 = time.perf_counter()
-        r = oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=k, cache_bytes=1 << 30)
+        r = oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=k, cache_bytes=cache)
         tc = time.perf_counter() - t1
+        what = (f"the whole training ({r.iterations} SMO steps to tol, status {r.status})" if k is None
+                else f"the first {r.iterations} SMO steps")
         result["cpu_baseline"] = {"value": r.iterations / tc, "unit": "SMO iterations/s", "cores": threads,
-                                  "kind": "oracle",
-                                  "sample": f"first {r.iterations} SMO steps of the same {n}x{d} problem, fp64 oracle "
-                                            f"with a 1 GiB LRU kernel-row cache, {tc:.1f} s"}
-        # the same oracle on one host thread: a bounded sample of the same problem (about a
-        # fifth of the time above), and the whole 1,000 x 16 training
-        k1 = int(max(10, rate / max(threads, 1) * args.cpu_seconds / 5))
+                                  "kind": "oracle", "seconds": tc,
+                                  "sample": f"{what} of the same {n}x{d} problem ({wl.name}), fp64 oracle on "
+                                            f"{threads} host threads, {tc:.1f} s"}
+        # the same oracle on one host thread: a bounded prefix of the same problem, and the whole
+        # 1,000 x 16 training
+        k1 = int(max(10, rate / max(threads, 1) * args.cpu_seconds / 10))
         t1 = time.perf_counter()
-        r1 = oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=k1, cache_bytes=1 << 30, threads=1)
+        r1 = oracle.train(X, y, wl.C, wl.gamma, wl.tol, max_iter=k1, cache_bytes=cache, threads=1)
         t1c = time.perf_counter() - t1
         w0 = synth.workload(0)
         X0, y0, _, _ = synth.generate(0, m=1)

@@ -30,7 +30,7 @@ def test_more_than_one_gpu_is_refused(monkeypatch, capsys):
 
 @pytest.mark.gpu
 def test_bench_line_contract(monkeypatch, capsys, gpu_ok):
-    """A short run (one timed step of the 20,000 x 784 workload, no side legs) prints one JSON
+    """A short run (one timed step of the default 100,000 x 32 workload, no side legs) prints one JSON
     line carrying the contract's fields, a roofline whose fraction is achieved / peak, and the
     configuration named by its workload."""
     code, out, err = run_bench(monkeypatch, capsys, "--steps", "1", "--warmup", "0", "--cpu-seconds", "0", "--no-ovo",
