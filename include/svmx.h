@@ -23,7 +23,8 @@
  *    ordinary host memory.  X arrays are fp32, row-major [rows][d], rows contiguous.
  *  - The caller owns every buffer, including the device workspace, whose size is given by
  *    the matching *_workspace_bytes query.  The library keeps no state between calls
- *    except the loaded code object and a thread-local error message.
+ *    except the loaded code object, a thread-local error message, and (svm_train_static only)
+ *    its static device scratch and that scratch's address on each device.
  *  - All device work is enqueued on options->stream (a hipStream_t; NULL = the null stream).
  *    Every call returns only after its outputs are complete.
  *  - Negative status: nothing was written to the outputs that can be relied upon, nothing
@@ -155,6 +156,24 @@ int64_t svm_train_workspace_bytes(int64_t n, int64_t d, const svm_options *o);
 svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma, double tol,
                      double *alpha, double *b, void *workspace, int64_t workspace_bytes, const svm_options *o,
                      svm_stats *st);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): svm_train without a workspace argument.  Its device
+ * scratch is a library-owned static array of SVM_STATIC_SCRATCH_BYTES on each device the library
+ * runs on (held until the process ends); it calls no hipMalloc/hipFree and creates no HIP events
+ * (t_gram, t_solve, t_finalize and t_kernel of *st are reported as 0).  Arguments, outputs and
+ * results are those of svm_train with the same options, except that SVM_GRAM_AUTO takes the Gram
+ * only when the whole plan fits the scratch (else the row path).  SVM_EWORKSPACE when the plan
+ * does not fit: on the Gram path beyond n = 4,060 at 16 features (3,712 at 784); the row path
+ * needs about 16 bytes a sample, within the scratch up to its own limit of 1,048,576 samples.
+ * Every call on one device uses that device's one array and leaves the last call's
+ * contents in it (each call initialises what it reads): calls that overlap in time on one device
+ * race, and must not be made.
+ */
+#define SVM_STATIC_SCRATCH_BYTES (64LL * 1024 * 1024)
+svm_status svm_train_static(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma,
+                            double tol, double *alpha, double *b, const svm_options *o, svm_stats *st);
 
 /* Device workspace bytes svm_predict needs. */
 int64_t svm_predict_workspace_bytes(int64_t n, int64_t d, int64_t m);

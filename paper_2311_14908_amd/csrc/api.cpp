@@ -14,6 +14,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -184,6 +185,16 @@ struct Layout {
   }
 };
 
+// ---------------------------------------------------------------------------- static scratch
+// The device workspace of svm_train_static: one array per device, alive until the process ends.
+// Its name is a host-side stand-in in host code; the device address comes from
+// hipGetSymbolAddress, taken once per device (with that device current) and kept.
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+
+svm_status static_scratch(void **out);
+
 // ---------------------------------------------------------------------------- binary plan
 struct TrainPlan {
   bool gram;
@@ -257,20 +268,25 @@ uint64_t spin_ticks() {
   return (uint64_t)(SPIN_SECONDS * 1000.0 * (double)khz);
 }
 
+// A pair of HIP events on the launch stream; init(false) leaves it off (no events are created,
+// every record is a no-op and seconds() is 0), for the entry point that creates no resources.
 struct Timer {
   hipEvent_t a = nullptr, b = nullptr;
   ~Timer() {
     if (a) (void)hipEventDestroy(a);
     if (b) (void)hipEventDestroy(b);
   }
-  hipError_t init() {
+  hipError_t init(bool on = true) {
+    if (!on) return hipSuccess;
     hipError_t e = hipEventCreate(&a);
     if (e != hipSuccess) return e;
     return hipEventCreate(&b);
   }
+  hipError_t start(hipStream_t s) { return a ? hipEventRecord(a, s) : hipSuccess; }
+  hipError_t stop(hipStream_t s) { return b ? hipEventRecord(b, s) : hipSuccess; }
   double seconds() {
     float ms = 0.f;
-    if (hipEventElapsedTime(&ms, a, b) != hipSuccess) return 0.0;
+    if (!a || !b || hipEventElapsedTime(&ms, a, b) != hipSuccess) return 0.0;
     return ms * 1e-3;
   }
 };
@@ -279,22 +295,22 @@ struct Timer {
 // Returns SVM_OK or a negative status.
 template <class Launch>
 svm_status run_launches(Launch launch, int32_t *error, int32_t nprob, int32_t total_wg, Ctl *d_ctl, hipStream_t stream,
-                        int32_t *launches, std::vector<Ctl> &h, double *t_kernel) {
+                        int32_t *launches, std::vector<Ctl> &h, double *t_kernel, bool timed = true) {
   int32_t herr = 0;
   Timer tk;
-  HIPCHK(tk.init());
+  HIPCHK(tk.init(timed));
   *t_kernel = 0.0;
   h.assign(nprob, Ctl{});
   std::vector<int64_t> prev(nprob, -1);
   for (;;) {
     int32_t maxres = 0;
-    HIPCHK(hipEventRecord(tk.a, stream));
+    HIPCHK(tk.start(stream));
     hipError_t e = launch(&maxres);
     if (e == hipErrorCooperativeLaunchTooLarge)
       return fail(SVM_ENOMEM, "%d solver workgroups do not fit on the device at once (at most %d)", total_wg, maxres);
     if (e != hipSuccess) return fail(SVM_EDEVICE, "solver launch: %s", hipGetErrorString(e));
     ++*launches;
-    HIPCHK(hipEventRecord(tk.b, stream));
+    HIPCHK(tk.stop(stream));
     HIPCHK(hipMemcpyAsync(h.data(), d_ctl, sizeof(Ctl) * nprob, hipMemcpyDeviceToHost, stream));
     HIPCHK(hipMemcpyAsync(&herr, error, sizeof(herr), hipMemcpyDeviceToHost, stream));
     HIPCHK(hipStreamSynchronize(stream));
@@ -315,9 +331,10 @@ svm_status run_launches(Launch launch, int32_t *error, int32_t nprob, int32_t to
 }
 
 svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t per_thread, bool gram, Ctl *d_ctl,
-                      hipStream_t stream, int32_t *launches, std::vector<Ctl> &h, double *t_kernel) {
+                      hipStream_t stream, int32_t *launches, std::vector<Ctl> &h, double *t_kernel,
+                      bool timed = true) {
   return run_launches([&](int32_t *maxres) { return launch_solver(sp, total_wg, per_thread, gram, stream, maxres); },
-                      sp.error, nprob, total_wg, d_ctl, stream, launches, h, t_kernel);
+                      sp.error, nprob, total_wg, d_ctl, stream, launches, h, t_kernel, timed);
 }
 
 // EINVAL unless every value of X[0 .. count) is finite (a NaN or an infinity would leave no
@@ -464,6 +481,26 @@ hipError_t predict_prepare(PredictWs &w, const Opts &r, const float *Xtr, int64_
 
 }  // namespace
 
+static __device__ __align__(256) unsigned char scratch[SVM_STATIC_SCRATCH_BYTES];
+
+namespace {
+svm_status static_scratch(void **out) {
+  int dev = 0;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(SVM_EDEVICE, "device %d outside the scratch table", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(SVM_EDEVICE, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SVM_OK;
+}
+}  // namespace
+
 // ============================================================================ C ABI
 extern "C" {
 
@@ -485,9 +522,11 @@ int64_t svm_train_workspace_bytes(int64_t n, int64_t d, const svm_options *o) {
   return p.total;
 }
 
-svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma, double tol,
-                     double *alpha, double *b, void *workspace, int64_t workspace_bytes, const svm_options *o,
-                     svm_stats *st) {
+// Binary training.  static_ws: the workspace is the library's static device scratch (the
+// caller passes none); the plan must fit it, and no HIP events or other resources are created.
+static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma,
+                             double tol, double *alpha, double *b, void *workspace, int64_t workspace_bytes,
+                             const svm_options *o, svm_stats *st, bool static_ws) {
   const auto t_start = std::chrono::steady_clock::now();
   g_err.clear();
   if (!X || !y || !alpha || !b) return fail(SVM_EINVAL, "NULL pointer argument");
@@ -497,11 +536,31 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options (struct_size or gram mode)");
   if (r.trace_len > 0 && (int64_t)r.trace_len > r.max_iter + 1) r.trace_len = (int32_t)(r.max_iter + 1);
   TrainPlan p;
-  svm_status s0 = plan_train(n, d, r, &p);
-  if (s0 != SVM_OK) return s0;
-  if (!workspace || workspace_bytes < p.total)
-    return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)p.total,
-                (long long)workspace_bytes);
+  svm_status s0;
+  if (static_ws) {
+    // AUTO takes the Gram only when the whole plan fits the scratch, else the row path
+    Opts rs = r;
+    if (rs.gram == SVM_GRAM_AUTO) rs.gram_budget = std::min<int64_t>(rs.gram_budget, SVM_STATIC_SCRATCH_BYTES);
+    s0 = plan_train(n, d, rs, &p);
+    if (s0 == SVM_OK && r.gram == SVM_GRAM_AUTO && p.gram && p.total > SVM_STATIC_SCRATCH_BYTES) {
+      rs.gram = SVM_GRAM_OFF;
+      s0 = plan_train(n, d, rs, &p);
+    }
+    if (s0 != SVM_OK) return s0;
+    if (p.total > SVM_STATIC_SCRATCH_BYTES)
+      return fail(SVM_EWORKSPACE, "n=%lld, d=%lld needs %lld bytes of device scratch; svm_train_static has %lld",
+                  (long long)n, (long long)d, (long long)p.total, (long long)SVM_STATIC_SCRATCH_BYTES);
+    s0 = static_scratch(&workspace);
+    if (s0 != SVM_OK) return s0;
+    workspace_bytes = SVM_STATIC_SCRATCH_BYTES;
+  } else {
+    s0 = plan_train(n, d, r, &p);
+    if (s0 != SVM_OK) return s0;
+    if (!workspace || workspace_bytes < p.total)
+      return fail(SVM_EWORKSPACE, "workspace of %lld bytes needed, %lld given", (long long)p.total,
+                  (long long)workspace_bytes);
+  }
+  const bool timed = !static_ws;
   hipStream_t stream = r.stream;
   s0 = check_labels_pm1(y, n, stream);
   if (s0 != SVM_OK) return s0;
@@ -548,10 +607,10 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
   const double t_upload = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
 
   Timer tg, ts, tf;
-  HIPCHK(tg.init());
-  HIPCHK(ts.init());
-  HIPCHK(tf.init());
-  HIPCHK(hipEventRecord(tg.a, stream));
+  HIPCHK(tg.init(timed));
+  HIPCHK(ts.init(timed));
+  HIPCHK(tf.init(timed));
+  HIPCHK(tg.start(stream));
   double *sqn = p.gram ? nullptr : reinterpret_cast<double *>(ws + p.off_sqn);
   if (p.gram && p.off_split >= 0)
     HIPCHK(launch_gram_split(X, n, d, (float)gamma, G, p.ld, ws + p.off_split, stream));
@@ -561,9 +620,9 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     HIPCHK(launch_split_rows(X, n, d, split_views(ws + p.off_split, n, d), stream));
   else
     HIPCHK(launch_row_norms(X, n, d, sqn, stream));
-  HIPCHK(hipEventRecord(tg.b, stream));
+  HIPCHK(tg.stop(stream));
 
-  HIPCHK(hipEventRecord(ts.a, stream));
+  HIPCHK(ts.start(stream));
   HIPCHK(launch_solver_init(dprob, 1, n, stream));
   SolveParams sp{};
   sp.probs = dprob;
@@ -613,16 +672,16 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     }
     const int32_t nwg = p.shape.nwg + (p.shape.nwg > 1 ? 1 : 0);  // owners and the solving workgroup
     s1 = run_launches([&](int32_t *maxres) { return launch_ws_solver(wp, nwg, stream, maxres); }, err, 1, nwg, ctl,
-                      stream, &launches, hc, &t_kernel);
+                      stream, &launches, hc, &t_kernel, timed);
   } else {
-    s1 = run_solver(sp, 1, p.shape.nwg, p.shape.per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel);
+    s1 = run_solver(sp, 1, p.shape.nwg, p.shape.per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel, timed);
   }
   if (s1 != SVM_OK) return s1;
   int64_t h_rounds = 0;
   HIPCHK(hipMemcpyAsync(&h_rounds, d_rounds, 8, hipMemcpyDeviceToHost, stream));
-  HIPCHK(hipEventRecord(ts.b, stream));
+  HIPCHK(ts.stop(stream));
 
-  HIPCHK(hipEventRecord(tf.a, stream));
+  HIPCHK(tf.start(stream));
   HIPCHK(launch_finalize(dprob, 1, C, fin, stream));
   double hfin[4];
   HIPCHK(hipMemcpyAsync(hfin, fin, sizeof(hfin), hipMemcpyDeviceToHost, stream));
@@ -633,7 +692,7 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     if (r.trace_b) HIPCHK(hipMemcpyAsync(r.trace_b, tb, 8 * 2 * steps, hipMemcpyDeviceToHost, stream));
   }
   if (r.f_out) HIPCHK(hipMemcpyAsync(r.f_out, f, 8 * n, hipMemcpyDeviceToDevice, stream));
-  HIPCHK(hipEventRecord(tf.b, stream));
+  HIPCHK(tf.stop(stream));
   HIPCHK(hipStreamSynchronize(stream));
 
   const Ctl &c = hc[0];
@@ -658,6 +717,17 @@ svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, dou
     st->t_upload = t_upload;
   }
   return c.status == ST_MAXITER ? SVM_NOT_CONVERGED : SVM_OK;
+}
+
+svm_status svm_train(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma, double tol,
+                     double *alpha, double *b, void *workspace, int64_t workspace_bytes, const svm_options *o,
+                     svm_stats *st) {
+  return train_impl(X, y, n, d, C, gamma, tol, alpha, b, workspace, workspace_bytes, o, st, false);
+}
+
+svm_status svm_train_static(const float *X, const int32_t *y, int64_t n, int64_t d, double C, double gamma,
+                            double tol, double *alpha, double *b, const svm_options *o, svm_stats *st) {
+  return train_impl(X, y, n, d, C, gamma, tol, alpha, b, nullptr, 0, o, st, true);
 }
 
 int64_t svm_predict_workspace_bytes(int64_t n, int64_t d, int64_t m) {
@@ -840,7 +910,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   HIPCHK(tg.init());
   HIPCHK(ts.init());
   HIPCHK(tf.init());
-  HIPCHK(hipEventRecord(tg.a, stream));
+  HIPCHK(tg.start(stream));
   double *sqn = p.gram ? nullptr : reinterpret_cast<double *>(ws + p.off_sqn);
   if (p.gram && p.off_split >= 0)
     HIPCHK(launch_gram_split(Xs, n, d, (float)gamma, G, p.ld, ws + p.off_split, stream));
@@ -848,8 +918,8 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
     HIPCHK(launch_gram(Xs, n, d, (float)gamma, G, p.ld, stream));
   else
     HIPCHK(launch_row_norms(Xs, n, d, sqn, stream));
-  HIPCHK(hipEventRecord(tg.b, stream));
-  HIPCHK(hipEventRecord(ts.a, stream));
+  HIPCHK(tg.stop(stream));
+  HIPCHK(ts.start(stream));
   HIPCHK(launch_solver_init(dprob, p.P, max_n, stream));
   SolveParams sp{};
   sp.probs = dprob;
@@ -886,12 +956,12 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
     hc.insert(hc.end(), hb.begin(), hb.end());
     woff += bwg[bi];
   }
-  HIPCHK(hipEventRecord(ts.b, stream));
-  HIPCHK(hipEventRecord(tf.a, stream));
+  HIPCHK(ts.stop(stream));
+  HIPCHK(tf.start(stream));
   HIPCHK(launch_finalize(dprob, p.P, C, fin, stream));
   std::vector<double> hfin(4 * (size_t)p.P);
   HIPCHK(hipMemcpyAsync(hfin.data(), fin, 8 * hfin.size(), hipMemcpyDeviceToHost, stream));
-  HIPCHK(hipEventRecord(tf.b, stream));
+  HIPCHK(tf.stop(stream));
   HIPCHK(hipStreamSynchronize(stream));
   bool maxed = false;
   const double t_total = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();

@@ -49,7 +49,8 @@ class svm_stats(C.Structure):
         return {name: getattr(self, name) for name, _ in self._fields_}
 
 
-EXPORTS = ("svm_default_options", "svm_train_workspace_bytes", "svm_train", "svm_predict_workspace_bytes",
+EXPORTS = ("svm_default_options", "svm_train_workspace_bytes", "svm_train", "svm_train_static",
+           "svm_predict_workspace_bytes",
            "svm_predict", "svm_train_ovo_workspace_bytes", "svm_train_ovo", "svm_predict_ovo_workspace_bytes",
            "svm_predict_ovo", "svm_kernel_rows", "svm_gram_workspace_bytes", "svm_gram", "svm_last_error")
 
@@ -71,6 +72,7 @@ def load(path: str | None = None):
         "svm_default_options": (None, [OP]),
         "svm_train_workspace_bytes": (I64, [I64, I64, OP]),
         "svm_train": (C.c_int, [V, V, I64, I64, D, D, D, V, C.POINTER(D), V, I64, OP, ST]),
+        "svm_train_static": (C.c_int, [V, V, I64, I64, D, D, D, V, C.POINTER(D), OP, ST]),
         "svm_predict_workspace_bytes": (I64, [I64, I64, I64]),
         "svm_predict": (C.c_int, [V, V, V, D, I64, I64, D, V, I64, V, V, I64, OP]),
         "svm_train_ovo_workspace_bytes": (I64, [I64, I64, I32, OP]),
@@ -164,6 +166,39 @@ def svm_train(X: torch.Tensor, y: torch.Tensor, C_: float, gamma: float, tol: fl
     st = svm_stats()
     status = _check(lib.svm_train(_ptr(X), _ptr(y), n, d, float(C_), float(gamma), float(tol), _ptr(alpha), C.byref(b),
                                   _ptr(ws), wsb, C.byref(o), C.byref(st)), ok=(SVM_OK, SVM_NOT_CONVERGED))
+    out = TrainOut(alpha=alpha, b=b.value, status=status, stats=st.as_dict())
+    if tl:
+        steps = min(tl, (st.rounds if o.working_set else st.iterations) + 1)
+        out.trace_ul = tws[:2 * steps].reshape(steps, 2).copy()
+        out.trace_b = tb[:2 * steps].reshape(steps, 2).copy()
+    return out
+
+
+STATIC_SCRATCH_BYTES = 64 * 1024 * 1024
+
+
+def svm_train_static(X: torch.Tensor, y: torch.Tensor, C_: float, gamma: float, tol: float, *,
+                     alpha: torch.Tensor | None = None, **opt) -> TrainOut:
+    """svm_train on the library's static device scratch (no workspace).  ``alpha`` may be given
+    (a device fp64 [n] tensor) so that the call itself allocates nothing."""
+    lib = load()
+    _dev(X, torch.float32, "X")
+    _dev(y, torch.int32, "y")
+    n, d = X.shape
+    o = options(**opt)
+    tl = int(o.trace_len)
+    tws = np.full(2 * max(tl, 1), -1, dtype=np.int32)
+    tb = np.full(2 * max(tl, 1), np.nan, dtype=np.float64)
+    if tl:
+        o.trace_ws = tws.ctypes.data_as(C.POINTER(C.c_int32))
+        o.trace_b = tb.ctypes.data_as(C.POINTER(C.c_double))
+    if alpha is None:
+        alpha = torch.empty(n, dtype=torch.float64, device=X.device)
+    _dev(alpha, torch.float64, "alpha")
+    b = C.c_double(0.0)
+    st = svm_stats()
+    status = _check(lib.svm_train_static(_ptr(X), _ptr(y), n, d, float(C_), float(gamma), float(tol), _ptr(alpha),
+                                         C.byref(b), C.byref(o), C.byref(st)), ok=(SVM_OK, SVM_NOT_CONVERGED))
     out = TrainOut(alpha=alpha, b=b.value, status=status, stats=st.as_dict())
     if tl:
         steps = min(tl, (st.rounds if o.working_set else st.iterations) + 1)
