@@ -49,7 +49,8 @@ def _load():
         lib.oracle_kernel_rows.argtypes = [P, C.c_int64, C.c_int64, P, C.c_int64, C.c_int, C.c_double, P, C.c_int]
         lib.oracle_train.restype = C.c_int
         lib.oracle_train.argtypes = [P, P, C.c_int64, C.c_int64, C.c_int, C.c_double, C.c_double, C.c_double,
-                                     C.c_int64, C.c_int64, C.c_int, P, P, C.POINTER(_Res), C.c_int64, P, P, P]
+                                     C.c_int64, C.c_int64, C.c_int, P, P, C.POINTER(_Res), C.c_int64, P, P, P,
+                                     C.c_int]
         lib.oracle_decision.restype = None
         lib.oracle_decision.argtypes = [P, P, P, C.c_double, C.c_int64, C.c_int64, C.c_int, C.c_double, P,
                                         C.c_int64, P, C.c_int]
@@ -97,9 +98,13 @@ class TrainResult:
     trace_gap: np.ndarray | None = None  # [steps, 2] runner-up gaps of the two scans
 
 
+MVP, SECOND_ORDER = 0, 1
+
+
 def train(X, y, C_, gamma, tol, *, kind=RBF, max_iter=None, cache_bytes=8 << 30, threads=None,
-          trace_len=0, want_f=False) -> TrainResult:
-    """Binary SMO with maximal-violating-pair selection (paper, Section III.B)."""
+          trace_len=0, want_f=False, selection=MVP) -> TrainResult:
+    """Binary SMO (paper, Section III.B): maximal-violating-pair selection, or with
+    ``selection=SECOND_ORDER`` the second-order rule for the second index of the pair."""
     lib = _load()
     X = _f32(X)
     y = np.ascontiguousarray(y, dtype=np.int32)
@@ -116,7 +121,7 @@ def train(X, y, C_, gamma, tol, *, kind=RBF, max_iter=None, cache_bytes=8 << 30,
     tg = np.full((max(tl, 1), 2), np.nan, dtype=np.float64)
     rc = lib.oracle_train(_p(X), _p(y), n, d, int(kind), float(C_), float(gamma), float(tol), int(max_iter),
                           int(cache_bytes), threads, _p(alpha), _p(f) if f is not None else None, C.byref(res), tl,
-                          _p(tul), _p(tb), _p(tg))
+                          _p(tul), _p(tb), _p(tg), int(selection))
     if rc < 0:
         raise ValueError(f"oracle_train rejected its input (status {rc})")
     steps = min(tl, int(res.iterations) + 1) if tl else 0

@@ -26,6 +26,7 @@
  *   I_up        {i : (y_i=+1 and a_i<C) or (y_i=-1 and a_i>0)}
  *   I_low       {i : (y_i=+1 and a_i>0) or (y_i=-1 and a_i<C)}
  *   selection   u = argmin_{I_up} f, l = argmax_{I_low} f; ties go to the smaller index
+ *               (or, on request, the second-order rule for l: see oracle_train)
  *   stop        b_low - b_up <= tol
  *   eta         K_uu + K_ll - 2 K_ul, replaced by 1e-12 when <= 0
  *   clipping    box [L,H] on a_l, partner clamped to [0,C], values within 1e-12*C of a
@@ -154,12 +155,22 @@ static double clampd(double v, double lo, double hi) { return v < lo ? lo : (v >
  * Binary SMO training (Section III.B).  Outputs alpha[n]; f[n] if non-NULL; the
  * result summary; and, for the first trace_len steps, the selected pair (u,l), the
  * selection values (b_up,b_low) and the runner-up gaps of both scans.
+ *
+ * The paper cites two working-pair rules (Section III.B).  selection = 0 takes the maximal
+ * violating pair above.  selection = 1 takes the second-order rule for the second index:
+ * u as above; l maximises the decrease of the objective that the unclipped two-variable step
+ * on (u, t) would give, (f_t - f_u)^2 / a_ut with a_ut = K_uu + K_tt - 2 K_ut (1e-12 when
+ * <= 0), over the members t of I_low with f_t > f_u, ties to the smaller index.  The stop
+ * rule is the same for both (b_low the largest f over I_low), and so is the step on (u, l).
+ * For selection = 1 the second runner-up gap is relative: (g_best - g_second) / g_best.
  */
 int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kind, double C, double gamma,
                  double tol, int64_t max_iter, int64_t cache_bytes, int threads, double *alpha, double *f_out,
-                 oracle_result *res, int64_t trace_len, int32_t *trace_ul, double *trace_b, double *trace_gap) {
+                 oracle_result *res, int64_t trace_len, int32_t *trace_ul, double *trace_b, double *trace_gap,
+                 int selection) {
   memset(res, 0, sizeof(*res));
-  if (!X || !y || !alpha || n < 2 || d < 1 || !(C > 0) || !(tol > 0) || (kind == ORACLE_RBF && !(gamma > 0))) {
+  if (!X || !y || !alpha || n < 2 || d < 1 || !(C > 0) || !(tol > 0) || (kind == ORACLE_RBF && !(gamma > 0)) ||
+      selection < 0 || selection > 1) {
     res->status = -1;
     return -1;
   }
@@ -174,7 +185,11 @@ int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kin
   krows kr;
   if (krows_init(&kr, X, n, d, kind, gamma, cache_bytes, threads)) { krows_free(&kr); res->status = -2; return -2; }
   double *f = (double *)malloc((size_t)n * sizeof(double));
-  if (!f) { krows_free(&kr); res->status = -2; return -2; }
+  /* K_tt of every sample, for the second-order rule */
+  double *diag = selection == 1 ? (double *)malloc((size_t)n * sizeof(double)) : NULL;
+  if (!f || (selection == 1 && !diag)) { free(f); free(diag); krows_free(&kr); res->status = -2; return -2; }
+  if (diag)
+    for (int64_t i = 0; i < n; ++i) diag[i] = oracle_kernel_value(X + i * d, X + i * d, d, kind, gamma);
 
   /* Initial point: a = 0, so f_i = -y_i. */
   for (int64_t i = 0; i < n; ++i) { alpha[i] = 0.0; f[i] = -(double)y[i]; }
@@ -198,20 +213,40 @@ int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kin
     if (u < 0 || l < 0) { status = 0; break; }
     b_up = f[u];
     b_low = f[l];
+    double gap_l = l2 >= 0 ? b_low - f[l2] : INFINITY;
+    /* KKT conditions hold to within tol: stop. */
+    const int stop = b_low - b_up <= tol;
+    const double *Ku = NULL;
+    if (!stop && t < max_iter && selection == 1) {
+      /* second-order choice of l among the members of I_low above f_u */
+      Ku = krows_get(&kr, u);
+      double g1 = -1.0, g2 = -1.0;
+      int64_t l1 = -1;
+      for (int64_t i = 0; i < n; ++i) {
+        if (!in_low(y[i], alpha[i], C) || !(f[i] > b_up)) continue;
+        const double bt = f[i] - b_up;
+        double at = Ku[u] + diag[i] - 2.0 * Ku[i];
+        if (at <= 0.0) at = 1e-12;
+        const double g = bt * bt / at;
+        if (g > g1) { g2 = g1; g1 = g; l1 = i; }
+        else if (g > g2) g2 = g;
+      }
+      l = l1;
+      gap_l = g2 >= 0.0 ? (g1 - g2) / g1 : INFINITY;
+    }
     if (t < trace_len) {
       if (trace_ul) { trace_ul[2 * t] = (int32_t)u; trace_ul[2 * t + 1] = (int32_t)l; }
       if (trace_b) { trace_b[2 * t] = b_up; trace_b[2 * t + 1] = b_low; }
       if (trace_gap) {
         trace_gap[2 * t] = u2 >= 0 ? f[u2] - b_up : INFINITY;
-        trace_gap[2 * t + 1] = l2 >= 0 ? b_low - f[l2] : INFINITY;
+        trace_gap[2 * t + 1] = gap_l;
       }
     }
-    /* KKT conditions hold to within tol: stop. */
-    if (b_low - b_up <= tol) { status = 0; break; }
+    if (stop) { status = 0; break; }
     if (t >= max_iter) { status = 1; break; }
 
     /* Two-variable sub-problem on (u, l). */
-    const double *Ku = krows_get(&kr, u);
+    if (!Ku) Ku = krows_get(&kr, u);
     const double *Kl = krows_get(&kr, l);
     double eta = Ku[u] + Kl[l] - 2.0 * Ku[l];
     if (eta <= 0.0) eta = 1e-12;
@@ -221,7 +256,7 @@ int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kin
     double L, H;
     if (s < 0) { L = fmax(0.0, al - au); H = fmin(C, C + al - au); }
     else { L = fmax(0.0, au + al - C); H = fmin(C, au + al); }
-    double al_new = clampd(al + yl * (b_up - b_low) / eta, L, H);
+    double al_new = clampd(al + yl * (b_up - f[l]) / eta, L, H);
     double au_new = clampd(au + s * (al - al_new), 0.0, C);
     const double snap = 1e-12 * C;
     if (fabs(al_new) <= snap) al_new = 0.0;
@@ -252,6 +287,7 @@ int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kin
   res->dual_obj = 0.5 * sa - 0.5 * saf;
   if (f_out) memcpy(f_out, f, (size_t)n * sizeof(double));
   free(f);
+  free(diag);
   krows_free(&kr);
   return status;
 }

@@ -22,7 +22,8 @@ void oracle_kernel_rows(const float *X, int64_t n, int64_t d, const int64_t *row
                         double gamma, double *out, int threads);
 int oracle_train(const float *X, const int32_t *y, int64_t n, int64_t d, int kind, double C, double gamma,
                  double tol, int64_t max_iter, int64_t cache_bytes, int threads, double *alpha, double *f_out,
-                 oracle_result *res, int64_t trace_len, int32_t *trace_ul, double *trace_b, double *trace_gap);
+                 oracle_result *res, int64_t trace_len, int32_t *trace_ul, double *trace_b, double *trace_gap,
+                 int selection);
 int oracle_train_ws(const float *X, const int32_t *y, int64_t n, int64_t d, int kind, double C, double gamma,
                     double tol, int64_t q, double frac, int64_t max_inner, int64_t max_iter, int64_t cache_bytes,
                     int threads, double *alpha, double *f_out, oracle_result *res, int64_t *rounds_out,
@@ -64,16 +65,19 @@ static int run(int64_t n, int64_t d, int64_t cache_bytes, int threads) {
   int32_t *tul = malloc(sizeof(int32_t) * 2 * tl);
   double *tb = malloc(sizeof(double) * 2 * tl), *tg = malloc(sizeof(double) * 2 * tl);
   oracle_result r;
-  for (int kind = 0; kind < 2; ++kind) {
-    int st = oracle_train(X, y, n, d, kind, 1.0, 0.5, 1e-3, 100000, cache_bytes, threads, alpha, f, &r, tl, tul, tb,
-                          tg);
-    CHECK(st == 0 && r.iterations > 0);
-  }
+  for (int kind = 0; kind < 2; ++kind)
+    for (int sel = 0; sel < 2; ++sel) {
+      int st = oracle_train(X, y, n, d, kind, 1.0, 0.5, 1e-3, 100000, cache_bytes, threads, alpha, f, &r, tl, tul, tb,
+                            tg, sel);
+      CHECK(st == 0 && r.iterations > 0);
+    }
   /* a step limit, and invalid input */
   CHECK(oracle_train(X, y, n, d, 0, 1.0, 0.5, 1e-6, 3, cache_bytes, threads, alpha, NULL, &r, 0, NULL, NULL,
-                     NULL) == 1);
+                     NULL, 1) == 1);
   CHECK(oracle_train(X, y, n, d, 0, -1.0, 0.5, 1e-3, 10, cache_bytes, threads, alpha, NULL, &r, 0, NULL, NULL,
-                     NULL) == -1);
+                     NULL, 0) == -1);
+  CHECK(oracle_train(X, y, n, d, 0, 1.0, 0.5, 1e-3, 10, cache_bytes, threads, alpha, NULL, &r, 0, NULL, NULL,
+                     NULL, 2) == -1);
 
   /* working-set rounds: q = 2, a middle size, and q larger than n */
   const int64_t qs[3] = {2, 8, 2 * n + 2};
