@@ -71,6 +71,17 @@ typedef enum {
   SVM_MFMA_F32 = 1        /* fp32 inputs on v_mfma_f32_16x16x4f32 */
 } svm_gram_mfma;
 
+/* How the working pair of each step is chosen (the paper cites two rules, Section III.B). */
+typedef enum {
+  SVM_SELECT_MVP = 0,         /* maximal violating pair: u = argmin_{I_up} f, l = argmax_{I_low} f */
+  SVM_SELECT_SECOND_ORDER = 1 /* u as above; l = the member t of I_low with f_t > f_u that maximises
+                                 (f_t - f_u)^2 / a_ut, a_ut = K_uu + K_tt - 2 K_ut (1e-12 when not
+                                 positive), ties to the smaller index: the decrease of the objective
+                                 the unclipped step on (u, t) would give.  The stop rule is unchanged
+                                 (b_low = max_{I_low} f).  Gram path only (each step reads row u
+                                 before l is known); not with working_set */
+} svm_selection;
+
 typedef struct {
   int32_t struct_size;       /* = sizeof(svm_options); set by svm_default_options */
   int32_t gram;              /* svm_gram_mode */
@@ -105,6 +116,8 @@ typedef struct {
                                 slice), read from there instead of from HBM at every step; 0 = as
                                 many as fit, -1 = none, k > 0 = at most k.  Results do not depend
                                 on it. */
+  int32_t selection;         /* svm_selection (binary and one-vs-one training) */
+  int32_t reserved;          /* must be 0 */
 } svm_options;
 
 typedef struct {

@@ -73,6 +73,7 @@ struct Opts {
   int32_t gram_mfma;
   int32_t working_set;
   int32_t resident_rows;
+  int32_t selection;
 };
 
 bool resolve(const svm_options *o, int64_t n, Opts *r) {
@@ -95,6 +96,9 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
   r->gram_mfma = o->gram_mfma;
   r->working_set = o->working_set;
   r->resident_rows = o->resident_rows;
+  r->selection = o->selection;
+  if (o->reserved != 0 || (r->selection != SVM_SELECT_MVP && r->selection != SVM_SELECT_SECOND_ORDER)) return false;
+  if (r->selection == SVM_SELECT_SECOND_ORDER && r->working_set != 0) return false;
   const bool ws_ok = r->working_set == 0 ||
                      (r->working_set >= 2 && r->working_set <= ws_q_max() && r->working_set % 2 == 0);
   return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF && r->levels >= 0 && r->levels <= 2 &&
@@ -220,6 +224,9 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   else
     p->gram = gram_bytes <= (double)o.gram_budget;
   if (p->gram && gram_bytes > 9.0e18) return fail(SVM_EINVAL, "the Gram's n^2 size overflows 64-bit byte counts");
+  if (o.selection == SVM_SELECT_SECOND_ORDER && !p->gram)
+    return fail(SVM_EINVAL, "second-order selection needs the Gram path (the Gram does not fit gram_budget_bytes, "
+                            "or gram = SVM_GRAM_OFF)");
   if (o.working_set > 0) {
     if (!choose_ws_shape(n, o.workgroups, o.working_set, p->gram, &p->shape))
       return fail(SVM_ENOMEM, "n=%lld exceeds the working-set solver's %d workgroups of %d samples", (long long)n,
@@ -389,6 +396,8 @@ svm_status plan_ovo(int64_t n, int64_t d, int32_t k, const Opts &o, OvoPlan *p) 
   p->ld = round_up(n, 64);
   const double gram_bytes = 4.0 * (double)n * (double)p->ld;
   p->gram = o.gram == SVM_GRAM_ON || (o.gram == SVM_GRAM_AUTO && gram_bytes <= (double)o.gram_budget);
+  if (o.selection == SVM_SELECT_SECOND_ORDER && !p->gram)
+    return fail(SVM_EINVAL, "second-order selection needs the Gram path");
   Layout L;
   p->off_perm = L.add(4 * n);
   p->off_xs = L.add(4 * n * d);
@@ -641,6 +650,7 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
   sp.cache_tags = p.cache_cap ? reinterpret_cast<int32_t *>(ws + p.off_tags) : nullptr;
   sp.cache_cap = p.cache_cap;
   sp.max_per_wg = p.shape.per_wg;
+  sp.second_order = r.selection == SVM_SELECT_SECOND_ORDER ? 1 : 0;
   sp.res_rows = 0;
   if (!p.gram && r.working_set == 0 && r.resident_rows >= 0) {
     const int64_t fit = solver_res_rows_max(sp, p.shape.per_thread);
@@ -935,6 +945,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
   sp.sqn = sqn;
   sp.d = d;
   sp.max_per_wg = max_per_wg;
+  sp.second_order = r.selection == SVM_SELECT_SECOND_ORDER ? 1 : 0;
   sp.spin_limit = spin_ticks();
   sp.error = err;
   int32_t launches = 0;

@@ -70,43 +70,100 @@ __device__ __forceinline__ Sel sel_wave(const Sel &mine) {
   return r;
 }
 
+// Candidate of the second-order choice of l (used with p.second_order): the largest gain
+// g = (f_t - b_up)^2 / a_ut over the members t of I_low above b_up (ties to the smaller index),
+// with f, multiplier, label and K(u, t) of that sample.
+struct Sel2 {
+  double g, fl, al, kul;
+  int il, yl;
+};
+
+__device__ __forceinline__ void rec_init(Sel &s) { sel_init(s); }
+__device__ __forceinline__ void rec_init(Sel2 &s) {
+  s.g = -INFINITY; s.fl = 0.0; s.al = 0.0; s.kul = 0.0; s.il = IBIG; s.yl = 0;
+}
+__device__ __forceinline__ void rec_merge(Sel &s, const Sel &o) { sel_merge(s, o); }
+__device__ __forceinline__ void rec_merge(Sel2 &s, const Sel2 &o) {
+  if (gt_max(o.g, o.il, s.g, s.il)) s = o;
+}
+__device__ __forceinline__ Sel rec_wave(const Sel &mine) { return sel_wave(mine); }
+__device__ __forceinline__ Sel2 rec_wave(const Sel2 &mine) {
+  const int lane = winner_lane<true>(mine.g, mine.il);
+  Sel2 r;
+  r.g = readlane_d(mine.g, lane);
+  r.fl = readlane_d(mine.fl, lane);
+  r.al = readlane_d(mine.al, lane);
+  r.kul = readlane_d(mine.kul, lane);
+  r.il = __builtin_amdgcn_readlane(mine.il, lane);
+  r.yl = __builtin_amdgcn_readlane(mine.yl, lane);
+  return r;
+}
+
 // LDS hand-off between the waves of a workgroup.  Two buffers used alternately, so one
 // barrier per hand-off suffices: a buffer is rewritten only after another hand-off's barrier.
-template <int NW>
-struct SelLds {
-  Sel slot[2][NW];
+template <class R, int NW>
+struct RecLds {
+  R slot[2][NW];
 };
 
 // Combine the wave results of all waves; every thread returns the same workgroup result.
-template <int NW>
-__device__ __forceinline__ Sel sel_block(const Sel &wave_res, SelLds<NW> &L, int &buf) {
+template <class R, int NW>
+__device__ __forceinline__ R rec_block(const R &wave_res, RecLds<R, NW> &L, int &buf) {
   if ((threadIdx.x & 63) == 0) L.slot[buf][threadIdx.x >> 6] = wave_res;
   __syncthreads();
-  Sel r = L.slot[buf][0];
+  R r = L.slot[buf][0];
 #pragma unroll
-  for (int q = 1; q < NW; ++q) sel_merge(r, L.slot[buf][q]);
+  for (int q = 1; q < NW; ++q) rec_merge(r, L.slot[buf][q]);
   buf ^= 1;
   return r;
 }
 
 __device__ __forceinline__ unsigned pack_index(int i, int y) { return (unsigned)i | (y < 0 ? 0x80000000u : 0u); }
+__device__ __forceinline__ void unpack_index(unsigned w, int &i, int &y) {
+  i = (int)(w & 0x7fffffffu);
+  y = (w >> 31) ? -1 : 1;
+}
 
 // Limbs of a record (xchg_record.hpp): v_up, a_up, index words, v_low, a_low; the label travels
 // in bit 31 of the index word.
-__device__ __forceinline__ void sel_limbs(const Sel &s, u64 (&L)[5]) {
+__device__ __forceinline__ void rec_limbs_of(const Sel &s, u64 (&L)[5]) {
   L[0] = (u64)__double_as_longlong(s.vu);
   L[1] = (u64)__double_as_longlong(s.au);
   L[2] = (u64)pack_index(s.iu, s.yu) | ((u64)pack_index(s.il, s.yl) << 32);
   L[3] = (u64)__double_as_longlong(s.vl);
   L[4] = (u64)__double_as_longlong(s.al);
 }
+__device__ __forceinline__ void rec_from_limbs(const u64 (&L)[5], Sel &o) {
+  o.vu = __longlong_as_double((long long)L[0]);
+  o.au = __longlong_as_double((long long)L[1]);
+  unpack_index((unsigned)L[2], o.iu, o.yu);
+  unpack_index((unsigned)(L[2] >> 32), o.il, o.yl);
+  o.vl = __longlong_as_double((long long)L[3]);
+  o.al = __longlong_as_double((long long)L[4]);
+}
+// Second-order record: gain, f_l, index word, a_l, K(u, l).
+__device__ __forceinline__ void rec_limbs_of(const Sel2 &s, u64 (&L)[5]) {
+  L[0] = (u64)__double_as_longlong(s.g);
+  L[1] = (u64)__double_as_longlong(s.fl);
+  L[2] = (u64)pack_index(s.il, s.yl);
+  L[3] = (u64)__double_as_longlong(s.al);
+  L[4] = (u64)__double_as_longlong(s.kul);
+}
+__device__ __forceinline__ void rec_from_limbs(const u64 (&L)[5], Sel2 &o) {
+  o.g = __longlong_as_double((long long)L[0]);
+  o.fl = __longlong_as_double((long long)L[1]);
+  unpack_index((unsigned)L[2], o.il, o.yl);
+  o.al = __longlong_as_double((long long)L[3]);
+  o.kul = __longlong_as_double((long long)L[4]);
+}
 
 // Lanes 0..REC_WORDS-1 of the calling wave each write one word of the record.
-__device__ __forceinline__ void put_record(u64 *rec, unsigned stamp, const Sel &s) {
+template <class R>
+__device__ __forceinline__ void put_record(u64 *rec, unsigned stamp, const R &s) {
   const int t = threadIdx.x & 63;
   if (t < REC_WORDS) {
     u64 L[5];
-    sel_limbs(s, L);
+    rec_limbs_of(s, L);
     st_word(rec + t, rec_word(L, t, stamp));
   }
 }
@@ -114,10 +171,11 @@ __device__ __forceinline__ void put_record(u64 *rec, unsigned stamp, const Sel &
 // Wave-level: wait for records q0 + lane, q0 + lane + stride, ... below q1 of `words` to carry
 // `stamp`, reduce them, and return the result to every lane of the wave (all 64 lanes must
 // call).
-__device__ Sel poll_reduce(const u64 *words, int q0, int q1, int stride, unsigned stamp, uint64_t spin_limit,
-                           int32_t *err, int *abort_flag) {
-  Sel s;
-  sel_init(s);
+template <class R>
+__device__ R poll_reduce(const u64 *words, int q0, int q1, int stride, unsigned stamp, uint64_t spin_limit,
+                         int32_t *err, int *abort_flag) {
+  R s;
+  rec_init(s);
   for (int q = q0 + (int)(threadIdx.x & 63); q < q1; q += stride) {
     const u64 *rec = words + (size_t)q * SLOT_WORDS;
     u64 w[REC_WORDS];
@@ -138,28 +196,21 @@ __device__ Sel poll_reduce(const u64 *words, int q0, int q1, int stride, unsigne
     }
     u64 L[5];
     rec_limbs(w, L);
-    Sel o;
-    o.vu = __longlong_as_double((long long)L[0]);
-    o.au = __longlong_as_double((long long)L[1]);
-    o.iu = (int)((unsigned)L[2] & 0x7fffffffu);
-    o.yu = ((unsigned)L[2] >> 31) ? -1 : 1;
-    o.il = (int)((unsigned)(L[2] >> 32) & 0x7fffffffu);
-    o.yl = ((unsigned)(L[2] >> 32) >> 31) ? -1 : 1;
-    o.vl = __longlong_as_double((long long)L[3]);
-    o.al = __longlong_as_double((long long)L[4]);
-    sel_merge(s, o);
+    R o;
+    rec_from_limbs(L, o);
+    rec_merge(s, o);
   }
-  return sel_wave(s);
+  return rec_wave(s);
 }
 
-// Exchange of the workgroup selections of one problem (see file comment, item 2).  Wave 0
+// Exchange of the workgroup results of one problem (see file comment, item 2).  Wave 0
 // publishes the record.  With one level, the records are polled by as many waves as needed
 // for one record per lane (wave w takes records w*64 + lane, then every 64*pollers-th), each
 // wave reduces its share, and the shares meet in LDS.  With two levels, wave 0 does the
-// global-memory work of both levels.
-template <int NW>
-__device__ Sel exchange(const Prob &P, int rank, unsigned stamp, const Sel &mine, SelLds<NW> &L, int &buf,
-                        uint64_t spin_limit, int32_t *err, int *abort_flag) {
+// global-memory work of both levels.  The stamp's parity selects the buffer.
+template <class R, int NW>
+__device__ R exchange(const Prob &P, int rank, unsigned stamp, const R &mine, RecLds<R, NW> &L, int &buf,
+                      uint64_t spin_limit, int32_t *err, int *abort_flag) {
   const size_t par = stamp & 1u;
   u64 *lv1 = P.slots + par * (size_t)P.nwg * SLOT_WORDS;
   const int wave = threadIdx.x >> 6;
@@ -171,22 +222,22 @@ __device__ Sel exchange(const Prob &P, int rank, unsigned stamp, const Sel &mine
       const int g = rank / P.g1;
       if (rank % P.g1 == 0) {
         const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
-        const Sel gs = poll_reduce(lv1, q0, q1, 64, stamp, spin_limit, err, abort_flag);
+        const R gs = poll_reduce<R>(lv1, q0, q1, 64, stamp, spin_limit, err, abort_flag);
         put_record(lv2 + (size_t)g * SLOT_WORDS, stamp, gs);
       }
-      const Sel s = poll_reduce(lv2, 0, P.ng, 64, stamp, spin_limit, err, abort_flag);
+      const R s = poll_reduce<R>(lv2, 0, P.ng, 64, stamp, spin_limit, err, abort_flag);
       if (threadIdx.x == 0) L.slot[buf][0] = s;
     }
   } else {
     pollers = min(NW, (P.nwg + 63) >> 6);
     if (wave < pollers) {
-      const Sel s = poll_reduce(lv1, wave * 64, P.nwg, 64 * pollers, stamp, spin_limit, err, abort_flag);
+      const R s = poll_reduce<R>(lv1, wave * 64, P.nwg, 64 * pollers, stamp, spin_limit, err, abort_flag);
       if ((threadIdx.x & 63) == 0) L.slot[buf][wave] = s;
     }
   }
   __syncthreads();
-  Sel r = L.slot[buf][0];
-  for (int q = 1; q < pollers; ++q) sel_merge(r, L.slot[buf][q]);
+  R r = L.slot[buf][0];
+  for (int q = 1; q < pollers; ++q) rec_merge(r, L.slot[buf][q]);
   buf ^= 1;
   return r;
 }
@@ -194,6 +245,17 @@ __device__ Sel exchange(const Prob &P, int rank, unsigned stamp, const Sel &mine
 __device__ __forceinline__ int64_t gmap(const Prob &P, int64_t j) { return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0); }
 __device__ __forceinline__ int label_of(const Prob &P, int64_t j) {
   return P.y ? P.y[gmap(P, j)] : (j < P.len0 ? 1 : -1);
+}
+
+// Gain of the second-order rule for a member t of I_low above b_up: (f_t - b_up)^2 / a_ut with
+// a_ut = K_uu + K_tt - 2 K_ut, K_uu = K_tt = 1 for the RBF kernel, 1e-12 when not positive.
+// Rounded as written (no contraction).
+__device__ __forceinline__ double so_gain(double ft, double bup, float kut) {
+#pragma clang fp contract(off)
+  const double bt = ft - bup;
+  double at = (1.0 + 1.0) - 2.0 * (double)kut;
+  if (at <= 0.0) at = 1e-12;
+  return bt * bt / at;
 }
 
 // Offer sample j (value f, multiplier a, label y) to this thread's candidates.
@@ -205,7 +267,8 @@ __device__ __forceinline__ void consider(Sel &s, double f, double a, int y, int 
 }
 
 // ---------------------------------------------------------------------------------------
-template <int BS, int PER, bool GRAM, bool VEC4, bool ONE = false>
+// SO (Gram path): the second index of the pair by the second-order rule (p.second_order).
+template <int BS, int PER, bool GRAM, bool VEC4, bool ONE = false, bool SO = false>
 __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   constexpr int NW = BS / 64;
   // Samples per lane group and batch (a sample's arithmetic does not depend on them): scalar
@@ -215,10 +278,11 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   // Row path, dynamic LDS: dot products against x_u and x_l [2][per_wg] (fp64), cache tags
   // [cap], then the rows of X this workgroup keeps resident [res][d] (16-byte aligned).
   extern __shared__ float4 dyn4[];
-  __shared__ SelLds<NW> sh;
+  __shared__ RecLds<Sel, NW> sh;
+  __shared__ RecLds<Sel2, NW> sh2;
   __shared__ int s_abort;
   __shared__ double s_kul;
-  int buf = 0;
+  int buf = 0, buf2 = 0;
 
   const int32_t pid = p.wg_prob[blockIdx.x];
   const Prob P = p.probs[pid];
@@ -286,9 +350,11 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   }
   for (;;) {
     // 1. workgroup candidates
-    s = sel_block<NW>(sel_wave(s), sh, buf);
-    // 2. exchange across the problem's workgroups
-    if (P.nwg > 1) s = exchange<NW>(P, rank, (unsigned)(t + 1), s, sh, buf, p.spin_limit, p.error, &s_abort);
+    s = rec_block<Sel, NW>(rec_wave(s), sh, buf);
+    // 2. exchange across the problem's workgroups (with the second-order rule every step has two
+    // exchanges, stamped 2t + 1 and 2t + 2)
+    const unsigned stamp1 = SO ? (unsigned)(2 * t + 1) : (unsigned)(t + 1);
+    if (P.nwg > 1) s = exchange<Sel, NW>(P, rank, stamp1, s, sh, buf, p.spin_limit, p.error, &s_abort);
     const bool aborted = s_abort != 0;
     // 3. stop rule
     if (rank == 0 && threadIdx.x == 0 && t < P.trace_len) {
@@ -310,14 +376,66 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       }
       break;
     }
-    const int64_t u = s.iu, l = s.il;
-    const int64_t gu = gmap(P, u), gl = gmap(P, l);
-    const double yu = (double)s.yu, yl = (double)s.yl;
+    const int64_t u = s.iu;
+    int64_t l = s.il;
+    const int64_t gu = gmap(P, u);
+    double yl = (double)s.yl, fl = s.vl, al = s.al;
+    const double yu = (double)s.yu;
 
     // 4. kernel rows of u and l for the own samples, K_ul, 2x2 solve, f update
     float ku[PER], kl[PER];
     double kul;
-    if (GRAM) {
+    if (GRAM && SO) {
+      // Second-order rule: row u first, the gains of the own members of I_low above b_up, a
+      // second exchange for l (its record carries f_l, a_l, y_l and K(u, l)), then row l.
+      const float *Ru = p.gram + gu * p.ld;
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+        if (j < lim) ku[k] = Ru[gmap(P, j)];
+      }
+      Sel2 c;
+      rec_init(c);
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+        const bool lo = (yv[k] > 0 && a[k] > 0.0) || (yv[k] < 0 && a[k] < C);
+        if (j < lim && lo && f[k] > s.vu) {
+          const double g = so_gain(f[k], s.vu, ku[k]);
+          if (gt_max(g, (int)j, c.g, c.il)) {
+            c.g = g; c.fl = f[k]; c.al = a[k]; c.kul = (double)ku[k]; c.il = (int)j; c.yl = yv[k];
+          }
+        }
+      }
+      c = rec_block<Sel2, NW>(rec_wave(c), sh2, buf2);
+      if (P.nwg > 1)
+        c = exchange<Sel2, NW>(P, rank, (unsigned)(2 * t + 2), c, sh2, buf2, p.spin_limit, p.error, &s_abort);
+      if (s_abort != 0) {
+        if (rank == 0 && threadIdx.x == 0) {
+          ctl->t = t;
+          ctl->status = ST_TIMEOUT;
+        }
+        break;
+      }
+      // A member of I_low above b_up exists whenever the stop rule fails (b_low > b_up + tol);
+      // the maximal violating pair's l stands in should none have been found.
+      if (c.il != IBIG) {
+        l = c.il;
+        yl = (double)c.yl;
+        fl = c.fl;
+        al = c.al;
+      }
+      if (rank == 0 && threadIdx.x == 0 && t < P.trace_len && P.trace_ul) P.trace_ul[2 * t + 1] = (int)l;
+      const int64_t gl = gmap(P, l);
+      const float *Rl = p.gram + gl * p.ld;
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int64_t j = base + threadIdx.x + (int64_t)k * BS;
+        if (j < lim) kl[k] = Rl[gmap(P, j)];
+      }
+      kul = c.il != IBIG ? c.kul : (double)Ru[gl];
+    } else if (GRAM) {
+      const int64_t gl = gmap(P, l);
       const float *Ru = p.gram + gu * p.ld;
       const float *Rl = p.gram + gl * p.ld;
 #pragma unroll
@@ -331,6 +449,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       }
       kul = (double)Ru[gl];
     } else {
+      const int64_t gl = gmap(P, l);
       const int64_t d = p.d;
       const int gs = group_size_for(d, VEC4);
       const int lig = threadIdx.x & (gs - 1);
@@ -422,9 +541,9 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         }
       }
     }
-    const PairStep ps = solve_pair(C, s.vu, s.vl, s.au, s.al, yu, yl, kul);
+    const PairStep ps = solve_pair(C, s.vu, fl, s.au, al, yu, yl, kul);
     const double au_new = ps.au, al_new = ps.al;
-    const double cu = (au_new - s.au) * yu, cl = (al_new - s.al) * yl;
+    const double cu = (au_new - s.au) * yu, cl = (al_new - al) * yl;
     sel_init(s);
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
@@ -539,14 +658,24 @@ static bool row_batch_one(const SolveParams &p, int32_t per_thread) {
   return per_thread == 8 && row_vec4(p) && group_size_for(p.d, true) <= 8;
 }
 
-template <int BS, int PER, bool GRAM, bool VEC4, bool ONE = false>
+template <int BS, int PER, bool GRAM, bool VEC4, bool ONE = false, bool SO = false>
 static const void *kernel_of() {
-  return reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4, ONE>);
+  return reinterpret_cast<const void *>(&smo_solve<BS, PER, GRAM, VEC4, ONE, SO>);
 }
 
 // The solver variant for a path, samples per thread, (row path) float4 lanes and batches of
-// one; NULL if none.
-static const void *solver_kernel(bool gram, int32_t per_thread, bool vec4, bool one = false) {
+// one, (Gram path) the second-order rule; NULL if none.
+static const void *solver_kernel(bool gram, int32_t per_thread, bool vec4, bool one = false, bool so = false) {
+  if (gram && so) {
+    switch (per_thread) {
+      case 1: return kernel_of<BS_GRAM, 1, true, false, false, true>();
+      case 2: return kernel_of<BS_GRAM, 2, true, false, false, true>();
+      case 4: return kernel_of<BS_GRAM, 4, true, false, false, true>();
+      case 8: return kernel_of<BS_GRAM, 8, true, false, false, true>();
+      case 16: return kernel_of<BS_GRAM, 16, true, false, false, true>();
+      default: return nullptr;
+    }
+  }
   if (gram) {
     switch (per_thread) {
       case 1: return kernel_of<BS_GRAM, 1, true, false>();
@@ -572,7 +701,9 @@ static const void *solver_kernel(bool gram, int32_t per_thread, bool vec4, bool 
 
 hipError_t launch_solver(const SolveParams &p, int32_t total_wg, int32_t per_thread, bool gram, hipStream_t s,
                          int32_t *max_coresident) {
-  const void *fn = solver_kernel(gram, per_thread, !gram && row_vec4(p), !gram && row_batch_one(p, per_thread));
+  if (p.second_order && !gram) return hipErrorInvalidValue;
+  const void *fn = solver_kernel(gram, per_thread, !gram && row_vec4(p), !gram && row_batch_one(p, per_thread),
+                                 p.second_order != 0);
   if (!fn) return hipErrorInvalidValue;
   const int bs = gram ? BS_GRAM : BS_ROWS;
   const size_t shmem = gram ? 0 : row_path_lds(p, p.res_rows);

@@ -64,7 +64,7 @@ struct SolveParams {
   int32_t cache_cap;
   int32_t res_rows;        // row path: rows of X each workgroup keeps in LDS (the first of its slice)
   int32_t max_per_wg;      // row path: largest per_wg of the launch's problems (sizes the LDS)
-  int32_t pad;
+  int32_t second_order;    // Gram path: 1 = the second index of each pair by the second-order rule
   uint64_t spin_limit;     // wall-clock ticks (100 MHz) a wait may last
   int32_t *error;          // set to 1 on a wait time-out
 };

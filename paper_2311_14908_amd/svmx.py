@@ -21,6 +21,7 @@ SVM_OK, SVM_NOT_CONVERGED = 0, 1
 SVM_EINVAL, SVM_ENOMEM, SVM_EDEVICE, SVM_EWORKSPACE = -1, -2, -3, -4
 GRAM_AUTO, GRAM_ON, GRAM_OFF = 0, 1, 2
 MFMA_SPLIT_F16, MFMA_F32 = 0, 1
+SELECT_MVP, SELECT_SECOND_ORDER = 0, 1
 
 
 class SvmError(RuntimeError):
@@ -35,7 +36,7 @@ class svm_options(C.Structure):
                 ("trace_len", C.c_int32), ("trace_ws", C.POINTER(C.c_int32)), ("trace_b", C.POINTER(C.c_double)),
                 ("f_out", C.c_void_p), ("stream", C.c_void_p), ("workgroups", C.c_int32),
                 ("exchange_levels", C.c_int32), ("gram_mfma", C.c_int32), ("working_set", C.c_int32),
-                ("resident_rows", C.c_int32)]
+                ("resident_rows", C.c_int32), ("selection", C.c_int32), ("reserved", C.c_int32)]
 
 
 class svm_stats(C.Structure):
@@ -112,7 +113,7 @@ def _dev(t: torch.Tensor, dtype, name):
 
 
 def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, check_every=0, trace_len=0,
-            workgroups=0, exchange_levels=0, gram_mfma=0, working_set=0, resident_rows=0,
+            workgroups=0, exchange_levels=0, gram_mfma=0, working_set=0, resident_rows=0, selection=0,
             f_out: torch.Tensor | None = None, stream=None):
     o = svm_options()
     load().svm_default_options(C.byref(o))
@@ -128,6 +129,7 @@ def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, 
     o.gram_mfma = gram_mfma
     o.working_set = working_set
     o.resident_rows = resident_rows
+    o.selection = selection
     o.f_out = None if f_out is None else f_out.data_ptr()
     s = stream if stream is not None else torch.cuda.current_stream()
     o.stream = s.cuda_stream

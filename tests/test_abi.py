@@ -37,7 +37,8 @@ def test_struct_layouts_match_header():
     lib = svmx.load()
     o = svmx.svm_options()
     lib.svm_default_options(C.byref(o))
-    assert o.struct_size == C.sizeof(svmx.svm_options) == 96
+    assert o.struct_size == C.sizeof(svmx.svm_options) == 104
+    assert o.selection == svmx.SELECT_MVP and o.reserved == 0
     assert o.check_every == 65536 and o.gram == svmx.GRAM_AUTO
     assert C.sizeof(svmx.svm_stats) == 120
 
@@ -105,6 +106,30 @@ def test_train_rejects(case, expect):
                        a["ws"], a["wsb"], C.byref(o), None)
     assert st == expect
     assert lib.svm_last_error().decode() != ""
+
+
+@pytest.mark.parametrize("opt", [
+    dict(selection=2),                                         # no such rule
+    dict(reserved=1),                                          # reserved field must be 0
+    dict(selection=svmx.SELECT_SECOND_ORDER, working_set=32),  # the working-set rounds have their own rule
+    dict(selection=svmx.SELECT_SECOND_ORDER, gram=svmx.GRAM_OFF),  # row l is needed before l is known
+    dict(selection=svmx.SELECT_SECOND_ORDER, gram_budget_bytes=1 << 10),  # AUTO falls back to the row path
+])
+def test_selection_option_rejects(opt):
+    """Second-order selection runs on the Gram path of the per-step solver only; anything else is
+    SVM_EINVAL, returned before any device access."""
+    lib = svmx.load()
+    o = _opts(**opt)
+    b = C.c_double(0)
+    st = lib.svm_train(FAKE, FAKE, 100, 4, 1.0, 0.5, 1e-3, FAKE, C.byref(b), FAKE, 1 << 40, C.byref(o), None)
+    assert st == svmx.SVM_EINVAL
+    assert lib.svm_last_error().decode() != ""
+    if "gram" in opt or "gram_budget_bytes" in opt:
+        bp = np.zeros(3).ctypes.data_as(C.c_void_p)
+        assert lib.svm_train_ovo(FAKE, FAKE, 100, 4, 3, 1.0, 0.5, 1e-3, FAKE, bp, FAKE, 1 << 40, C.byref(o),
+                                 None) == svmx.SVM_EINVAL
+    else:
+        assert lib.svm_train_workspace_bytes(100, 4, C.byref(o)) == -1
 
 
 def test_ovo_rejects():

@@ -9,9 +9,12 @@ Gates (as for the small cases):
                 runner-up gap is below 1e-6 (a tie within the fp32-kernel error of f, where
                 either choice is a maximal violating pair)
   objective     relative 1e-4
-  decisions     max abs 1e-3 on the stored test points; identical labels where |d| >= 1e-3
-  validity      0 <= a <= C, sum a y = 0, and tol-KKT on sampled rows with f recomputed by the
-                oracle from the GPU's alpha (slack 1e-4 for the fp32 kernel values)
+  decisions     max abs 1e-3 on the stored test points; labels compared on every point (one-vs-one:
+                the voted class must be one the oracle's decisions allow, exactly the oracle's
+                where no pair decision is within the measured error of zero)
+  validity      0 <= a <= C, sum a y = 0, tol-KKT on every row with f recomputed by the oracle
+                from the GPU's alpha (slack 1e-4 for the fp32 kernel values), and the duality
+                gap 0 <= P - W <= n C tol from the same f
 """
 import hashlib
 import json
@@ -23,6 +26,7 @@ import torch
 
 import oracle
 from paper_2311_14908_amd import svmx, synth
+from tests.label_checks import check_binary_labels, check_ovo_predictions, kkt_and_gap, ovo_vote
 
 pytestmark = pytest.mark.gpu
 
@@ -85,24 +89,18 @@ def test_binary_full_size(cid, gram):
     assert abs(st["dual_obj"] - R["dual_obj"]) <= 1e-4 * abs(R["dual_obj"])
     d_gpu = svmx.svm_predict(Xd, yd, out.alpha, out.b, wl.gamma, dev(Xt[:nt])).cpu().numpy()
     d_ref = np.array(R["test_decisions"])
-    err = np.max(np.abs(d_gpu - d_ref))
+    err = float(np.max(np.abs(d_gpu - d_ref)))
     print(f"max |d_gpu - d_oracle| = {err:.2e}")
     assert err <= 1e-3
-    sure = np.abs(d_ref) >= 1e-3
-    assert np.array_equal(d_gpu[sure] > 0, d_ref[sure] > 0)
+    check_binary_labels(d_gpu, d_ref, err)
 
-    # validity of the GPU solution, checked by the oracle
+    # validity of the GPU solution, checked by the oracle on every row
     a = out.alpha.cpu().numpy()
     assert np.all(a >= 0) and np.all(a <= wl.C)
     assert abs(float(a @ y)) <= 1e-9 * wl.C * len(y)
-    rows = np.random.default_rng(cid).choice(len(y), 128, replace=False)
-    f = oracle.f_from_alpha(X, y, a, wl.gamma, rows=rows)
-    ar, yr = a[rows], y[rows]
-    up = ((yr > 0) & (ar < wl.C)) | ((yr < 0) & (ar > 0))
-    low = ((yr > 0) & (ar > 0)) | ((yr < 0) & (ar < wl.C))
-    slack = 1e-4
-    assert np.all(f[up] >= out.b - wl.tol / 2 - slack)
-    assert np.all(f[low] <= out.b + wl.tol / 2 + slack)
+    f = oracle.f_from_alpha(X, y, a, wl.gamma)
+    gap, _ = kkt_and_gap(f, y, a, out.b, wl.C, wl.tol, slack=1e-4)
+    print(f"duality gap P - W = {gap:.3e} (bound n C tol = {len(y) * wl.C * wl.tol:.1f})")
 
 
 @pytest.mark.parametrize("gram", [svmx.GRAM_AUTO, svmx.GRAM_OFF])
@@ -125,11 +123,12 @@ def test_ovo_full_size(gram):
     dec, pred = svmx.svm_predict_ovo(Xd, ld, k, out.alpha, out.b, wl.gamma, dev(Xt[:nt]))
     d_ref = np.array(R["test_decisions"])
     dec = dec.cpu().numpy()
-    err = np.max(np.abs(dec - d_ref))
+    err = float(np.max(np.abs(dec - d_ref)))
     print(f"\none-vs-one (gram {gram}): max |d_gpu - d_oracle| = {err:.2e}")
     assert err <= 1e-3
-    sure = np.all(np.abs(d_ref) >= 1e-3, axis=1)
-    assert np.array_equal(pred.cpu().numpy()[sure], np.array(R["test_pred"])[sure])
+    # the vote restated in the checks gives the oracle's stored classes from its stored decisions
+    assert [ovo_vote(r > 0, k) for r in d_ref] == list(R["test_pred"])
+    check_ovo_predictions(pred.cpu().numpy(), d_ref, k, err)
 
 
 def test_ovo_row_path_full_size_pairs_equal_binary():
@@ -174,17 +173,11 @@ def test_working_set_full_size(cid, q, gram):
     assert abs(st["dual_obj"] - R["dual_obj"]) <= 1e-4 * abs(R["dual_obj"])
     d_gpu = svmx.svm_predict(Xd, yd, out.alpha, out.b, wl.gamma, dev(Xt[:nt])).cpu().numpy()
     d_ref = np.array(R["test_decisions"])
-    assert np.max(np.abs(d_gpu - d_ref)) <= 1e-3
-    sure = np.abs(d_ref) >= 1e-3
-    assert np.array_equal(d_gpu[sure] > 0, d_ref[sure] > 0)
+    err = float(np.max(np.abs(d_gpu - d_ref)))
+    assert err <= 1e-3
+    check_binary_labels(d_gpu, d_ref, err)
     a = out.alpha.cpu().numpy()
     assert np.all(a >= 0) and np.all(a <= wl.C)
     assert abs(float(a @ y)) <= 1e-9 * wl.C * len(y)
-    rows = np.random.default_rng(100 + cid).choice(len(y), 128, replace=False)
-    f = oracle.f_from_alpha(X, y, a, wl.gamma, rows=rows)
-    ar, yr = a[rows], y[rows]
-    up = ((yr > 0) & (ar < wl.C)) | ((yr < 0) & (ar > 0))
-    low = ((yr > 0) & (ar > 0)) | ((yr < 0) & (ar < wl.C))
-    slack = 1e-4
-    assert np.all(f[up] >= out.b - wl.tol / 2 - slack)
-    assert np.all(f[low] <= out.b + wl.tol / 2 + slack)
+    f = oracle.f_from_alpha(X, y, a, wl.gamma)
+    kkt_and_gap(f, y, a, out.b, wl.C, wl.tol, slack=1e-4)
