@@ -10,8 +10,9 @@ Prints ONE JSON line.  ``value`` is SMO iterations per second over the timed ste
 ``train_seconds`` is the mean svm_train wall time.  ``roofline`` describes the dominant
 kernel (the persistent SMO solver) against the HBM roofline with the algorithmic bytes of
 an SMO step (two kernel rows 8n, f read+write 16n, status n = 25n bytes).  ``gram_build``
-reports the Gram precompute against the dense fp16 MFMA peak (its contraction runs as
-split-fp16 products) with the method's n^2 d flops.  ``row_path`` reports the 20,000 x 784
+reports the Gram precompute against its roofline: the method's n^2 d flops at the dense fp16
+MFMA peak (its contraction runs as split-fp16 products) or its 4 n^2 bytes of stores at the HBM
+peak, whichever takes longer.  ``row_path`` reports the 20,000 x 784
 solve with kernel rows evaluated from X at every step (4nd + 21n bytes a step), and
 ``row_path_large`` the same recipe at 300,000 x 784.  ``ovo`` trains the 10-class one-vs-one
 workload end to end, with rooflines for its global Gram and for the launch that advances all
@@ -22,7 +23,8 @@ one-vs-one) for context.  ``workloads`` trains the other binary workloads end to
 each.  ``working_set`` trains the Gram-path workloads with the working-set solver
 (svm_options.working_set = q: rounds of pair steps on q samples, f updated once a round) beside
 the pair solver, and the 20,000 x 784 workload once more without a Gram (row path); its
-iterations are pair steps too.  ``cpu_baseline`` times the fp64 CPU oracle on the same problem
+iterations are pair steps too.  ``second_order`` trains the same three workloads with the
+second-order choice of the pair's second index beside the maximal violating pair.  ``cpu_baseline`` times the fp64 CPU oracle on the same problem
 on this host's cores: the whole training when it fits the time budget, else its first steps.
 """
 from __future__ import annotations
@@ -64,15 +66,25 @@ def counter_bytes_per_step(workload_name, n, d):
 
 
 def gram_roofline(n, d, seconds):
-    """The Gram precompute against the dense fp16 MFMA peak, with the method's n^2 d flops."""
+    """The Gram precompute against its roofline: the method's n^2 d flops (symmetric count) at the
+    dense fp16 MFMA peak (the contraction runs as split-fp16 products on the fp16 instruction)
+    against its 4 n^2 bytes of stores at the HBM peak; `bound` is the resource whose ideal time is
+    longer, and achieved/peak/frac are given for it (both fractions are reported)."""
     flops = float(n) * n * d
+    wbytes = 4.0 * n * n
     tf = flops / seconds / 1e12 if seconds > 0 else None
+    gbps = wbytes / seconds / 1e9 if seconds > 0 else None
+    t_mfma, t_hbm = flops / (FP16_MFMA_PEAK_TFLOPS * 1e12), wbytes / (HBM_PEAK_GBPS * 1e9)
+    mfma = {"achieved": tf, "peak": FP16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": tf / FP16_MFMA_PEAK_TFLOPS if tf else None}
+    hbm = {"achieved": gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gbps / HBM_PEAK_GBPS if gbps else None}
+    bound = "mfma" if t_mfma >= t_hbm else "hbm"
     return {"kernel": "gram_rbf_f16x3 (fp32 inputs split into fp16 halves, 3 products per fp32 product)",
-            "bound": "mfma", "flops": flops, "seconds": seconds, "achieved": tf, "peak": FP16_MFMA_PEAK_TFLOPS,
-            "unit": "TFLOP/s", "frac": tf / FP16_MFMA_PEAK_TFLOPS if tf else None,
+            "bound": bound, **(mfma if bound == "mfma" else hbm), "flops": flops, "gram_bytes": wbytes,
+            "seconds": seconds, "ideal_seconds": {"mfma": t_mfma, "hbm_write": t_hbm},
+            "mfma_frac": mfma["frac"], "hbm_write_frac": hbm["frac"],
             "executed_fp16_tflops": 3.0 * tf if tf else None,
-            "fp32_equivalent_vs_fp32_mfma_peak": tf / FP32_MFMA_PEAK_TFLOPS if tf else None,
-            "gram_bytes": 4.0 * n * n, "write_GBps": 4.0 * n * n / seconds / 1e9 if seconds > 0 else None}
+            "fp32_equivalent_vs_fp32_mfma_peak": tf / FP32_MFMA_PEAK_TFLOPS if tf else None}
 
 
 def log(*a):
@@ -99,6 +111,8 @@ def main():
                     help="skip the end-to-end trainings of the other binary workloads")
     ap.add_argument("--ws-q", type=str, default="32,128",
                     help="working-set sizes of the working-set leg, comma separated ('' = skip)")
+    ap.add_argument("--no-second-order", action="store_true",
+                    help="skip the second-order selection leg (Gram-path binary workloads)")
     ap.add_argument("--no-paper-shapes", action="store_true",
                     help="skip the context runs at the paper's shapes (d=102, 200-800 per class)")
     ap.add_argument("--ovo-row-steps", type=int, default=300,
@@ -420,6 +434,35 @@ def main():
             del Xkd, ykd
             torch.cuda.empty_cache()
         result["working_set"] = wsr
+
+    if not args.no_second_order:
+        # second-order choice of l (svm_options.selection) beside the maximal violating pair on
+        # the Gram-path binary workloads: steps, microseconds a step, train seconds (one warm-up,
+        # one timed training each)
+        sor = {}
+        for cid in (1, 2, 3):
+            wk = synth.workload(cid)
+            Xk, yk, _, _ = synth.generate(cid, m=1)
+            Xkd, ykd = torch.from_numpy(Xk).cuda(), torch.from_numpy(yk).cuda()
+            ent = {}
+            for name, sel in (("mvp", svmx.SELECT_MVP), ("second_order", svmx.SELECT_SECOND_ORDER)):
+                svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, gram=svmx.GRAM_ON, selection=sel)
+                torch.cuda.synchronize()
+                t1 = time.perf_counter()
+                rk = svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, gram=svmx.GRAM_ON, selection=sel)
+                torch.cuda.synchronize()
+                tk = time.perf_counter() - t1
+                sk = rk.stats
+                ent[name] = {"train_seconds": tk, "smo_iterations": sk["iterations"],
+                             "us_per_smo_step": 1e6 * sk["t_kernel"] / sk["iterations"],
+                             "solver_kernel_seconds": sk["t_kernel"], "dual_obj": sk["dual_obj"]}
+                del rk
+            ent["second_order"]["steps_vs_mvp"] = ent["second_order"]["smo_iterations"] / ent["mvp"]["smo_iterations"]
+            ent["second_order"]["speedup_vs_mvp"] = ent["mvp"]["train_seconds"] / ent["second_order"]["train_seconds"]
+            sor[wk.name] = ent
+            del Xkd, ykd
+            torch.cuda.empty_cache()
+        result["second_order"] = sor
 
     if not args.no_paper_shapes:
         # context runs of the paper's shapes (102 features, 200-800 samples per class; binary and

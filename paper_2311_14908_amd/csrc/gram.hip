@@ -3,8 +3,9 @@
 // G_ij = exp(-gamma * max(0, |x_i|^2 + |x_j|^2 - 2 x_i.x_j)): the dot products form the
 // contraction X X^T, run on v_mfma_f32_16x16x4f32 with fp32 inputs and accumulation over the
 // upper-triangle tiles only (G is symmetric); the row norms are accumulated from the same LDS
-// tiles and the RBF map is the epilogue.  The
-// kernel is the Gaussian RBF the paper names (Section III.C).
+// tiles and the RBF map is the epilogue, whose stores are non-temporal (the Gram is not read
+// again here, so its lines should not displace the operand slabs from L2).  The kernel is the
+// Gaussian RBF the paper names (Section III.C).
 #include "common.hpp"
 #include "rbf_rows.hpp"
 #include "tile_order.hpp"
@@ -136,15 +137,15 @@ __global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X
       if (gc < n) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (gr0 + e < n) G[(gr0 + e) * ld + gc] = kv[e];
+          if (gr0 + e < n) __builtin_nontemporal_store(kv[e], &G[(gr0 + e) * ld + gc]);
         if (mirror) {
           float *dst = G + gc * ld + gr0;
           if (STORE4 && gr0 + 3 < n) {
-            *reinterpret_cast<float4 *>(dst) = make_float4(kv[0], kv[1], kv[2], kv[3]);
+            __builtin_nontemporal_store((v4f){kv[0], kv[1], kv[2], kv[3]}, reinterpret_cast<v4f *>(dst));
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (gr0 + e < n) dst[e] = kv[e];
+              if (gr0 + e < n) __builtin_nontemporal_store(kv[e], &dst[e]);
           }
         }
       }
