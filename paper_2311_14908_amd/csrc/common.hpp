@@ -20,6 +20,17 @@ struct SplitX {
   int64_t dp;
 };
 SplitX split_views(void *scratch, int64_t n, int64_t d);
+
+// Kernel value from the fp32 accumulation of the split-fp16 product of rows i and j (row i the
+// MFMA's first operand): the scales, |x_i|^2 + |x_j|^2 - 2 x_i.x_j with one fused multiply-add,
+// clamped at 0, exp2(c t), c = -gamma log2(e) (one fused multiply-add, written out, so the
+// rounding does not depend on what the compiler contracts).
+__device__ __forceinline__ float split_rbf(float acc, float si, float sj, float ni, float nj, float c) {
+  const float dot = (acc * si) * sj;
+  float t = __builtin_fmaf(-2.0f, dot, ni + nj);
+  t = t > 0.f ? t : 0.f;
+  return __builtin_amdgcn_exp2f(c * t);
+}
 hipError_t launch_split_rows(const float *X, int64_t n, int64_t d, const SplitX &s, hipStream_t st);
 
 // Split-fp16 Gram (gram_split.hip): scratch bytes, and the build into G.

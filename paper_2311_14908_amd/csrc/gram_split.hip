@@ -203,12 +203,8 @@ __global__ void __launch_bounds__(SBS) gram_rbf_f16x3(SplitX s, int64_t n, float
       const int64_t gc = j0 + lc;
       float kv[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float dot = (acc[a][bb][e] * sA[lr0 + e]) * sB[lc];
-        float t = nA[lr0 + e] + nB[lc] - 2.0f * dot;
-        t = t > 0.f ? t : 0.f;
-        kv[e] = (gr0 + e == gc) ? 1.0f : __builtin_amdgcn_exp2f(c * t);
-      }
+      for (int e = 0; e < 4; ++e)
+        kv[e] = (gr0 + e == gc) ? 1.0f : split_rbf(acc[a][bb][e], sA[lr0 + e], sB[lc], nA[lr0 + e], nB[lc], c);
       if (diag) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) T[lr0 + e][lc] = kv[e];

@@ -101,9 +101,11 @@ __device__ __forceinline__ void side_winner(double v, int i, double a, int y, do
   ry = __builtin_amdgcn_readlane(y, lane);
 }
 
-__device__ __forceinline__ void st_word(u64 *p, u64 v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ void st_word(u64 *p, u64 v) {
+  __hip_atomic_store(gp(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ u64 ld_word(const u64 *p) {
-  return __hip_atomic_load(const_cast<u64 *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load(gp(const_cast<u64 *>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // 2x2 sub-problem on (u, l): eta = K_uu + K_ll - 2 K_ul with K_uu = K_ll = 1 for the RBF
 // kernel, the box [L, H] on a_l, the partner clamped to [0, C], values within 1e-12 C of a

@@ -9,6 +9,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include "solver_params.hpp"
+
 namespace svmx {
 
 // Feature positions (float4 units when VEC4) each lane of a group takes in the first register
@@ -75,7 +77,7 @@ template <> struct Lane<false> {
 template <bool VEC4>
 __device__ __forceinline__ double sq_norm(const float *x, int64_t d, int lig, int gs) {
   typedef typename Lane<VEC4>::T T;
-  const T *p = reinterpret_cast<const T *>(x);
+  const SVMX_GLOBAL T *p = gp(reinterpret_cast<const T *>(x));
   const int64_t units = VEC4 ? (d >> 2) : d;
   float acc = 0.f;
   for (int64_t k = lig; k < units; k += gs) acc = Lane<VEC4>::dot(p[k], p[k], acc);
@@ -100,8 +102,8 @@ __device__ __forceinline__ void load_pair(RowPair<VEC4, MAXM> &r, const float *x
     const int64_t k = lig + (int64_t)m * gs;
     const int64_t kk = k < units ? k : units - 1;
     r.mk[m] = k < units ? 1.f : 0.f;
-    r.a[m] = Lane<VEC4>::scale(reinterpret_cast<const T *>(xu)[kk], r.mk[m]);
-    r.b[m] = Lane<VEC4>::scale(reinterpret_cast<const T *>(xl)[kk], r.mk[m]);
+    r.a[m] = Lane<VEC4>::scale(gp(reinterpret_cast<const T *>(xu))[kk], r.mk[m]);
+    r.b[m] = Lane<VEC4>::scale(gp(reinterpret_cast<const T *>(xl))[kk], r.mk[m]);
   }
 }
 
@@ -113,7 +115,7 @@ __device__ __forceinline__ T row_unit(const float *row, int64_t k) {
 #if __HIP_DEVICE_COMPILE__
   if constexpr (XLDS) return ((__attribute__((address_space(3))) const T *)row)[k];
 #endif
-  return reinterpret_cast<const T *>(row)[k];
+  return gp(reinterpret_cast<const T *>(row))[k];
 }
 
 // Block 0 of nb <= SB samples xs[0..nb): positions k = lig + m*gs, m < MAXM (float4 units when
@@ -167,8 +169,8 @@ __device__ __forceinline__ void dot_partials(const typename Lane<VEC4>::T (&v0)[
       const int64_t k = k0 + (int64_t)m * gs;
       const int64_t kk = k < units ? k : units - 1;
       mk[m] = k < units ? 1.f : 0.f;
-      a[m] = reinterpret_cast<const T *>(xu)[kk];
-      b[m] = reinterpret_cast<const T *>(xl)[kk];
+      a[m] = gp(reinterpret_cast<const T *>(xu))[kk];
+      b[m] = gp(reinterpret_cast<const T *>(xl))[kk];
 #pragma unroll
       for (int s = 0; s < SB; ++s) v[s][m] = row_unit<XLDS, T>(xs[s < nb ? s : nb - 1], kk);
     }

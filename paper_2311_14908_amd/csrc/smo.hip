@@ -244,7 +244,7 @@ __device__ R exchange(const Prob &P, int rank, unsigned stamp, const R &mine, Re
 
 __device__ __forceinline__ int64_t gmap(const Prob &P, int64_t j) { return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0); }
 __device__ __forceinline__ int label_of(const Prob &P, int64_t j) {
-  return P.y ? P.y[gmap(P, j)] : (j < P.len0 ? 1 : -1);
+  return P.y ? gp(P.y)[gmap(P, j)] : (j < P.len0 ? 1 : -1);
 }
 
 // Gain of the second-order rule for a member t of I_low above b_up: (f_t - b_up)^2 / a_ut with
@@ -300,8 +300,8 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   for (int k = 0; k < PER; ++k) {
     const int64_t j = base + threadIdx.x + (int64_t)k * BS;
     if (j < lim) {
-      f[k] = P.f[j];
-      a[k] = P.alpha[j];
+      f[k] = gp(P.f)[j];
+      a[k] = gp(P.alpha)[j];
       yv[k] = label_of(P, j);
     } else {
       f[k] = 0.0;
@@ -320,19 +320,19 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   double sq[PER];  // squared norms of the own samples (row path)
   if (!GRAM) {
     if (use_cache) {
-      for (int s = threadIdx.x; s < p.cache_cap; s += BS) tags[s] = p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s];
+      for (int s = threadIdx.x; s < p.cache_cap; s += BS) tags[s] = gp(p.cache_tags)[(size_t)blockIdx.x * p.cache_cap + s];
     }
     typedef typename Lane<VEC4>::T T;
     const int64_t units = VEC4 ? (p.d >> 2) : p.d;
     T *xr = reinterpret_cast<T *>(xres);
     for (int64_t e = threadIdx.x; e < res * units; e += BS) {
       const int64_t r = e / units, k = e - r * units;
-      xr[e] = reinterpret_cast<const T *>(p.X + gmap(P, base + r) * p.d)[k];
+      xr[e] = gp(reinterpret_cast<const T *>(p.X + gmap(P, base + r) * p.d))[k];
     }
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int64_t j = base + threadIdx.x + (int64_t)k * BS;
-      sq[k] = j < lim ? p.sqn[gmap(P, j)] : 0.0;
+      sq[k] = j < lim ? gp(p.sqn)[gmap(P, j)] : 0.0;
     }
   }
   __syncthreads();
@@ -388,7 +388,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
     if (GRAM && SO) {
       // Second-order rule: row u first, the gains of the own members of I_low above b_up, a
       // second exchange for l (its record carries f_l, a_l, y_l and K(u, l)), then row l.
-      const float *Ru = p.gram + gu * p.ld;
+      const SVMX_GLOBAL float *Ru = gp(p.gram) + gu * p.ld;
 #pragma unroll
       for (int k = 0; k < PER; ++k) {
         const int64_t j = base + threadIdx.x + (int64_t)k * BS;
@@ -427,7 +427,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       }
       if (rank == 0 && threadIdx.x == 0 && t < P.trace_len && P.trace_ul) P.trace_ul[2 * t + 1] = (int)l;
       const int64_t gl = gmap(P, l);
-      const float *Rl = p.gram + gl * p.ld;
+      const SVMX_GLOBAL float *Rl = gp(p.gram) + gl * p.ld;
 #pragma unroll
       for (int k = 0; k < PER; ++k) {
         const int64_t j = base + threadIdx.x + (int64_t)k * BS;
@@ -436,8 +436,8 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       kul = c.il != IBIG ? c.kul : (double)Ru[gl];
     } else if (GRAM) {
       const int64_t gl = gmap(P, l);
-      const float *Ru = p.gram + gu * p.ld;
-      const float *Rl = p.gram + gl * p.ld;
+      const SVMX_GLOBAL float *Ru = gp(p.gram) + gu * p.ld;
+      const SVMX_GLOBAL float *Rl = gp(p.gram) + gl * p.ld;
 #pragma unroll
       for (int k = 0; k < PER; ++k) {
         const int64_t j = base + threadIdx.x + (int64_t)k * BS;
@@ -458,7 +458,7 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
       // Block 0 of x_u and x_l is held in registers for the whole step; the samples stream
       // past it in batches of SB.
       const float *xu = p.X + gu * d, *xl = p.X + gl * d;
-      const double nu = p.sqn[gu], nl = p.sqn[gl];
+      const double nu = gp(p.sqn)[gu], nl = gp(p.sqn)[gl];
       RowPair<VEC4, ROW_MAXM> rp;
       load_pair(rp, xu, xl, d, lig, gs);
       int su = -1, sl = -1;
@@ -527,10 +527,10 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
         const int64_t j = base + threadIdx.x + (int64_t)k * BS;
         if (j < lim) {
           const int64_t q = j - base;
-          ku[k] = hit_u ? p.cache[(size_t)su * p.ld + j] : rbf_from_dot(nu, sq[k], dotu[q], p.gamma);
-          kl[k] = hit_l ? p.cache[(size_t)sl * p.ld + j] : rbf_from_dot(nl, sq[k], dotl[q], p.gamma);
-          if (store_u) p.cache[(size_t)su * p.ld + j] = ku[k];
-          if (store_l) p.cache[(size_t)sl * p.ld + j] = kl[k];
+          ku[k] = hit_u ? gp(p.cache)[(size_t)su * p.ld + j] : rbf_from_dot(nu, sq[k], dotu[q], p.gamma);
+          kl[k] = hit_l ? gp(p.cache)[(size_t)sl * p.ld + j] : rbf_from_dot(nl, sq[k], dotl[q], p.gamma);
+          if (store_u) gp(p.cache)[(size_t)su * p.ld + j] = ku[k];
+          if (store_l) gp(p.cache)[(size_t)sl * p.ld + j] = kl[k];
         }
       }
       if (use_cache) {
@@ -562,13 +562,13 @@ __global__ void __launch_bounds__(BS) smo_solve(SolveParams p) {
   for (int k = 0; k < PER; ++k) {
     const int64_t j = base + threadIdx.x + (int64_t)k * BS;
     if (j < lim) {
-      P.f[j] = f[k];
-      P.alpha[j] = a[k];
+      gp(P.f)[j] = f[k];
+      gp(P.alpha)[j] = a[k];
     }
   }
   if (use_cache) {
     __syncthreads();
-    for (int s2 = threadIdx.x; s2 < p.cache_cap; s2 += BS) p.cache_tags[(size_t)blockIdx.x * p.cache_cap + s2] = tags[s2];
+    for (int s2 = threadIdx.x; s2 < p.cache_cap; s2 += BS) gp(p.cache_tags)[(size_t)blockIdx.x * p.cache_cap + s2] = tags[s2];
   }
 }
 

@@ -9,6 +9,21 @@ namespace svmx {
 
 typedef unsigned long long u64;
 
+// Global-memory view of a pointer.  The kernels reach global memory through pointers held in
+// parameter blocks and descriptors; the compiler cannot tell their address space and would use
+// FLAT instructions, which also count against the LDS wait counter, so every wait for an LDS
+// access (each barrier, each LDS hand-off) would wait for outstanding global loads and stores
+// as well.  Accesses through gp() are global instructions.
+#if defined(__HIP_DEVICE_COMPILE__) && __HIP_DEVICE_COMPILE__
+#define SVMX_GLOBAL __attribute__((address_space(1)))
+#else
+#define SVMX_GLOBAL
+#endif
+template <class T>
+__host__ __device__ __forceinline__ SVMX_GLOBAL T *gp(T *p) {
+  return (SVMX_GLOBAL T *)p;
+}
+
 // Problem status kept in Ctl::status.
 enum : int32_t { ST_RUNNING = 0, ST_CONVERGED = 1, ST_MAXITER = 2, ST_TIMEOUT = -1 };
 

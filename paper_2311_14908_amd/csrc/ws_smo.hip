@@ -98,14 +98,15 @@ __device__ __forceinline__ unsigned rev_lane(unsigned x) {
 }
 
 // Compare-exchange with the lane at distance d: in an ascending pair the lower lane keeps the
-// smaller element, in a descending pair the larger one.
+// smaller element, in a descending pair the larger one.  The entries of a list are distinct
+// except empty ones, which are equal and interchangeable, so one comparison decides both lanes:
+// a lane takes its partner's entry when "the partner's comes first" equals "keep the smaller".
 __device__ __forceinline__ void kv_cx(u64 &k, unsigned &v, int d, bool asc) {
   const int lane = threadIdx.x & 63;
   const u64 ok = xor_lane64(k, d);
   const unsigned ov = xor_lane(v, d);
   const bool keep_min = ((lane & d) == 0) == asc;
-  const bool take = keep_min ? kv_lt(ok, ov, k, v) : kv_lt(k, v, ok, ov);
-  if (take) {
+  if (kv_lt(ok, ov, k, v) == keep_min) {
     k = ok;
     v = ov;
   }
@@ -132,6 +133,75 @@ __device__ __forceinline__ void wave_merge64(u64 &k, unsigned &v, u64 bk, unsign
   for (int d = 32; d > 0; d >>= 1) kv_cx(k, v, d, true);
 }
 
+// Value of lane (lane ^ (M - 1)) for M = 16, 32, 64: the mirror inside groups of M lanes (DPP
+// row_mirror, then the lane swaps across rows and halves).
+template <int M>
+__device__ __forceinline__ unsigned mirror_lane(unsigned x) {
+  const unsigned m = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x140, 0xF, 0xF, false);  // row_mirror
+  if (M == 16) return m;
+  const unsigned m2 = xor_lane(m, 16);
+  return M == 32 ? m2 : xor_lane(m2, 32);
+}
+
+template <int M>
+__device__ __forceinline__ void kv_mirror(u64 k, unsigned v, u64 &ok, unsigned &ov) {
+  ok = ((u64)mirror_lane<M>((unsigned)(k >> 32)) << 32) | mirror_lane<M>((unsigned)k);
+  ov = mirror_lane<M>(v);
+}
+
+// Lists in segments.  A wave holds 64 / SEG lists of SEG entries, list s in lanes [s SEG,
+// (s + 1) SEG), each ascending.  Merging keeps the SEG smallest of two lists: the element-wise
+// minimum of one list and the other mirrored is bitonic and holds them, and the half-cleaners
+// d = SEG/2 .. 1 sort it.  Lists of up to 16 entries thus merge four at a time in one register,
+// with row-local DPP only.
+template <int SEG>
+__device__ __forceinline__ void seg_clean(u64 &k, unsigned &v) {
+#pragma unroll
+  for (int d = SEG / 2; d > 0; d >>= 1) kv_cx(k, v, d, true);
+}
+
+// One level inside a register: the partner of lane l is lane l ^ (M - 1), M = 2 SEG, 4 SEG, ...
+// After the level with M = 2^j SEG every segment of a group of M lanes holds the same list (the
+// merged list and its mirror image sort to the same entries), so the next level can again
+// pair each segment with the mirror of the group of twice its size.
+template <int SEG, int M>
+__device__ __forceinline__ void seg_level(u64 &k, unsigned &v) {
+  u64 ok;
+  unsigned ov;
+  kv_mirror<M>(k, v, ok, ov);
+  if (kv_lt(ok, ov, k, v)) {
+    k = ok;
+    v = ov;
+  }
+  seg_clean<SEG>(k, v);
+}
+
+// All 64 / SEG lists of a register merged: afterwards every segment holds the SEG smallest.
+template <int SEG>
+__device__ __forceinline__ void seg_reduce(u64 &k, unsigned &v) {
+  if (SEG <= 16) seg_level<SEG, 32>(k, v);
+  if (SEG <= 32) seg_level<SEG, 64>(k, v);
+}
+
+// (k, v) and (bk, bv) hold the same layout of lists; (k, v) becomes the SEG smallest of both,
+// segment by segment (SEG = 64: wave_merge64).
+template <int SEG>
+__device__ __forceinline__ void seg_merge(u64 &k, unsigned &v, u64 bk, unsigned bv) {
+  u64 rk;
+  unsigned rv;
+  kv_mirror<SEG>(bk, bv, rk, rv);
+  if (kv_lt(rk, rv, k, v)) {
+    k = rk;
+    v = rv;
+  }
+  seg_clean<SEG>(k, v);
+}
+
+__device__ __forceinline__ u64 readlane64(u64 x, int l) {
+  return ((u64)(unsigned)__builtin_amdgcn_readlane((int)(x >> 32), l) << 32) |
+         (unsigned)__builtin_amdgcn_readlane((int)x, l);
+}
+
 // s + c k, rounded as written (no contraction), so every placement sums to the same bits.
 __device__ __forceinline__ double ws_acc(double s, double c, float k) {
 #pragma clang fp contract(off)
@@ -146,7 +216,7 @@ __device__ __forceinline__ int64_t ws_gmap(const Prob &P, int64_t j) {
   return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0);
 }
 __device__ __forceinline__ int ws_label(const Prob &P, int64_t j) {
-  return P.y ? P.y[ws_gmap(P, j)] : (j < P.len0 ? 1 : -1);
+  return P.y ? gp(P.y)[ws_gmap(P, j)] : (j < P.len0 ? 1 : -1);
 }
 
 // Lane `lane` of the calling wave publishes entry `lane` of a list: the three words of the
@@ -159,35 +229,45 @@ __device__ __forceinline__ void put_cand(u64 *list, int lane, u64 key, unsigned 
   for (int c = 0; c < CAND_WORDS; ++c) st_word(dst + c, w[c]);
 }
 
-// Wave-level: merge lists first, first + step, ... below last (side `side`, h entries each; at
-// most WS_MAXL lists) of the words at `words` into (k, v); v = (list - first0) * 64 + lane
+// Wave-level: merge lists first, first + step, ... below last (side `side`, h <= SEG entries
+// each; at most WS_MAXL lists) of the words at `words` into (k, v): afterwards lanes 0 .. h - 1
+// hold the h smallest, ascending (every segment of SEG lanes holds the same list).  A register
+// takes 64 / SEG lists, list i of register r in segment i; v = (list - first0) * 64 + entry
 // indexes the staging arrays, which receive each taken candidate's aux word and multiplier
-// bits.  Every lane waits for its entry of all lists at once, so the round trips overlap.
+// bits.  Every lane waits for its entries of all lists at once, so the round trips overlap.
+template <int SEG>
 __device__ void merge_lists(const u64 *words, int side, int first0, int first, int last, int step, int h,
                             unsigned stamp, unsigned *st_aux, u64 *st_ab, u64 &k, unsigned &v, uint64_t spin_limit,
                             int32_t *err, int *abort_flag) {
+  constexpr int R = 64 / SEG;         // lists per register
+  constexpr int NR = WS_MAXL / R;     // registers
   const int lane = threadIdx.x & 63;
+  const int seg = lane / SEG, e = lane % SEG;
   const int nl = first < last ? (last - first + step - 1) / step : 0;
-  u64 w[WS_MAXL][CAND_WORDS];
+  u64 w[NR][CAND_WORDS];
 #pragma unroll
-  for (int i = 0; i < WS_MAXL; ++i)
+  for (int r = 0; r < NR; ++r)
 #pragma unroll
-    for (int c = 0; c < CAND_WORDS; ++c) w[i][c] = 0;
-  if (lane < h) {
-    unsigned pending = (1u << nl) - 1u;
+    for (int c = 0; c < CAND_WORDS; ++c) w[r][c] = 0;
+  if (e < h) {
+    unsigned pending = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+      if (r * R + seg < nl) pending |= 1u << r;
     const uint64_t t0 = wall_clock64();
     while (pending) {
 #pragma unroll
-      for (int i = 0; i < WS_MAXL; ++i) {
-        if (pending & (1u << i)) {
-          const u64 *src = words + ((size_t)(first + i * step) * 2 + side) * 64 * CAND_WORDS + (size_t)lane * CAND_WORDS;
+      for (int r = 0; r < NR; ++r) {
+        if (pending & (1u << r)) {
+          const int i = r * R + seg;
+          const u64 *src = words + ((size_t)(first + i * step) * 2 + side) * 64 * CAND_WORDS + (size_t)e * CAND_WORDS;
           bool ok = true;
 #pragma unroll
           for (int c = 0; c < CAND_WORDS; ++c) {
-            w[i][c] = ld_word(src + c);
-            ok = ok && cand_stamped(w[i][c], stamp);
+            w[r][c] = ld_word(src + c);
+            ok = ok && cand_stamped(w[r][c], stamp);
           }
-          if (ok) pending &= ~(1u << i);
+          if (ok) pending &= ~(1u << r);
         }
       }
       if (pending && wall_clock64() - t0 > spin_limit) {
@@ -197,31 +277,37 @@ __device__ void merge_lists(const u64 *words, int side, int first0, int first, i
       }
     }
   }
-  k = KSENT;
-  v = VSENT;
+  u64 rk[NR];
+  unsigned rv[NR];
 #pragma unroll
-  for (int i = 0; i < WS_MAXL; ++i) {
-    if (i >= nl) break;
-    u64 ck = KSENT;
-    unsigned cv = VSENT;
-    if (lane < h) {
+  for (int r = 0; r < NR; ++r) {
+    const int i = r * R + seg;
+    rk[r] = KSENT;
+    rv[r] = VSENT;
+    if (i < nl && e < h) {
       u64 key, ab;
       unsigned aux;
-      cand_fields(w[i], key, aux, ab);
+      cand_fields(w[r], key, aux, ab);
       if (key != KSENT) {
-        ck = key;
-        cv = (unsigned)((first + i * step - first0) * 64 + lane);
-        st_aux[cv] = aux;
-        st_ab[cv] = ab;
+        rk[r] = key;
+        rv[r] = (unsigned)((first + i * step - first0) * 64 + e);
+        st_aux[rv[r]] = aux;
+        st_ab[rv[r]] = ab;
       }
     }
-    if (i == 0) {
-      k = ck;
-      v = cv;
-    } else {
-      wave_merge64(k, v, ck, cv);
-    }
   }
+  // the lists of each register, then the registers pairwise
+  const int nr = (nl + R - 1) / R;
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+    if (r < nr && R > 1) seg_reduce<SEG>(rk[r], rv[r]);
+#pragma unroll
+  for (int span = 1; span < NR; span <<= 1)
+#pragma unroll
+    for (int r = 0; r + span < NR; r += 2 * span)
+      if (r + span < nr) seg_merge<SEG>(rk[r], rv[r], rk[r + span], rv[r + span]);
+  k = rk[0];
+  v = rv[0];
 }
 
 // Waits until word `w` carries `stamp`; returns its 60-bit payload.
@@ -245,6 +331,8 @@ struct WsLds {
   signed char y[WS_SLICE_MAX];
   u64 lk[WS_NW][64];
   unsigned lv[WS_NW][64];
+  u64 pk[WS_NW][64];  // own lists: each wave's members below its threshold, 64 at a time
+  unsigned pv[WS_NW][64];
   union {
     struct {
       unsigned aux[2][WS_LISTS_MAX * 64];
@@ -408,7 +496,7 @@ __device__ __forceinline__ void row_chunk_load(RowLoad &L, const SplitX &X, int6
   for (int sl = 0; sl < 2; ++sl) {
     const _Float16 *hb = sl ? X.lo : X.hi;
     if (gb >= 0) {
-      const h8 *q8 = reinterpret_cast<const h8 *>(hb + gb * X.dp + k0) + lkq;
+      const SVMX_GLOBAL h8 *q8 = gp(reinterpret_cast<const h8 *>(hb + gb * X.dp + k0)) + lkq;
       L.r[2 * sl] = q8[0];
       L.r[2 * sl + 1] = q8[1];
     } else {
@@ -416,7 +504,7 @@ __device__ __forceinline__ void row_chunk_load(RowLoad &L, const SplitX &X, int6
       L.r[2 * sl + 1] = (h8){};
     }
     if (gs >= 0) {
-      const h8 *q8 = reinterpret_cast<const h8 *>(hb + gs * X.dp + k0) + lkq;
+      const SVMX_GLOBAL h8 *q8 = gp(reinterpret_cast<const h8 *>(hb + gs * X.dp + k0)) + lkq;
       L.r[4 + 2 * sl] = q8[0];
       L.r[4 + 2 * sl + 1] = q8[1];
     } else {
@@ -469,8 +557,8 @@ __device__ __forceinline__ void row64_load(RowLoad64 &L, const SplitX &X, const 
   const bool in = full || c < 4;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    L.b[i] = (gb[i] >= 0 && in) ? reinterpret_cast<const h8 *>(hb + gb[i] * X.dp + k0)[c] : (h8){};
-    L.s[i] = (gs[i] >= 0 && in) ? reinterpret_cast<const h8 *>(hb + gs[i] * X.dp + k0)[c] : (h8){};
+    L.b[i] = (gb[i] >= 0 && in) ? gp(reinterpret_cast<const h8 *>(hb + gb[i] * X.dp + k0))[c] : (h8){};
+    L.s[i] = (gs[i] >= 0 && in) ? gp(reinterpret_cast<const h8 *>(hb + gs[i] * X.dp + k0))[c] : (h8){};
   }
 }
 
@@ -559,7 +647,7 @@ __device__ __attribute__((noinline)) void owner_rows_block(WsLds &S, const WsPar
         const int j = tj * 16 + r16;
         if (tj < tj_n && j < len) {
           const int64_t gj = ws_gmap(P, base + j);
-          const float sj = X.scale[gj], nj = X.nrm[gj];
+          const float sj = gp(X.scale)[gj], nj = gp(X.nrm)[gj];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int pr = tp * 16 + 4 * kq + e;
@@ -619,7 +707,7 @@ __device__ __attribute__((noinline)) void owner_rows(WsLds &S, const WsParams &p
         const int j = j0 + tj * 16 + r16;
         if (j < len) {
           const int64_t gj = ws_gmap(P, base + j);
-          const float sj = X.scale[gj], nj = X.nrm[gj];
+          const float sj = gp(X.scale)[gj], nj = gp(X.nrm)[gj];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int pr = tp * 16 + 4 * kq + e;
@@ -637,7 +725,107 @@ __device__ __attribute__((noinline)) void owner_rows(WsLds &S, const WsParams &p
   }
 }
 
-template <bool GRAM>
+// Key of sample pos for a side (0: I_up by f, 1: I_low by -f), or KSENT if it is not a member.
+__device__ __forceinline__ u64 side_key(const WsLds &S, int side, int pos, int len, double C) {
+  if (pos >= len) return KSENT;
+  const double fj = S.f[pos], aj = S.a[pos];
+  const int yj = S.y[pos];
+  if (!(side == 0 ? ws_in_up(yj, aj, C) : ws_in_low(yj, aj, C))) return KSENT;
+  return f_key(side == 0 ? fj : -fj);
+}
+
+// One wave's best members of one side among the chunks of 64 samples c = half, half + 2, ...:
+// (k, v) ascending, lanes 0 .. h - 1 exact.  With one chunk it is sorted outright.  With more,
+// the h-th smallest of the lanes' own best members is a threshold no member of the wave's best
+// h exceeds (at least h members are at or below it); only the members at or below it are
+// gathered in LDS and sorted, 64 at a time, the threshold tightening to the list's h-th entry
+// after each batch.
+struct KV {
+  u64 k;
+  unsigned v;
+};
+
+__device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, int len, int h, double C) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nch = (len + 63) / 64;
+  u64 k = KSENT;
+  unsigned v = VSENT;
+  if (nch - half <= 2) {  // at most one chunk for this wave
+    if (half < nch) {
+      u64 ck = side_key(S, side, half * 64 + lane, len, C);
+      unsigned cv = ck != KSENT ? (unsigned)(half * 64 + lane) : VSENT;
+      if (__ballot(ck != KSENT) != 0) wave_sort64(ck, cv);
+      k = ck;
+      v = cv;
+    }
+    return KV{k, v};
+  }
+  u64 tk = KSENT;
+  unsigned tv = VSENT;
+  for (int c = half; c < nch; c += 2) {
+    const int pos = c * 64 + lane;
+    const u64 ck = side_key(S, side, pos, len, C);
+    if (ck != KSENT && kv_lt(ck, (unsigned)pos, tk, tv)) {
+      tk = ck;
+      tv = (unsigned)pos;
+    }
+  }
+  wave_sort64(tk, tv);
+  tk = readlane64(tk, h - 1);
+  tv = (unsigned)__builtin_amdgcn_readlane((int)tv, h - 1);
+  bool have = false;
+  int np = 0;
+  u64 *pk = S.pk[wave];
+  unsigned *pv = S.pv[wave];
+  const u64 below = (1ull << lane) - 1ull;
+  auto flush = [&]() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    u64 fk = lane < np ? pk[lane] : KSENT;
+    unsigned fv = lane < np ? pv[lane] : VSENT;
+    wave_sort64(fk, fv);
+    if (!have) {
+      k = fk;
+      v = fv;
+      have = true;
+    } else {
+      wave_merge64(k, v, fk, fv);
+    }
+    const u64 nk = readlane64(k, h - 1);
+    const unsigned nv = (unsigned)__builtin_amdgcn_readlane((int)v, h - 1);
+    if (kv_lt(nk, nv, tk, tv)) {
+      tk = nk;
+      tv = nv;
+    }
+    np = 0;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  };
+  for (int c = half; c < nch; c += 2) {
+    const int pos = c * 64 + lane;
+    const u64 ck = side_key(S, side, pos, len, C);
+    bool q = ck != KSENT && !kv_lt(tk, tv, ck, (unsigned)pos);
+    u64 mask = __ballot(q);
+    int nq = __popcll(mask);
+    if (nq == 0) continue;
+    if (np + nq > 64) {
+      flush();
+      q = q && !kv_lt(tk, tv, ck, (unsigned)pos);
+      mask = __ballot(q);
+      nq = __popcll(mask);
+    }
+    if (q) {
+      const int at = np + __popcll(mask & below);
+      pk[at] = ck;
+      pv[at] = (unsigned)pos;
+    }
+    np += nq;
+  }
+  if (np > 0) flush();
+  return KV{k, v};
+}
+
+template <bool GRAM, int SEG>
 __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
   __shared__ WsLds S;
   const SolveParams &sp = p.sp;
@@ -663,8 +851,8 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
   u64 *kbuf = bcast + 2 * WS_BCAST_PITCH;
 
   for (int j = tid; j < len; j += WS_BS) {
-    S.f[j] = P.f[base + j];
-    S.a[j] = P.alpha[base + j];
+    S.f[j] = gp(P.f)[base + j];
+    S.a[j] = gp(P.alpha)[base + j];
     S.y[j] = (signed char)ws_label(P, base + j);
   }
   if (tid == 0) S.abort_flag = 0;
@@ -681,33 +869,13 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     const size_t par = (size_t)(round & 1);
     const int side = wave >> 1, half = wave & 1;
     // ---- 1a. this workgroup's two lists: waves 0, 1 take I_up, waves 2, 3 take I_low; each
-    // wave sorts every other chunk of 64 samples and merges them, then the two halves meet.
+    // wave takes every other chunk of 64 samples (own_list), then the two halves meet.
     u64 k = KSENT;
     unsigned v = VSENT;
-    {
-      bool have = false;
-      for (int c = half; c * 64 < len; c += 2) {
-        const int pos = c * 64 + lane;
-        u64 ck = KSENT;
-        unsigned cv = VSENT;
-        if (pos < len) {
-          const double fj = S.f[pos], aj = S.a[pos];
-          const int yj = S.y[pos];
-          if (side == 0 ? ws_in_up(yj, aj, C) : ws_in_low(yj, aj, C)) {
-            ck = f_key(side == 0 ? fj : -fj);
-            cv = (unsigned)pos;
-          }
-        }
-        if (__ballot(ck != KSENT) == 0) continue;
-        wave_sort64(ck, cv);
-        if (!have) {
-          k = ck;
-          v = cv;
-          have = true;
-        } else {
-          wave_merge64(k, v, ck, cv);
-        }
-      }
+    if (owner) {
+      const KV r = own_list(S, side, half, len, h, C);
+      k = r.k;
+      v = r.v;
     }
     if (half == 1) {
       S.lk[wave][lane] = k;
@@ -732,15 +900,15 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     if (owner && P.g1 > 0 && rank % P.g1 == 0) {
       const int g = rank / P.g1;
       const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
-      merge_lists(P.slots + par * P.nwg * WS_LIST_WORDS, side, q0, q0 + half, q1, 2, h, stamp, S.u.st.aux[side],
-                  S.u.st.ab[side], k, v, sp.spin_limit, sp.error, &S.abort_flag);
+      merge_lists<SEG>(P.slots + par * P.nwg * WS_LIST_WORDS, side, q0, q0 + half, q1, 2, h, stamp,
+                       S.u.st.aux[side], S.u.st.ab[side], k, v, sp.spin_limit, sp.error, &S.abort_flag);
       if (half == 1) {
         S.lk[wave][lane] = k;
         S.lv[wave][lane] = v;
       }
       __syncthreads();
       if (half == 0) {
-        wave_merge64(k, v, S.lk[wave + 1][lane], S.lv[wave + 1][lane]);
+        seg_merge<SEG>(k, v, S.lk[wave + 1][lane], S.lv[wave + 1][lane]);
         if (lane < h) {
           const bool ok = k != KSENT;
           put_cand(P.slots2 + (par * P.ng + g) * WS_LIST_WORDS + (size_t)side * 64 * CAND_WORDS, lane, k,
@@ -754,14 +922,14 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       const bool two = P.g1 > 0;
       const u64 *words = two ? P.slots2 + par * P.ng * WS_LIST_WORDS : P.slots + par * P.nwg * WS_LIST_WORDS;
       const int nls = two ? P.ng : P.nwg;
-      merge_lists(words, side, 0, half, nls, 2, h, stamp, S.u.st.aux[side], S.u.st.ab[side], k, v, sp.spin_limit,
-                  sp.error, &S.abort_flag);
+      merge_lists<SEG>(words, side, 0, half, nls, 2, h, stamp, S.u.st.aux[side], S.u.st.ab[side], k, v,
+                       sp.spin_limit, sp.error, &S.abort_flag);
       if (half == 1) {
         S.lk[wave][lane] = k;
         S.lv[wave][lane] = v;
       }
       __syncthreads();
-      if (half == 0) wave_merge64(k, v, S.lk[wave + 1][lane], S.lv[wave + 1][lane]);
+      if (half == 0) seg_merge<SEG>(k, v, S.lk[wave + 1][lane], S.lv[wave + 1][lane]);
     } else if (half == 0 && k != KSENT) {
       // one workgroup: its own lists are the problem's; stage them like merged candidates
       S.u.st.aux[side][v] = ws_aux(base + v, S.y[v]);
@@ -842,8 +1010,8 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       if (GRAM) {
         S.roff[tid] = gb * sp.ld;
       } else {
-        S.bsc[tid] = p.split.scale[gb];
-        S.bnr[tid] = p.split.nrm[gb];
+        S.bsc[tid] = gp(p.split.scale)[gb];
+        S.bnr[tid] = gp(p.split.nrm)[gb];
       }
     }
     if (!GRAM && owner && wave == 0) {
@@ -899,7 +1067,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
           for (int b = 0; b < WS_GATHER; ++b) {
             const int e = min(e0 + b * WS_BS + tid, mm - 1);
             const int ra = e / m, cb = e - ra * m;
-            kv[b] = sp.gram[S.roff[ra] + ws_gmap(P, S.bi[cb])];
+            kv[b] = gp(sp.gram)[S.roff[ra] + ws_gmap(P, S.bi[cb])];
           }
 #pragma unroll
           for (int b = 0; b < WS_GATHER; ++b) {
@@ -951,7 +1119,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
           for (int b = 0; b < WS_GATHER; ++b) {
             const int e = min(e0 + b * WS_BS + tid, ml - 1);
             const int ra = e / len, pos = e - ra * len;
-            kv[b] = sp.gram[S.roff[ra] + ws_gmap(P, base + pos)];
+            kv[b] = gp(sp.gram)[S.roff[ra] + ws_gmap(P, base + pos)];
           }
 #pragma unroll
           for (int b = 0; b < WS_GATHER; ++b) {
@@ -1019,7 +1187,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
             for (int r = r0; r < r1; r += WS_GATHER) {
               float kk[WS_GATHER];
 #pragma unroll
-              for (int e = 0; e < WS_GATHER; ++e) kk[e] = sp.gram[S.nzoff[min(r + e, r1 - 1)] + gj];
+              for (int e = 0; e < WS_GATHER; ++e) kk[e] = gp(sp.gram)[S.nzoff[min(r + e, r1 - 1)] + gj];
 #pragma unroll
               for (int e = 0; e < WS_GATHER; ++e)
                 if (r + e < r1) s = ws_acc(s, S.nzc[r + e], kk[e]);
@@ -1044,8 +1212,8 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
   }
 
   for (int j = tid; j < len; j += WS_BS) {
-    P.f[base + j] = S.f[j];
-    P.alpha[base + j] = S.a[j];
+    gp(P.f)[base + j] = S.f[j];
+    gp(P.alpha)[base + j] = S.a[j];
   }
   if (rank == 0 && tid == 0) {
     ctl->t = t;
@@ -1059,8 +1227,18 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
 }
 
 hipError_t launch_ws_solver(const WsParams &p, int32_t total_wg, hipStream_t s, int32_t *max_coresident) {
-  const void *fn = p.sp.gram ? reinterpret_cast<const void *>(&ws_solve<true>)
-                             : reinterpret_cast<const void *>(&ws_solve<false>);
+  // lists merge in segments of 16, 32 or 64 entries (the smallest that holds q / 2)
+  const int h = p.q / 2;
+  const void *fn;
+  if (h <= 16)
+    fn = p.sp.gram ? reinterpret_cast<const void *>(&ws_solve<true, 16>)
+                   : reinterpret_cast<const void *>(&ws_solve<false, 16>);
+  else if (h <= 32)
+    fn = p.sp.gram ? reinterpret_cast<const void *>(&ws_solve<true, 32>)
+                   : reinterpret_cast<const void *>(&ws_solve<false, 32>);
+  else
+    fn = p.sp.gram ? reinterpret_cast<const void *>(&ws_solve<true, 64>)
+                   : reinterpret_cast<const void *>(&ws_solve<false, 64>);
   int dev = 0, cus = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
