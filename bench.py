@@ -4,12 +4,17 @@
 One step is one pass of the whole hot path over one synthetic workload: RBF Gram build
 (MFMA), the SMO solve to tol, the finalize reduction, and decision values for the test
 split.  Inputs are resident in HBM before the timed region starts.  The default workload is
-the largest single-GPU binary one, 100,000 x 32 with its 40 GB fp32 Gram resident in HBM.
+the largest single-GPU binary one, 100,000 x 32 with its 40 GB fp32 Gram resident in HBM, and
+the solve takes the library's automatic schedule (svm_options.working_set = -1: working-set
+rounds of maximal-violating-pair steps where they beat one pair a step, decided after 128
+rounds; ``schedule`` says which ran).
 
-Prints ONE JSON line.  ``value`` is SMO iterations per second over the timed steps;
+Prints ONE JSON line.  ``value`` is SMO iterations (pair steps) per second over the timed steps;
 ``train_seconds`` is the mean svm_train wall time.  ``roofline`` describes the dominant
-kernel (the persistent SMO solver) against the HBM roofline with the algorithmic bytes of
-an SMO step (two kernel rows 8n, f read+write 16n, status n = 25n bytes).  ``gram_build``
+kernel (the solver that ran) against the HBM roofline with its algorithmic bytes: per SMO step
+of the per-step solver two kernel rows 8n, f read+write 16n, status n = 25n bytes; for the
+working-set rounds 8n per pair step (the rows its f update needs) and 17n per round.
+``pair_solver`` times the per-step solver on the same problem, with its roofline.  ``gram_build``
 reports the Gram precompute against its roofline: the method's n^2 d flops at the dense fp16
 MFMA peak (its contraction runs as split-fp16 products) or its 4 n^2 bytes of stores at the HBM
 peak, whichever takes longer.  ``row_path`` reports the 20,000 x 784
@@ -41,6 +46,9 @@ FP16_MFMA_PEAK_TFLOPS = 2500.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 SOLVER_SOURCES = ("paper_2311_14908_amd/csrc/smo.hip", "paper_2311_14908_amd/csrc/rbf_rows.hpp",
                   "paper_2311_14908_amd/csrc/solver_params.hpp", "paper_2311_14908_amd/csrc/pair_step.hpp")
+WS_SOURCES = ("paper_2311_14908_amd/csrc/ws_smo.hip", "paper_2311_14908_amd/csrc/ws_record.hpp",
+              "paper_2311_14908_amd/csrc/solver_params.hpp", "paper_2311_14908_amd/csrc/pair_step.hpp",
+              "paper_2311_14908_amd/csrc/common.hpp")
 
 
 def counters_path(n, d):
@@ -61,6 +69,24 @@ def counter_bytes_per_step(workload_name, n, d):
     for p in SOLVER_SOURCES:
         h.update(open(os.path.join(ROOT, p), "rb").read())
     if rec.get("solver_sources_sha256") != h.hexdigest() or rec.get("workload") != workload_name:
+        return None
+    return rec
+
+
+def ws_counter_bytes(workload_name, n, d):
+    """HBM bytes per working-set round from rocprofv3 FETCH_SIZE/WRITE_SIZE, as recorded in
+    profiles/ for the working-set solver; None when missing, for another workload, or stale."""
+    import hashlib
+    try:
+        path = os.path.join(ROOT, "profiles", f"ws_solve_n{n}_d{d}_hbm_counters.md")
+        line = [l for l in open(path) if "ws_sources_sha256" in l][0]
+        rec = json.loads(line.strip())
+    except (OSError, IndexError, ValueError):
+        return None
+    h = hashlib.sha256()
+    for p in WS_SOURCES:
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    if rec.get("ws_sources_sha256") != h.hexdigest() or rec.get("workload") != workload_name:
         return None
     return rec
 
@@ -98,6 +124,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (0..3 binary)")
     ap.add_argument("--gram", choices=["auto", "on", "off"], default="auto")
+    ap.add_argument("--working-set", type=int, default=-1,
+                    help="svm_options.working_set of the timed trainings: -1 = automatic (rounds where they "
+                         "beat the per-step solver, decided after 128 rounds), 0 = per-step solver, q = rounds of q")
     ap.add_argument("--row-path-steps", type=int, default=4000, help="SMO steps of the row-path measurement (0 = skip)")
     ap.add_argument("--row-large-n", type=int, default=300_000,
                     help="samples of the large row-path measurement (workload 1's recipe, X far larger than the "
@@ -153,7 +182,7 @@ def main():
     torch.cuda.synchronize()
 
     def step():
-        out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=gram_mode)
+        out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=gram_mode, working_set=args.working_set)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         dec = svmx.svm_predict(Xd, yd, out.alpha, out.b, wl.gamma, Xtd)
@@ -176,12 +205,28 @@ def main():
     acc = float(np.mean(np.where(dec > 0, 1, -1) == yt))
     launches = sum(s["launches"] for s in st)
     t_kernel = sum(s["t_kernel"] for s in st)
-    step_bytes = 25.0 * n
-    solver_gbps = step_bytes * iters / t_kernel / 1e9
-    counters = counter_bytes_per_step(wl.name, n, d)
+    rounds = sum(s["rounds"] for s in st)
+    schedule = st[0]["schedule"]
     gram_used = bool(st[0]["gram_used"])
-    traffic = (counters["gram_path_hbm_bytes_per_smo_step"] * iters / launches
-               if counters and gram_used else None)
+    if schedule == 1:
+        # working-set rounds: per pair step two kernel rows (8n, the rows the f update needs), per
+        # round f read and written and the status (17n)
+        solver_bytes = 8.0 * n * iters + 17.0 * n * rounds
+        kname = "ws_solve"
+        counters = ws_counter_bytes(wl.name, n, d)
+        traffic = counters["ws_solve_hbm_bytes_per_round"] * rounds / launches if counters else None
+        note = ("working-set rounds: bound by the latency of the round's chain (own lists, two merge levels, "
+                "K_BB, the pair steps in one wave, the f update), not by HBM bandwidth")
+    else:
+        # per-step solver: two kernel rows 8n, f read+write 16n, status n per SMO step
+        solver_bytes = 25.0 * n * iters
+        kname = "smo_solve"
+        counters = counter_bytes_per_step(wl.name, n, d)
+        traffic = (counters["gram_path_hbm_bytes_per_smo_step"] * iters / launches
+                   if counters and gram_used else None)
+        note = ("a step moves 25n algorithmic bytes but is bound by latency: the cross-workgroup exchange of the "
+                "selections and the dependent read of the two Gram rows")
+    solver_gbps = solver_bytes / t_kernel / 1e9
 
     result = {
         "metric": "SMO iterations/sec + train seconds; kernel-row HBM GB/s vs peak",
@@ -197,20 +242,23 @@ def main():
         "dtype": "f32 kernel values (Gram contraction: split-fp16 x3 MFMA products, fp32 accumulation), f64 solve",
         "data": "synthetic (seeded), resident in HBM",
         "config": {"workload": f"{wl.name}: binary RBF-SVM, C={wl.C:g}, gamma={wl.gamma:g}, tol={wl.tol:g}",
-                   "n": n, "d": d, "m_test": m, "gram": bool(st[0]["gram_used"])},
+                   "n": n, "d": d, "m_test": m, "gram": bool(st[0]["gram_used"]), "working_set": args.working_set},
         "train_seconds": mean("t_total"),
         "iterations_per_step": iters / args.steps,
         "phases_s": {"upload": mean("t_upload"), "gram": mean("t_gram"), "solve": mean("t_solve"), "solver_kernel": t_kernel / args.steps,
                      "finalize": mean("t_finalize"), "predict": float(np.mean(t_pred))},
         "n_sv": st[-1]["n_sv"], "n_bound_sv": st[-1]["n_bound_sv"], "dual_obj": st[-1]["dual_obj"],
         "test_accuracy": acc,
-        "roofline": {"kernel": "smo_solve", "bound": "hbm", "achieved": solver_gbps, "peak": HBM_PEAK_GBPS,
+        "schedule": {0: "per-step solver", 1: "working-set rounds", 2: "working-set probe, then per-step solver"}[schedule],
+        "working_set_rounds": rounds / args.steps,
+        "roofline": {"kernel": kname, "bound": "hbm", "achieved": solver_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": solver_gbps / HBM_PEAK_GBPS, "traffic": traffic,
-                     "bytes_per_step": step_bytes, "launch_avg_ms": 1e3 * t_kernel / launches,
+                     "bytes": solver_bytes / launches, "bytes_per_launch_rule":
+                         "8n per pair step + 17n per round" if schedule == 1 else "25n per SMO step",
+                     "launch_avg_ms": 1e3 * t_kernel / launches,
                      "us_per_smo_step": 1e6 * t_kernel / iters,
-                     "note": "a step moves 25n algorithmic bytes but is bound by latency: the "
-                             "cross-workgroup exchange of the selections and the dependent read of "
-                             "the two Gram rows"},
+                     "us_per_round": 1e6 * t_kernel / rounds if rounds else None,
+                     "note": note},
         # the default Gram runs the fp32 contraction as three fp16 MFMA products per fp32 product
         # (split halves) on the fp16 MFMA instruction, so its peak is the dense fp16 one; the
         # achieved rate counts the method's n^2 d flops (symmetric), not the executed products
@@ -240,6 +288,29 @@ def main():
                              "note": "pinned host X and y copied in, trained, alpha copied out; PCIe "
                                      "included; not the headline value"}
     del Xd2, yd2, Xh, yh, ah
+
+    # The per-step solver (one maximal violating pair a step, svm_options.working_set = 0) on the same
+    # problem: the method step by step, with the roofline of its kernel.
+    if args.working_set != 0:
+        svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=gram_mode)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        pr = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=gram_mode)
+        torch.cuda.synchronize()
+        tpr = time.perf_counter() - t1
+        ps_ = pr.stats
+        pb = 25.0 * n * ps_["iterations"]
+        pc = counter_bytes_per_step(wl.name, n, d)
+        ptraffic = (pc["gram_path_hbm_bytes_per_smo_step"] * ps_["iterations"] / ps_["launches"]
+                    if pc and ps_["gram_used"] else None)
+        result["pair_solver"] = {"kernel": "smo_solve", "train_seconds": tpr, "smo_iterations": ps_["iterations"],
+                                 "iters_per_s": ps_["iterations"] / tpr, "bound": "hbm",
+                                 "achieved": pb / ps_["t_kernel"] / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                 "frac": pb / ps_["t_kernel"] / 1e9 / HBM_PEAK_GBPS, "traffic": ptraffic,
+                                 "bytes_per_step": 25.0 * n, "launch_avg_ms": 1e3 * ps_["t_kernel"] / ps_["launches"],
+                                 "us_per_smo_step": 1e6 * ps_["t_kernel"] / ps_["iterations"],
+                                 "dual_obj": ps_["dual_obj"]}
+        del pr
 
     # The row path on the 20,000 x 784 workload (where the kernel-row GEMV is the step's work) and on
     # the same recipe at 300,000 x 784.
@@ -365,16 +436,17 @@ def main():
             wk = synth.workload(cid)
             Xk, yk, _, _ = synth.generate(cid, m=1)
             Xkd, ykd = torch.from_numpy(Xk).cuda(), torch.from_numpy(yk).cuda()
-            svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol)
+            svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, working_set=args.working_set)
             torch.cuda.synchronize()
             t1 = time.perf_counter()
-            rk = svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol)
+            rk = svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, working_set=args.working_set)
             torch.cuda.synchronize()
             tk = time.perf_counter() - t1
             sk = rk.stats
             nk = Xk.shape[0]
             gb = 25.0 * nk * sk["iterations"] / sk["t_kernel"] / 1e9
-            per[wk.name] = {"train_seconds": tk, "smo_iterations": sk["iterations"],
+            per[wk.name] = {"train_seconds": tk, "smo_iterations": sk["iterations"], "schedule": sk["schedule"],
+                            "rounds": sk["rounds"],
                             "iters_per_s": sk["iterations"] / sk["t_solve"], "gram_seconds": sk["t_gram"],
                             "us_per_smo_step": 1e6 * sk["t_kernel"] / sk["iterations"], "gram_used": sk["gram_used"],
                             "solver_GBps": gb, "solver_frac_of_hbm_peak": gb / HBM_PEAK_GBPS}
@@ -395,7 +467,7 @@ def main():
             Xk, yk, _, _ = synth.generate(cid, m=1)
             Xkd, ykd = torch.from_numpy(Xk).cuda(), torch.from_numpy(yk).cuda()
             ent = {}
-            for q in [0] + qs:
+            for q in [0] + qs + [-1]:
                 svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, gram=svmx.GRAM_ON, working_set=q)
                 torch.cuda.synchronize()
                 t1 = time.perf_counter()
@@ -403,8 +475,9 @@ def main():
                 torch.cuda.synchronize()
                 tk = time.perf_counter() - t1
                 sk = rk.stats
-                ent["pair" if q == 0 else f"q{q}"] = {
+                ent["pair" if q == 0 else ("auto" if q < 0 else f"q{q}")] = {
                     "train_seconds": tk, "smo_iterations": sk["iterations"], "rounds": sk["rounds"],
+                    "schedule": sk["schedule"], "us_per_round": 1e6 * sk["t_kernel"] / sk["rounds"] if sk["rounds"] else None,
                     "iters_per_s": sk["iterations"] / sk["t_solve"], "solver_kernel_seconds": sk["t_kernel"],
                     "dual_obj": sk["dual_obj"]}
                 del rk
@@ -415,7 +488,7 @@ def main():
                 # the same problem without a Gram: pair steps evaluate two rows of K from X a
                 # step, working-set rounds evaluate K(B, .) for all of B in one pass a round
                 rent = {}
-                for q in [0] + [v for v in qs if v <= 128]:
+                for q in [0] + [v for v in qs if v <= 128] + [-1]:
                     kw = dict(gram=svmx.GRAM_OFF, working_set=q)
                     svmx.svm_train(Xkd, ykd, wk.C, wk.gamma, wk.tol, **kw)
                     torch.cuda.synchronize()
@@ -424,8 +497,9 @@ def main():
                     torch.cuda.synchronize()
                     tk = time.perf_counter() - t1
                     sk = rk.stats
-                    rent["pair" if q == 0 else f"q{q}"] = {
+                    rent["pair" if q == 0 else ("auto" if q < 0 else f"q{q}")] = {
                         "train_seconds": tk, "smo_iterations": sk["iterations"], "rounds": sk["rounds"],
+                        "schedule": sk["schedule"],
                         "iters_per_s": sk["iterations"] / sk["t_solve"], "dual_obj": sk["dual_obj"]}
                     del rk
                 for key, e in rent.items():

@@ -82,6 +82,8 @@ typedef enum {
                                  before l is known); not with working_set */
 } svm_selection;
 
+#define SVM_WORKING_SET_AUTO (-1) /* svm_options.working_set: decided per problem (see there) */
+
 typedef struct {
   int32_t struct_size;       /* = sizeof(svm_options); set by svm_default_options */
   int32_t gram;              /* svm_gram_mode */
@@ -102,7 +104,16 @@ typedef struct {
                                 (two levels above 128 workgroups per problem) */
   int32_t gram_mfma;         /* svm_gram_mfma */
   int32_t working_set;       /* 0 = one maximal violating pair per step with f updated every step
-                                (Section III.B).  q = 2..128, even: working-set rounds -- B = the
+                                (Section III.B).  SVM_WORKING_SET_AUTO (-1): binary training with
+                                the first-order rule, no trace and automatic workgroups, n > 4096:
+                                rounds of q = 128 (rows of 256 features or more) or 32 for the first
+                                128 rounds, continued if they took at least as many pair steps per
+                                round as a round costs (Gram path: 25 at q = 128, 6.5 at 32; row
+                                path: 15 and 7, measured on MI355X), else the per-step solver
+                                takes over from their state (svm_stats.schedule says which); every
+                                other case per-step.  Deterministic: the rule reads the state after
+                                a fixed number of rounds, not the host check cadence.
+                                q = 2..128, even: working-set rounds -- B = the
                                 q/2 smallest f of I_up and the q/2 largest of I_low (ties to the
                                 smaller index), pair steps on B alone until its gap is at most
                                 max(tol, 0.5 x the round's gap) or 100 q steps, then f updated once
@@ -135,7 +146,8 @@ typedef struct {
                            the launch stream) */
   int64_t rounds;       /* working-set rounds (0 for the per-step solver) */
   int32_t resident_rows; /* rows of X each solver workgroup kept in LDS (binary row path) */
-  int32_t reserved;
+  int32_t schedule;     /* binary training: 0 = per-step solver, 1 = working-set rounds, 2 = rounds
+                           (the automatic probe), then the per-step solver */
   double t_upload;      /* seconds of input validation and staging before the precompute: the
                            labels copied to the host and checked (one-vs-one: and class-sorted),
                            the problem descriptors copied to the device, the device-side scan of X

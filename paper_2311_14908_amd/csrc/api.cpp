@@ -52,6 +52,18 @@ constexpr int64_t LDS_BYTES = 160 * 1024;
 constexpr int32_t MAX_CLASSES = 64;
 constexpr double WS_FRAC = 0.5;           // working-set rounds stop at max(tol, 0.5 x the round's gap)
 constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
+// working_set = SVM_WORKING_SET_AUTO: q = 128 for rows of 256 features or more, else 32; the
+// first WS_AUTO_PROBE_ROUNDS rounds decide.  The rounds go on when they took at least as many
+// pair steps per round as a round costs in pair steps (measured on MI355X: a round of q = 32
+// costs about 6 pair steps on the Gram path -- 32 us against 5.4 at 100,000 x 32, 26 against
+// 4.6 at 50,000 x 128 -- and about 7 on the row path -- 58 us against 8.3 at 100,000 x 32; one
+// of q = 128 about 23 on the Gram path -- 94 us against 4.1 at 20,000 x 784 -- and 13 on the
+// row path), else the pair solver takes over from the state the rounds reached.
+constexpr int64_t WS_AUTO_PROBE_ROUNDS = 128;
+double ws_auto_min_steps(int32_t q, bool gram) {
+  if (q >= 128) return gram ? 25.0 : 15.0;
+  return gram ? 6.5 : 7.0;
+}
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
@@ -98,8 +110,8 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
   r->resident_rows = o->resident_rows;
   r->selection = o->selection;
   if (o->reserved != 0 || (r->selection != SVM_SELECT_MVP && r->selection != SVM_SELECT_SECOND_ORDER)) return false;
-  if (r->selection == SVM_SELECT_SECOND_ORDER && r->working_set != 0) return false;
-  const bool ws_ok = r->working_set == 0 ||
+  if (r->selection == SVM_SELECT_SECOND_ORDER && r->working_set > 0) return false;
+  const bool ws_ok = r->working_set == 0 || r->working_set == SVM_WORKING_SET_AUTO ||
                      (r->working_set >= 2 && r->working_set <= ws_q_max() && r->working_set % 2 == 0);
   return r->gram >= SVM_GRAM_AUTO && r->gram <= SVM_GRAM_OFF && r->levels >= 0 && r->levels <= 2 &&
          (r->gram_mfma == SVM_MFMA_SPLIT_F16 || r->gram_mfma == SVM_MFMA_F32) && ws_ok && r->resident_rows >= -1;
@@ -204,6 +216,10 @@ struct TrainPlan {
   bool gram;
   int64_t ld;
   Shape shape;
+  int32_t working_set;   // q of the working-set rounds (0: pair steps only)
+  int32_t auto_q;        // working_set = AUTO chose rounds of q: probe them, maybe switch
+  double auto_min_steps; // pair steps per round the probe must reach to keep the rounds
+  Shape pair_shape;      // the pair solver's shape, for a switch
   int32_t cache_cap;
   int64_t off_f, off_gram, off_split, off_sqn, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2,
       off_tul, off_tb, off_fin, off_err, off_rounds;
@@ -211,7 +227,8 @@ struct TrainPlan {
   int64_t total;
 };
 
-svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
+svm_status plan_train(int64_t n, int64_t d, const Opts &o_in, TrainPlan *p) {
+  Opts o = o_in;
   if (n < 2 || d < 1) return fail(SVM_EINVAL, "need n >= 2 and d >= 1 (got n=%lld, d=%lld)", (long long)n, (long long)d);
   if (n > 0x7ffffffeLL) return fail(SVM_ENOMEM, "n=%lld exceeds the 32-bit sample index", (long long)n);
   if (d > (INT64_MAX / 8) / n) return fail(SVM_EINVAL, "n*d overflows 64-bit byte counts");
@@ -227,6 +244,23 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   if (o.selection == SVM_SELECT_SECOND_ORDER && !p->gram)
     return fail(SVM_EINVAL, "second-order selection needs the Gram path (the Gram does not fit gram_budget_bytes, "
                             "or gram = SVM_GRAM_OFF)");
+  p->auto_q = 0;
+  p->auto_min_steps = 0.0;
+  if (o.working_set == SVM_WORKING_SET_AUTO) {
+    // rounds only where a problem spreads over several workgroups, with the first-order rule,
+    // no trace (a trace records pair steps) and the automatic workgroup count
+    o.working_set = 0;
+    const int32_t q = d >= 256 ? 128 : 32;
+    Shape ws;
+    if (o.selection == SVM_SELECT_MVP && o.trace_len == 0 && o.workgroups == 0 && n > 4096 &&
+        choose_ws_shape(n, 0, q, p->gram, &ws) && ws.nwg > 1) {
+      o.working_set = q;
+      p->auto_q = q;
+      p->auto_min_steps = ws_auto_min_steps(q, p->gram);
+      if (!choose_shape(n, p->gram, 0, o.levels, &p->pair_shape)) return fail(SVM_ENOMEM, "problem too large to place");
+    }
+  }
+  p->working_set = o.working_set;
   if (o.working_set > 0) {
     if (!choose_ws_shape(n, o.workgroups, o.working_set, p->gram, &p->shape))
       return fail(SVM_ENOMEM, "n=%lld exceeds the working-set solver's %d workgroups of %d samples", (long long)n,
@@ -252,7 +286,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o, TrainPlan *p) {
   p->off_tags = p->cache_cap ? L.add(4LL * p->cache_cap * p->shape.nwg) : -1;
   p->off_ctl = L.add(sizeof(Ctl));
   p->off_prob = L.add(sizeof(Prob));
-  p->off_wgp = L.add(4LL * (p->shape.nwg + 1));
+  p->off_wgp = L.add(4LL * std::max(p->shape.nwg + 1, p->auto_q ? p->pair_shape.nwg : 0));
   const int64_t per_rec = o.working_set > 0 ? ws_list_words() : SLOT_WORDS;
   p->slot_words = 2LL * p->shape.nwg * per_rec;
   p->slot2_words = 2LL * std::max(1, p->shape.ng) * per_rec + (o.working_set > 0 ? ws_bcast_words() : 0);
@@ -298,15 +332,19 @@ struct Timer {
   }
 };
 
-// Launch a solver (launch(&max_coresident) enqueues one launch) until no problem is running.
-// Returns SVM_OK or a negative status.
-template <class Launch>
+struct NeverStop {
+  bool operator()() const { return false; }
+};
+
+// Launch a solver (launch(&max_coresident) enqueues one launch) until no problem is running,
+// or until stop() says so after a launch.  Returns SVM_OK or a negative status.
+template <class Launch, class Stop = NeverStop>
 svm_status run_launches(Launch launch, int32_t *error, int32_t nprob, int32_t total_wg, Ctl *d_ctl, hipStream_t stream,
-                        int32_t *launches, std::vector<Ctl> &h, double *t_kernel, bool timed = true) {
+                        int32_t *launches, std::vector<Ctl> &h, double *t_kernel, bool timed = true,
+                        Stop stop = Stop()) {
   int32_t herr = 0;
   Timer tk;
   HIPCHK(tk.init(timed));
-  *t_kernel = 0.0;
   h.assign(nprob, Ctl{});
   std::vector<int64_t> prev(nprob, -1);
   for (;;) {
@@ -334,9 +372,11 @@ svm_status run_launches(Launch launch, int32_t *error, int32_t nprob, int32_t to
     }
     if (!running) return SVM_OK;
     if (!progress) return fail(SVM_EDEVICE, "solver made no progress");
+    if (stop()) return SVM_OK;
   }
 }
 
+// (*t_kernel accumulates over the calls of one training.)
 svm_status run_solver(SolveParams sp, int32_t nprob, int32_t total_wg, int32_t per_thread, bool gram, Ctl *d_ctl,
                       hipStream_t stream, int32_t *launches, std::vector<Ctl> &h, double *t_kernel,
                       bool timed = true) {
@@ -604,8 +644,8 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
   hp.per_wg = p.shape.per_wg;
   hp.g1 = p.shape.g1;
   hp.ng = p.shape.ng;
-  hp.slots2 = (p.shape.g1 || r.working_set > 0) ? reinterpret_cast<u64 *>(ws + p.off_slots2) : nullptr;
-  std::vector<int32_t> hwgp(p.shape.nwg + 1, 0);
+  hp.slots2 = (p.shape.g1 || p.working_set > 0) ? reinterpret_cast<u64 *>(ws + p.off_slots2) : nullptr;
+  std::vector<int32_t> hwgp(std::max(p.shape.nwg + 1, p.auto_q ? p.pair_shape.nwg : 0), 0);
   HIPCHK(hipMemcpyAsync(dprob, &hp, sizeof(Prob), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemcpyAsync(wgp, hwgp.data(), 4 * hwgp.size(), hipMemcpyHostToDevice, stream));
   HIPCHK(hipMemsetAsync(err, 0, 16, stream));
@@ -625,7 +665,7 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
     HIPCHK(launch_gram_split(X, n, d, (float)gamma, G, p.ld, ws + p.off_split, stream));
   else if (p.gram)
     HIPCHK(launch_gram(X, n, d, (float)gamma, G, p.ld, stream));
-  else if (r.working_set > 0)
+  else if (p.working_set > 0)
     HIPCHK(launch_split_rows(X, n, d, split_views(ws + p.off_split, n, d), stream));
   else
     HIPCHK(launch_row_norms(X, n, d, sqn, stream));
@@ -652,12 +692,21 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
   sp.max_per_wg = p.shape.per_wg;
   sp.second_order = r.selection == SVM_SELECT_SECOND_ORDER ? 1 : 0;
   sp.res_rows = 0;
-  if (!p.gram && r.working_set == 0 && r.resident_rows >= 0) {
-    const int64_t fit = solver_res_rows_max(sp, p.shape.per_thread);
-    if (fit < 0) return fail(SVM_EDEVICE, "row path: LDS capacity query failed");
-    int64_t res = std::min<int64_t>(fit, p.shape.per_wg);
-    if (r.resident_rows > 0) res = std::min<int64_t>(res, r.resident_rows);
-    sp.res_rows = (int32_t)res;
+  // row path of the pair solver: rows of X each workgroup keeps in LDS
+  auto resident = [&](SolveParams &q, const Shape &sh) -> svm_status {
+    q.res_rows = 0;
+    if (!p.gram && r.resident_rows >= 0) {
+      const int64_t fit = solver_res_rows_max(q, sh.per_thread);
+      if (fit < 0) return fail(SVM_EDEVICE, "row path: LDS capacity query failed");
+      int64_t res = std::min<int64_t>(fit, sh.per_wg);
+      if (r.resident_rows > 0) res = std::min<int64_t>(res, r.resident_rows);
+      q.res_rows = (int32_t)res;
+    }
+    return SVM_OK;
+  };
+  if (p.working_set == 0) {
+    s0 = resident(sp, p.shape);
+    if (s0 != SVM_OK) return s0;
   }
   sp.spin_limit = spin_ticks();
   sp.error = err;
@@ -666,7 +715,9 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
   double t_kernel = 0.0;
   int64_t *d_rounds = reinterpret_cast<int64_t *>(ws + p.off_rounds);
   svm_status s1;
-  if (r.working_set > 0) {
+  int32_t schedule = p.working_set > 0 ? 1 : 0;  // svm_stats.schedule
+  int64_t h_rounds = 0;
+  if (p.working_set > 0) {
     HIPCHK(hipMemsetAsync(slots, 0, 8 * p.slot_words, stream));
     HIPCHK(hipMemsetAsync(ws + p.off_slots2, 0, 8 * p.slot2_words, stream));
     HIPCHK(hipMemsetAsync(d_rounds, 0, 8, stream));
@@ -674,21 +725,65 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
     wp.sp = sp;
     wp.rounds = d_rounds;
     wp.frac = WS_FRAC;
-    wp.q = r.working_set;
-    wp.max_inner = WS_INNER_PER_Q * r.working_set;
+    wp.q = p.working_set;
+    wp.max_inner = WS_INNER_PER_Q * p.working_set;
+    wp.round_end = INT64_MAX;
     if (!p.gram) {
       wp.split = split_views(ws + p.off_split, n, d);
       wp.cexp = (float)(-gamma * 1.4426950408889634);
     }
     const int32_t nwg = p.shape.nwg + (p.shape.nwg > 1 ? 1 : 0);  // owners and the solving workgroup
-    s1 = run_launches([&](int32_t *maxres) { return launch_ws_solver(wp, nwg, stream, maxres); }, err, 1, nwg, ctl,
-                      stream, &launches, hc, &t_kernel, timed);
+    auto ws_launch = [&](int32_t *maxres) { return launch_ws_solver(wp, nwg, stream, maxres); };
+    bool go_on = true;
+    if (p.auto_q) {
+      // the probe: the first WS_AUTO_PROBE_ROUNDS rounds (in as many launches as the host check
+      // cadence makes), then the rule
+      wp.round_end = WS_AUTO_PROBE_ROUNDS;
+      auto probed = [&]() {
+        if (hipMemcpy(&h_rounds, d_rounds, 8, hipMemcpyDeviceToHost) != hipSuccess) return true;
+        return h_rounds >= WS_AUTO_PROBE_ROUNDS;
+      };
+      s1 = run_launches(ws_launch, err, 1, nwg, ctl, stream, &launches, hc, &t_kernel, timed, probed);
+      if (s1 != SVM_OK) return s1;
+      if (hc[0].status == ST_RUNNING) {
+        HIPCHK(hipMemcpy(&h_rounds, d_rounds, 8, hipMemcpyDeviceToHost));
+        go_on = (double)hc[0].t >= p.auto_min_steps * (double)h_rounds;
+      } else {
+        go_on = false;  // solved within the probe
+      }
+      wp.round_end = INT64_MAX;
+    }
+    if (go_on) {
+      s1 = run_launches(ws_launch, err, 1, nwg, ctl, stream, &launches, hc, &t_kernel, timed);
+    } else if (hc[0].status == ST_RUNNING) {
+      // the pair solver takes over from the state the rounds left: f and alpha in the workspace
+      // and the caller's alpha, the step count in the control block.  Its exchange words are
+      // stamped so that no current stamp matches them (the next two steps read stamps t + 1
+      // and t + 2); the row path gets its squared row norms.
+      schedule = 2;
+      const Shape &sh = p.pair_shape;
+      hp.nwg = sh.nwg;
+      hp.per_wg = sh.per_wg;
+      hp.g1 = sh.g1;
+      hp.ng = sh.ng;
+      hp.slots2 = reinterpret_cast<u64 *>(ws + p.off_slots2);
+      HIPCHK(hipMemcpyAsync(dprob, &hp, sizeof(Prob), hipMemcpyHostToDevice, stream));
+      const uint32_t stale = (uint32_t)((hc[0].t + 9) & 15) << 28;
+      HIPCHK(hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(slots), stale, 2 * p.slot_words, stream));
+      HIPCHK(hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(ws + p.off_slots2), stale, 2 * p.slot2_words, stream));
+      if (!p.gram) HIPCHK(launch_row_norms(X, n, d, sqn, stream));
+      sp.max_per_wg = sh.per_wg;
+      s0 = resident(sp, sh);
+      if (s0 != SVM_OK) return s0;
+      s1 = run_solver(sp, 1, sh.nwg, sh.per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel, timed);
+    } else {
+      s1 = SVM_OK;
+    }
   } else {
     s1 = run_solver(sp, 1, p.shape.nwg, p.shape.per_thread, p.gram, ctl, stream, &launches, hc, &t_kernel, timed);
   }
   if (s1 != SVM_OK) return s1;
-  int64_t h_rounds = 0;
-  HIPCHK(hipMemcpyAsync(&h_rounds, d_rounds, 8, hipMemcpyDeviceToHost, stream));
+  if (p.working_set > 0) HIPCHK(hipMemcpyAsync(&h_rounds, d_rounds, 8, hipMemcpyDeviceToHost, stream));
   HIPCHK(ts.stop(stream));
 
   HIPCHK(tf.start(stream));
@@ -697,7 +792,7 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
   HIPCHK(hipMemcpyAsync(hfin, fin, sizeof(hfin), hipMemcpyDeviceToHost, stream));
   HIPCHK(hipStreamSynchronize(stream));
   if (r.trace_len) {
-    const int64_t steps = std::min<int64_t>(r.trace_len, (r.working_set > 0 ? h_rounds : hc[0].t) + 1);
+    const int64_t steps = std::min<int64_t>(r.trace_len, (p.working_set > 0 ? h_rounds : hc[0].t) + 1);
     if (r.trace_ws) HIPCHK(hipMemcpyAsync(r.trace_ws, tul, 4 * 2 * steps, hipMemcpyDeviceToHost, stream));
     if (r.trace_b) HIPCHK(hipMemcpyAsync(r.trace_b, tb, 8 * 2 * steps, hipMemcpyDeviceToHost, stream));
   }
@@ -721,9 +816,9 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
     st->t_finalize = tf.seconds();
     st->t_total = std::chrono::duration<double>(std::chrono::steady_clock::now() - t_start).count();
     st->t_kernel = t_kernel;
-    st->rounds = r.working_set > 0 ? h_rounds : 0;
+    st->rounds = p.working_set > 0 ? h_rounds : 0;
     st->resident_rows = sp.res_rows;
-    st->reserved = 0;
+    st->schedule = schedule;
     st->t_upload = t_upload;
   }
   return c.status == ST_MAXITER ? SVM_NOT_CONVERGED : SVM_OK;
@@ -996,7 +1091,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
       S.t_kernel = t_kernel;
       S.rounds = 0;
       S.resident_rows = 0;
-      S.reserved = 0;
+      S.schedule = 0;
       S.t_upload = t_upload;
     }
   }

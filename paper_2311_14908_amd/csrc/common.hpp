@@ -99,6 +99,7 @@ struct WsParams {
   SplitX split;      // row path (sp.gram == NULL): split-fp16 rows of X, scales and norms
   float cexp;        // row path: -gamma * log2(e)
   int32_t pad;
+  int64_t round_end; // a launch also ends once this many rounds are done
 };
 hipError_t launch_ws_solver(const WsParams &p, int32_t total_wg, hipStream_t s, int32_t *max_coresident);
 int ws_slice_max();

@@ -14,10 +14,11 @@
 //      q/2 of the I_up list, then those of the first q/2 of the I_low list that are not
 //      already in B.
 //   2. stop rule on the heads of the two lists, which are the maximal violating pair.
-//   3. the solving workgroup gathers K_BB from the Gram into LDS, runs the pair steps on B in
-//      one wave until the gap on B is at most max(tol, frac * gap of the round) or the round's
-//      step cap is reached, and publishes the new multipliers of B; meanwhile every owner
-//      loads the Gram rows of B over its own samples into LDS;
+//   3. the owners fetch K_BB from the Gram between them and publish it; the solving workgroup
+//      collects it into LDS, runs the pair steps on B in one wave until the gap on B is at most
+//      max(tol, frac * gap of the round) or the round's step cap is reached, and publishes the
+//      new multipliers of B; meanwhile every owner loads the Gram rows of B over its own
+//      samples into LDS;
 //   4. every owner adds sum_p c_p K(B_p, j) to f_j of its own samples (c_p the change of a y
 //      at B_p, in a fixed grouping of B's order) and stores the new multipliers of its
 //      members of B.
@@ -845,9 +846,9 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
   const int64_t base = owner ? (int64_t)rank * P.per_wg : 0;
   const int len = owner ? (int)min<int64_t>(P.per_wg, P.n - base) : 0;
   u64 *bcast = P.slots2 + 2 * (size_t)P.ng * WS_LIST_WORDS;
-  // row path: K_BB as published by the owners, [2][WS_QMAX][WS_QMAX] words of (32-bit round
-  // stamp, fp32 bits) -- 32-bit stamps, so a word of an earlier round never passes for a
-  // current one, whichever entries a round leaves untouched
+  // K_BB as published by the owners, [2][WS_QMAX][WS_QMAX] words of (32-bit round stamp, fp32
+  // bits) -- 32-bit stamps, so a word of an earlier round never passes for a current one,
+  // whichever entries a round leaves untouched
   u64 *kbuf = bcast + 2 * WS_BCAST_PITCH;
 
   for (int j = tid; j < len; j += WS_BS) {
@@ -998,10 +999,10 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     if (status != ST_RUNNING) break;
 
     // ---- 3. the pair steps on B: K_BB into LDS, then one wave of the solving workgroup.
-    // Gram path: the solving workgroup gathers K_BB from the Gram while the owners load the
-    // Gram rows of B over their own samples.  Row path: every owner evaluates K(B, own
-    // samples) and publishes the columns of K_BB of its own members of B; the solving
-    // workgroup collects them.
+    // Gram path: the owners fetch K_BB from the Gram between them and publish it, then load the
+    // Gram rows of B over their own samples while the pair steps run.  Row path: every owner
+    // evaluates K(B, own samples) and publishes the columns of K_BB of its own members of B.
+    // The solving workgroup collects K_BB.
     const bool rows_in_lds = GRAM ? owner && !solo && m * len <= WS_QMAX * WS_QMAX : owner;
     const size_t kpar = par * (size_t)(WS_QMAX * WS_QMAX);
     const unsigned kstamp = (unsigned)(round + 1);
@@ -1026,7 +1027,19 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       if (lane == 0) S.nown = cnt;
     }
     __syncthreads();
-    if (solver && !GRAM) {
+    // Gram path with several owners: the owners fetch K_BB between them (owner r the entries
+    // r, r + nwg, ...) and publish it as the row path does, since one workgroup alone can keep
+    // only so many scattered reads in flight.
+    const bool kdist = GRAM && !solo;
+    if (kdist && owner) {
+      const int mm = m * m;
+      for (int e = rank + tid * P.nwg; e < mm; e += WS_BS * P.nwg) {
+        const int ra = e / m, cb = e - ra * m;
+        const float kv = gp(sp.gram)[S.roff[ra] + ws_gmap(P, S.bi[cb])];
+        st_word(kbuf + kpar + (size_t)ra * WS_QMAX + cb, ((u64)kstamp << 32) | (u64)__float_as_uint(kv));
+      }
+    }
+    if (solver && (!GRAM || kdist)) {
       // wait for every published entry of K_BB, WS_GATHER per thread at a time
       const int mm = m * m;
       for (int e0 = 0; e0 < mm; e0 += WS_BS * WS_GATHER) {
@@ -1057,9 +1070,9 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       }
     }
     if (solver) {
-      if (GRAM) {
-        // K_BB: flat indices clamped to the last element, so the loads of a batch issue back
-        // to back; only the stores are guarded
+      if (GRAM && !kdist) {
+        // one workgroup: K_BB from the Gram; flat indices clamped to the last element, so the
+        // loads of a batch issue back to back; only the stores are guarded
         const int mm = m * m;
         for (int e0 = 0; e0 < mm; e0 += WS_BS * WS_GATHER) {
           float kv[WS_GATHER];
@@ -1208,7 +1221,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       status = ST_TIMEOUT;
       break;
     }
-    if (t >= t_end) break;  // launch budget spent: the state is whole at a round boundary
+    if (t >= t_end || round >= p.round_end) break;  // launch budget spent: the state is whole at a round boundary
   }
 
   for (int j = tid; j < len; j += WS_BS) {

@@ -22,6 +22,7 @@ SVM_EINVAL, SVM_ENOMEM, SVM_EDEVICE, SVM_EWORKSPACE = -1, -2, -3, -4
 GRAM_AUTO, GRAM_ON, GRAM_OFF = 0, 1, 2
 MFMA_SPLIT_F16, MFMA_F32 = 0, 1
 SELECT_MVP, SELECT_SECOND_ORDER = 0, 1
+WORKING_SET_AUTO = -1
 
 
 class SvmError(RuntimeError):
@@ -44,7 +45,7 @@ class svm_stats(C.Structure):
                 ("b_low", C.c_double), ("dual_obj", C.c_double), ("gram_used", C.c_int32), ("launches", C.c_int32),
                 ("t_gram", C.c_double), ("t_solve", C.c_double), ("t_finalize", C.c_double), ("t_total", C.c_double),
                 ("t_kernel", C.c_double), ("rounds", C.c_int64),
-                ("resident_rows", C.c_int32), ("reserved", C.c_int32), ("t_upload", C.c_double)]
+                ("resident_rows", C.c_int32), ("schedule", C.c_int32), ("t_upload", C.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -170,7 +171,7 @@ def svm_train(X: torch.Tensor, y: torch.Tensor, C_: float, gamma: float, tol: fl
                                   _ptr(ws), wsb, C.byref(o), C.byref(st)), ok=(SVM_OK, SVM_NOT_CONVERGED))
     out = TrainOut(alpha=alpha, b=b.value, status=status, stats=st.as_dict())
     if tl:
-        steps = min(tl, (st.rounds if o.working_set else st.iterations) + 1)
+        steps = min(tl, (st.rounds if o.working_set > 0 else st.iterations) + 1)
         out.trace_ul = tws[:2 * steps].reshape(steps, 2).copy()
         out.trace_b = tb[:2 * steps].reshape(steps, 2).copy()
     return out
@@ -203,7 +204,7 @@ def svm_train_static(X: torch.Tensor, y: torch.Tensor, C_: float, gamma: float, 
                                          C.byref(b), C.byref(o), C.byref(st)), ok=(SVM_OK, SVM_NOT_CONVERGED))
     out = TrainOut(alpha=alpha, b=b.value, status=status, stats=st.as_dict())
     if tl:
-        steps = min(tl, (st.rounds if o.working_set else st.iterations) + 1)
+        steps = min(tl, (st.rounds if o.working_set > 0 else st.iterations) + 1)
         out.trace_ul = tws[:2 * steps].reshape(steps, 2).copy()
         out.trace_b = tb[:2 * steps].reshape(steps, 2).copy()
     return out

@@ -132,6 +132,21 @@ def test_selection_option_rejects(opt):
         assert lib.svm_train_workspace_bytes(100, 4, C.byref(o)) == -1
 
 
+def test_working_set_auto_option():
+    """working_set = SVM_WORKING_SET_AUTO plans for the rounds where they may run (binary, n > 4096,
+    several owners, no trace), else for the per-step solver; other negative values are invalid."""
+    lib = svmx.load()
+    ws = lambda n, d, **kw: lib.svm_train_workspace_bytes(n, d, C.byref(_opts(**kw)))
+    auto = svmx.WORKING_SET_AUTO
+    assert ws(100_000, 32, working_set=auto) == ws(100_000, 32, working_set=32)
+    assert ws(20_000, 784, working_set=auto) == ws(20_000, 784, working_set=128)
+    assert ws(3000, 8, working_set=auto) == ws(3000, 8)  # small: one workgroup, per-step
+    assert ws(100_000, 32, working_set=auto, trace_len=10) == ws(100_000, 32, trace_len=10)
+    assert ws(100_000, 32, working_set=auto, selection=svmx.SELECT_SECOND_ORDER) == \
+        ws(100_000, 32, selection=svmx.SELECT_SECOND_ORDER)
+    assert ws(100_000, 32, working_set=-2) == -1 and ws(100_000, 32, working_set=3) == -1
+
+
 def test_ovo_rejects():
     lib = svmx.load()
     b = np.zeros(100)

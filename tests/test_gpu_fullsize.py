@@ -181,3 +181,36 @@ def test_working_set_full_size(cid, q, gram):
     assert abs(float(a @ y)) <= 1e-9 * wl.C * len(y)
     f = oracle.f_from_alpha(X, y, a, wl.gamma)
     kkt_and_gap(f, y, a, out.b, wl.C, wl.tol, slack=1e-4)
+
+
+@pytest.mark.parametrize("cid,gram,schedule", [(1, svmx.GRAM_AUTO, 1), (2, svmx.GRAM_AUTO, 2), (3, svmx.GRAM_AUTO, 1),
+                                               (1, svmx.GRAM_OFF, 1), (3, svmx.GRAM_OFF, None)])
+def test_auto_full_size(cid, gram, schedule):
+    """working_set = AUTO at the full workload sizes: the schedule its rule picks (rounds on the
+    784-feature problem and at 100,000 x 32, the pair solver after the probe on the 8-component
+    mixture, whose rounds take fewer pair steps than they cost), and the optimum gates against the
+    stored oracle solve: W, decisions and labels, tol-KKT and the duality gap on every row."""
+    R = ref(cid)
+    wl = synth.workload(cid)
+    X, y, Xt, _ = synth.generate(cid)
+    nt = len(R["test_decisions"])
+    assert digest(X, y, Xt[:nt]) == R["inputs_sha256"], "inputs differ from the stored reference"
+    Xd, yd = dev(X), dev(y)
+    out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=gram, working_set=svmx.WORKING_SET_AUTO)
+    assert out.status == svmx.SVM_OK
+    st = out.stats
+    print(f"\nworkload {cid} gram {gram}: schedule {st['schedule']}, {st['rounds']} rounds, {st['iterations']} pair "
+          f"steps, W={st['dual_obj']:.9f} (oracle {R['dual_obj']:.9f})")
+    if schedule is not None:
+        assert st["schedule"] == schedule
+    assert abs(st["dual_obj"] - R["dual_obj"]) <= 1e-4 * abs(R["dual_obj"])
+    d_gpu = svmx.svm_predict(Xd, yd, out.alpha, out.b, wl.gamma, dev(Xt[:nt])).cpu().numpy()
+    d_ref = np.array(R["test_decisions"])
+    err = float(np.max(np.abs(d_gpu - d_ref)))
+    assert err <= 1e-3
+    check_binary_labels(d_gpu, d_ref, err)
+    a = out.alpha.cpu().numpy()
+    assert np.all(a >= 0) and np.all(a <= wl.C)
+    assert abs(float(a @ y)) <= 1e-9 * wl.C * len(y)
+    f = oracle.f_from_alpha(X, y, a, wl.gamma)
+    kkt_and_gap(f, y, a, out.b, wl.C, wl.tol, slack=1e-4)
