@@ -1189,6 +1189,20 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       const int ngrp = WS_BS / span;  // 4, 2 or 1 thread groups
       const int grp = tid / span;
       const int g0 = grp * (WS_QUARTERS / ngrp), g1 = g0 + WS_QUARTERS / ngrp;
+      if (ngrp == 1 && rows_in_lds) {
+        // every thread sums all four quarters of its samples: the same grouping, in registers
+        for (int pos = tid; pos < len; pos += WS_BS) {
+          double q[WS_QUARTERS];
+#pragma unroll
+          for (int g = 0; g < WS_QUARTERS; ++g) {
+            const int r0 = g * nnz / WS_QUARTERS, r1 = (g + 1) * nnz / WS_QUARTERS;
+            double sg = 0.0;
+            for (int r = r0; r < r1; ++r) sg = ws_acc(sg, S.nzc[r], S.u.K[S.nzp[r] * len + pos]);
+            q[g] = sg;
+          }
+          S.f[pos] = S.f[pos] + (((q[0] + q[1]) + q[2]) + q[3]);
+        }
+      } else {
       for (int pos = tid - grp * span; pos < len; pos += WS_BS) {
         const int64_t gj = ws_gmap(P, base + pos);
         for (int g = g0; g < g1; ++g) {
@@ -1213,6 +1227,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       for (int pos = tid; pos < len; pos += WS_BS) {
         const double s = ((S.w.part[0][pos] + S.w.part[1][pos]) + S.w.part[2][pos]) + S.w.part[3][pos];
         S.f[pos] = S.f[pos] + s;
+      }
       }
     }
     ++round;
