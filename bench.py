@@ -279,7 +279,7 @@ def main():
     t_h2d = time.perf_counter() - t1
     t1 = time.perf_counter()
     Xd2, yd2 = Xh.to("cuda", non_blocking=True), yh.to("cuda", non_blocking=True)
-    oh = svmx.svm_train(Xd2, yd2, wl.C, wl.gamma, wl.tol, gram=gram_mode)
+    oh = svmx.svm_train(Xd2, yd2, wl.C, wl.gamma, wl.tol, gram=gram_mode, working_set=args.working_set)
     ah = oh.alpha.to("cpu")
     torch.cuda.synchronize()
     t_host = time.perf_counter() - t1
