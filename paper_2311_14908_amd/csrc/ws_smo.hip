@@ -352,7 +352,7 @@ struct WsLds {
       h8 s[2][4][128];      // and a block of own samples, [hi, lo][k chunk][column]
     } rs;
   } w;
-  int bi[WS_QMAX];
+  alignas(16) int bi[WS_QMAX];  // read four at a time
   signed char by[WS_QMAX];
   double bf[WS_QMAX], ba[WS_QMAX], bn[WS_QMAX];
   int nzp[WS_QMAX];
@@ -735,17 +735,32 @@ __device__ __forceinline__ u64 side_key(const WsLds &S, int side, int pos, int l
   return f_key(side == 0 ? fj : -fj);
 }
 
+// Bitonic sort of the first S lanes (S = 16, 32, 64): lanes S .. 63 must hold empty entries,
+// which stay there, so the 64 lanes read as one ascending list.
+template <int S>
+__device__ __forceinline__ void wave_sort_first(u64 &k, unsigned &v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int s = 2; s <= S; s <<= 1)
+#pragma unroll
+    for (int d = s >> 1; d > 0; d >>= 1) kv_cx(k, v, d, (lane & s) == 0);
+}
+
 // One wave's best members of one side among the chunks of 64 samples c = half, half + 2, ...:
 // (k, v) ascending, lanes 0 .. h - 1 exact.  With one chunk it is sorted outright.  With more,
-// the h-th smallest of the lanes' own best members is a threshold no member of the wave's best
-// h exceeds (at least h members are at or below it); only the members at or below it are
-// gathered in LDS and sorted, 64 at a time, the threshold tightening to the list's h-th entry
-// after each batch.
+// every member's key stays in registers and each lane keeps its own best; the minima of groups
+// of 64 / SEG lanes are at least SEG >= h members, so the largest of those minima is a threshold
+// no member of the wave's best h exceeds.  Only the members at or below it are gathered in LDS
+// and sorted (over 16, 32 or 64 lanes, as many as they need), 64 at a time, the threshold
+// tightening to the list's h-th entry after each batch.
 struct KV {
   u64 k;
   unsigned v;
 };
 
+constexpr int WS_OWN_CHUNKS = WS_SLICE_MAX / 128;  // chunks of 64 samples one wave takes
+
+template <int SEG>
 __device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, int len, int h, double C) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = (len + 63) / 64;
@@ -761,19 +776,38 @@ __device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, i
     }
     return KV{k, v};
   }
+  u64 ck[WS_OWN_CHUNKS];
   u64 tk = KSENT;
   unsigned tv = VSENT;
-  for (int c = half; c < nch; c += 2) {
-    const int pos = c * 64 + lane;
-    const u64 ck = side_key(S, side, pos, len, C);
-    if (ck != KSENT && kv_lt(ck, (unsigned)pos, tk, tv)) {
-      tk = ck;
+#pragma unroll
+  for (int i = 0; i < WS_OWN_CHUNKS; ++i) {
+    const int pos = (half + 2 * i) * 64 + lane;
+    ck[i] = side_key(S, side, pos, len, C);  // empty past len
+    if (ck[i] != KSENT && kv_lt(ck[i], (unsigned)pos, tk, tv)) {
+      tk = ck[i];
       tv = (unsigned)pos;
     }
   }
-  wave_sort64(tk, tv);
-  tk = readlane64(tk, h - 1);
-  tv = (unsigned)__builtin_amdgcn_readlane((int)tv, h - 1);
+  // minimum over groups of G lanes, then the maximum over the 64 / G >= SEG >= h groups
+  constexpr int G = 64 / SEG;
+#pragma unroll
+  for (int d = 1; d < G; d <<= 1) {
+    const u64 ok = xor_lane64(tk, d);
+    const unsigned ov = xor_lane(tv, d);
+    if (kv_lt(ok, ov, tk, tv)) {
+      tk = ok;
+      tv = ov;
+    }
+  }
+#pragma unroll
+  for (int d = G; d < 64; d <<= 1) {
+    const u64 ok = xor_lane64(tk, d);
+    const unsigned ov = xor_lane(tv, d);
+    if (kv_lt(tk, tv, ok, ov)) {
+      tk = ok;
+      tv = ov;
+    }
+  }
   bool have = false;
   int np = 0;
   u64 *pk = S.pk[wave];
@@ -784,7 +818,12 @@ __device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, i
     __builtin_amdgcn_wave_barrier();
     u64 fk = lane < np ? pk[lane] : KSENT;
     unsigned fv = lane < np ? pv[lane] : VSENT;
-    wave_sort64(fk, fv);
+    if (np <= 16)
+      wave_sort_first<16>(fk, fv);
+    else if (np <= 32)
+      wave_sort_first<32>(fk, fv);
+    else
+      wave_sort_first<64>(fk, fv);
     if (!have) {
       k = fk;
       v = fv;
@@ -802,22 +841,22 @@ __device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, i
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
-  for (int c = half; c < nch; c += 2) {
-    const int pos = c * 64 + lane;
-    const u64 ck = side_key(S, side, pos, len, C);
-    bool q = ck != KSENT && !kv_lt(tk, tv, ck, (unsigned)pos);
+#pragma unroll
+  for (int i = 0; i < WS_OWN_CHUNKS; ++i) {
+    const int pos = (half + 2 * i) * 64 + lane;
+    bool q = ck[i] != KSENT && !kv_lt(tk, tv, ck[i], (unsigned)pos);
     u64 mask = __ballot(q);
     int nq = __popcll(mask);
     if (nq == 0) continue;
     if (np + nq > 64) {
       flush();
-      q = q && !kv_lt(tk, tv, ck, (unsigned)pos);
+      q = q && !kv_lt(tk, tv, ck[i], (unsigned)pos);
       mask = __ballot(q);
       nq = __popcll(mask);
     }
     if (q) {
       const int at = np + __popcll(mask & below);
-      pk[at] = ck;
+      pk[at] = ck[i];
       pv[at] = (unsigned)pos;
     }
     np += nq;
@@ -874,7 +913,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     u64 k = KSENT;
     unsigned v = VSENT;
     if (owner) {
-      const KV r = own_list(S, side, half, len, h, C);
+      const KV r = own_list<SEG>(S, side, half, len, h, C);
       k = r.k;
       v = r.v;
     }
@@ -956,9 +995,18 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       const bool ok = lane < h && k != KSENT;
       const unsigned aux = ok ? S.u.st.aux[1][v] : 0u;
       const int idx = ok ? (int)(aux & 0x7fffffffu) : -1;
-      const int upi = lane < nu ? S.bi[lane] : -2;
+      // is idx among the first nu entries of the I_up list?  Broadcast LDS reads, four indices
+      // a read, over a bound known at compile time (nu <= h <= SEG): no loop, no lane reads.
+      const int nus = __builtin_amdgcn_readfirstlane(nu);
       bool dup = false;
-      for (int r = 0; r < nu; ++r) dup = dup || (__builtin_amdgcn_readlane(upi, r) == idx);
+#pragma unroll
+      for (int r = 0; r < SEG; r += 4) {
+        if (r < nus) {
+          const int4 w = *reinterpret_cast<const int4 *>(&S.bi[r]);
+          dup = dup || (w.x == idx) || (r + 1 < nus && w.y == idx) || (r + 2 < nus && w.z == idx) ||
+                (r + 3 < nus && w.w == idx);
+        }
+      }
       const bool keep = ok && !dup;
       const u64 mk = __ballot(keep);
       const int nok = __popcll(__ballot(ok));
