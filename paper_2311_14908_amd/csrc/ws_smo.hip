@@ -213,6 +213,13 @@ __device__ __forceinline__ unsigned ws_aux(int64_t j, int y) { return (unsigned)
 __device__ __forceinline__ bool ws_in_up(int y, double a, double C) { return (y > 0 && a < C) || (y < 0 && a > 0.0); }
 __device__ __forceinline__ bool ws_in_low(int y, double a, double C) { return (y > 0 && a > 0.0) || (y < 0 && a < C); }
 
+// Local sample index -> global row: the two class ranges of a problem.
+struct GMap {
+  int64_t off0, len0, off1;
+};
+__device__ __forceinline__ int64_t ws_gmap(const GMap &P, int64_t j) {
+  return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0);
+}
 __device__ __forceinline__ int64_t ws_gmap(const Prob &P, int64_t j) {
   return j < P.len0 ? P.off0 + j : P.off1 + (j - P.len0);
 }
@@ -411,10 +418,10 @@ __device__ __forceinline__ void wave_minmax(double &a, double &b) {
 // without lane-divergent branches, and the two wave reductions are independent chains that
 // the scheduler can interleave.  Not inlined: the loop gets registers of its own instead of
 // reloading the kernel's spilled scalars every step.
-__device__ __attribute__((noinline)) void local_solve(WsLds &S, const WsParams &p, int m, double b_up, double b_low,
-                                                     int64_t t) {
-  const SolveParams &sp = p.sp;
-  const double C = sp.C;
+// The parameters come as values: a reference to the kernel's parameter block would make the
+// kernel keep a copy of it in scratch memory and reload fields from there inside the round.
+__device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double tol, double frac, int64_t max_inner_p,
+                                                     int64_t max_iter, int m, double b_up, double b_low, int64_t t) {
   const int lane = threadIdx.x & 63;
   const int p0 = lane, p1 = lane + 64;
   const bool v0 = p0 < m, v1 = p1 < m;
@@ -423,8 +430,8 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, const WsParams &
   const int y0 = v0 ? S.by[p0] : 0, y1 = v1 ? S.by[p1] : 0;
   const int i0 = v0 ? S.bi[p0] : IBIG, i1 = v1 ? S.bi[p1] : IBIG;
   const double dy0 = (double)y0, dy1 = (double)y1;
-  const double tl = fmax(sp.tol, p.frac * (b_low - b_up));
-  const int max_inner = (int)min<int64_t>(p.max_inner, sp.max_iter - t);
+  const double tl = fmax(tol, frac * (b_low - b_up));
+  const int max_inner = (int)min<int64_t>(max_inner_p, max_iter - t);
   int inner = 0;
   for (; inner < max_inner; ++inner) {
     // this lane's best member of each side (positions l and l + 64)
@@ -601,9 +608,8 @@ __device__ __forceinline__ void row64_mma(WsLds &S, v4f (&acc)[2][8], int tp_n, 
   }
 }
 
-__device__ __attribute__((noinline)) void owner_rows_block(WsLds &S, const WsParams &p, const Prob &P, int m,
+__device__ __attribute__((noinline)) void owner_rows_block(WsLds &S, SplitX X, float cexp, GMap P, int m,
                                                           int64_t base, int len) {
-  const SplitX &X = p.split;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kq = lane >> 4, r16 = lane & 15;
   const int nst = (int)((X.dp + 63) / 64);  // stages; the last one holds 32 features when dp % 64 == 32
@@ -656,7 +662,7 @@ __device__ __attribute__((noinline)) void owner_rows_block(WsLds &S, const WsPar
               const float dot = (acc[a][tj][e] * S.bsc[pr]) * sj;
               float t = S.bnr[pr] + nj - 2.0f * dot;
               t = t > 0.f ? t : 0.f;
-              S.u.K[pr * len + j] = (S.bi[pr] == base + j) ? 1.0f : __builtin_amdgcn_exp2f(p.cexp * t);
+              S.u.K[pr * len + j] = (S.bi[pr] == base + j) ? 1.0f : __builtin_amdgcn_exp2f(cexp * t);
             }
           }
         }
@@ -666,9 +672,8 @@ __device__ __attribute__((noinline)) void owner_rows_block(WsLds &S, const WsPar
   __syncthreads();
 }
 
-__device__ __attribute__((noinline)) void owner_rows(WsLds &S, const WsParams &p, const Prob &P, int m, int64_t base,
+__device__ __attribute__((noinline)) void owner_rows(WsLds &S, SplitX X, float cexp, GMap P, int m, int64_t base,
                                                     int len) {
-  const SplitX &X = p.split;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kq = lane >> 4, r16 = lane & 15;
   const int stages = (int)(X.dp / 32);
@@ -716,7 +721,7 @@ __device__ __attribute__((noinline)) void owner_rows(WsLds &S, const WsParams &p
               const float dot = (acc[i][e] * S.bsc[pr]) * sj;
               float t = S.bnr[pr] + nj - 2.0f * dot;
               t = t > 0.f ? t : 0.f;
-              S.u.K[pr * len + j] = (S.bi[pr] == base + j) ? 1.0f : __builtin_amdgcn_exp2f(p.cexp * t);
+              S.u.K[pr * len + j] = (S.bi[pr] == base + j) ? 1.0f : __builtin_amdgcn_exp2f(cexp * t);
             }
           }
         }
@@ -1141,7 +1146,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         }
       }
       __syncthreads();
-      if (wave == 0) local_solve(S, p, m, b_up, b_low, t);
+      if (wave == 0) local_solve(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
       __syncthreads();
       if (!solo) {
         // publish the new multipliers (two words each) and the step count
@@ -1160,9 +1165,9 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       if (!GRAM) {
         // row path: K(B, own samples) into LDS, then the columns of K_BB of the own members
         if (len <= 128)
-          owner_rows_block(S, p, P, m, base, len);
+          owner_rows_block(S, p.split, p.cexp, GMap{P.off0, P.len0, P.off1}, m, base, len);
         else
-          owner_rows(S, p, P, m, base, len);
+          owner_rows(S, p.split, p.cexp, GMap{P.off0, P.len0, P.off1}, m, base, len);
         const int nk = S.nown * m;
         for (int e = tid; e < nk; e += WS_BS) {
           const int kk = e / m, a = e - kk * m;
@@ -1237,36 +1242,70 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       const int ngrp = WS_BS / span;  // 4, 2 or 1 thread groups
       const int grp = tid / span;
       const int g0 = grp * (WS_QUARTERS / ngrp), g1 = g0 + WS_QUARTERS / ngrp;
-      if (ngrp == 1 && rows_in_lds) {
-        // every thread sums all four quarters of its samples: the same grouping, in registers
-        for (int pos = tid; pos < len; pos += WS_BS) {
-          double q[WS_QUARTERS];
+      int qr0[WS_QUARTERS], qr1[WS_QUARTERS];
 #pragma unroll
-          for (int g = 0; g < WS_QUARTERS; ++g) {
-            const int r0 = g * nnz / WS_QUARTERS, r1 = (g + 1) * nnz / WS_QUARTERS;
-            double sg = 0.0;
-            for (int r = r0; r < r1; ++r) sg = ws_acc(sg, S.nzc[r], S.u.K[S.nzp[r] * len + pos]);
-            q[g] = sg;
+      for (int g = 0; g < WS_QUARTERS; ++g) {
+        qr0[g] = g * nnz / WS_QUARTERS;
+        qr1[g] = (g + 1) * nnz / WS_QUARTERS;
+      }
+      const int qlen = nnz - (WS_QUARTERS - 1) * nnz / WS_QUARTERS;  // the longest quarter (the last)
+      if (ngrp == 1 && rows_in_lds) {
+        // every thread sums all four quarters of two of its samples in registers: the eight
+        // chains advance together, each in its own order, so the sums are those written
+        for (int pa = tid; pa < len; pa += 2 * WS_BS) {
+          const int pb = pa + WS_BS;
+          const bool hb = pb < len;
+          double qa[WS_QUARTERS], qb[WS_QUARTERS];
+#pragma unroll
+          for (int g = 0; g < WS_QUARTERS; ++g) qa[g] = qb[g] = 0.0;
+          for (int i = 0; i < qlen; ++i) {
+#pragma unroll
+            for (int g = 0; g < WS_QUARTERS; ++g) {
+              const int r = qr0[g] + i;
+              if (r < qr1[g]) {
+                const double c = S.nzc[r];
+                const float *row = S.u.K + S.nzp[r] * len;
+                qa[g] = ws_acc(qa[g], c, row[pa]);
+                if (hb) qb[g] = ws_acc(qb[g], c, row[pb]);
+              }
+            }
           }
-          S.f[pos] = S.f[pos] + (((q[0] + q[1]) + q[2]) + q[3]);
+          S.f[pa] = S.f[pa] + (((qa[0] + qa[1]) + qa[2]) + qa[3]);
+          if (hb) S.f[pb] = S.f[pb] + (((qb[0] + qb[1]) + qb[2]) + qb[3]);
+        }
+      } else if (rows_in_lds) {
+        // each thread its one or two quarters (g0, g0 + 1) of one sample, the chains together
+        const int ra0 = g0 * nnz / WS_QUARTERS, la = (g0 + 1) * nnz / WS_QUARTERS - ra0;
+        const int rb0 = ra0 + la, lb = g1 - g0 == 2 ? (g0 + 2) * nnz / WS_QUARTERS - rb0 : 0;
+        const int lm = max(la, lb);
+        for (int pos = tid - grp * span; pos < len; pos += WS_BS) {
+          double sa = 0.0, sb = 0.0;
+          for (int i = 0; i < lm; ++i) {
+            if (i < la) sa = ws_acc(sa, S.nzc[ra0 + i], S.u.K[S.nzp[ra0 + i] * len + pos]);
+            if (i < lb) sb = ws_acc(sb, S.nzc[rb0 + i], S.u.K[S.nzp[rb0 + i] * len + pos]);
+          }
+          S.w.part[g0][pos] = sa;
+          if (g1 - g0 == 2) S.w.part[g0 + 1][pos] = sb;
+        }
+        __syncthreads();
+        for (int pos = tid; pos < len; pos += WS_BS) {
+          const double s = ((S.w.part[0][pos] + S.w.part[1][pos]) + S.w.part[2][pos]) + S.w.part[3][pos];
+          S.f[pos] = S.f[pos] + s;
         }
       } else {
+      // the rows of B do not fit in LDS next to the slice: read them from the Gram
       for (int pos = tid - grp * span; pos < len; pos += WS_BS) {
         const int64_t gj = ws_gmap(P, base + pos);
         for (int g = g0; g < g1; ++g) {
           const int r0 = g * nnz / WS_QUARTERS, r1 = (g + 1) * nnz / WS_QUARTERS;
           double s = 0.0;
-          if (rows_in_lds) {
-            for (int r = r0; r < r1; ++r) s = ws_acc(s, S.nzc[r], S.u.K[S.nzp[r] * len + pos]);
-          } else {
-            for (int r = r0; r < r1; r += WS_GATHER) {
-              float kk[WS_GATHER];
+          for (int r = r0; r < r1; r += WS_GATHER) {
+            float kk[WS_GATHER];
 #pragma unroll
-              for (int e = 0; e < WS_GATHER; ++e) kk[e] = gp(sp.gram)[S.nzoff[min(r + e, r1 - 1)] + gj];
+            for (int e = 0; e < WS_GATHER; ++e) kk[e] = gp(sp.gram)[S.nzoff[min(r + e, r1 - 1)] + gj];
 #pragma unroll
-              for (int e = 0; e < WS_GATHER; ++e)
-                if (r + e < r1) s = ws_acc(s, S.nzc[r + e], kk[e]);
-            }
+            for (int e = 0; e < WS_GATHER; ++e)
+              if (r + e < r1) s = ws_acc(s, S.nzc[r + e], kk[e]);
           }
           S.w.part[g][pos] = s;
         }
