@@ -9,6 +9,7 @@
 #include "common.hpp"
 #include "rbf_rows.hpp"
 #include "tile_order.hpp"
+#include "tile_store.hpp"
 
 #include <math.h>
 
@@ -119,38 +120,30 @@ __global__ void __launch_bounds__(GBS) gram_rbf_mfma(const float *__restrict__ X
   __syncthreads();
   // epilogue: lane holds D[4*(lane/16)+e][lane%16] of each 16x16 block
   const bool mirror = ti != tj;
+  const int kq = lane >> 4, r16 = lane & 15;
+  float kv[4][4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
-    const int lr0 = wm * 64 + a * 16 + 4 * (lane >> 4);
+    const int lr0 = wm * 64 + a * 16 + 4 * kq;
     const int64_t gr0 = i0 + lr0;
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
-      const int lc = wn * 64 + bb * 16 + (lane & 15);
+      const int lc = wn * 64 + bb * 16 + r16;
       const int64_t gc = j0 + lc;
-      float kv[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         float t = nA[lr0 + e] + nB[lc] - 2.0f * acc[a][bb][e];
         t = t > 0.f ? t : 0.f;
-        kv[e] = (gr0 + e == gc) ? 1.0f : __builtin_amdgcn_exp2f(c * t);
+        kv[a][bb][e] = (gr0 + e == gc) ? 1.0f : __builtin_amdgcn_exp2f(c * t);
       }
-      if (gc < n) {
+      if (!mirror && gc < n) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (gr0 + e < n) __builtin_nontemporal_store(kv[e], &G[(gr0 + e) * ld + gc]);
-        if (mirror) {
-          float *dst = G + gc * ld + gr0;
-          if (STORE4 && gr0 + 3 < n) {
-            __builtin_nontemporal_store((v4f){kv[0], kv[1], kv[2], kv[3]}, reinterpret_cast<v4f *>(dst));
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (gr0 + e < n) __builtin_nontemporal_store(kv[e], &dst[e]);
-          }
-        }
+          if (gr0 + e < n) __builtin_nontemporal_store(kv[a][bb][e], &G[(gr0 + e) * ld + gc]);
       }
     }
   }
+  if (mirror) store_tile_128<STORE4>(G, ld, n, i0 + wm * 64, j0 + wn * 64, kq, r16, kv);
 }
 
 hipError_t launch_gram(const float *X, int64_t n, int64_t d, float gamma, float *G, int64_t ld, hipStream_t s) {
