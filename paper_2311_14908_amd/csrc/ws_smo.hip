@@ -386,6 +386,9 @@ __device__ __forceinline__ double dpp_full_d(double v) {  // every lane reads it
   return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
+// HALF: lanes 32 .. 63 hold neutral values (+inf for a, -inf for b), so lane 31 holds the
+// result after the row_bcast:15 step and the last step is skipped.
+template <bool HALF = false>
 __device__ __forceinline__ void wave_minmax(double &a, double &b) {
 #define SVMX_MM_FULL(CTRL)                       \
   {                                              \
@@ -406,11 +409,11 @@ __device__ __forceinline__ void wave_minmax(double &a, double &b) {
   SVMX_MM_FULL(0x124)     // row_ror:4
   SVMX_MM_FULL(0x128)     // row_ror:8
   SVMX_MM_MASK(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
-  SVMX_MM_MASK(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
+  if (!HALF) SVMX_MM_MASK(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
 #undef SVMX_MM_FULL
 #undef SVMX_MM_MASK
-  a = readlane_d(a, 63);
-  b = readlane_d(b, 63);
+  a = readlane_d(a, HALF ? 31 : 63);
+  b = readlane_d(b, HALF ? 31 : 63);
 }
 
 // The pair steps on B (wave 0 only; K_BB in S.u.K): S.bn receives the new multipliers,
@@ -420,11 +423,15 @@ __device__ __forceinline__ void wave_minmax(double &a, double &b) {
 // reloading the kernel's spilled scalars every step.
 // The parameters come as values: a reference to the kernel's parameter block would make the
 // kernel keep a copy of it in scratch memory and reload fields from there inside the round.
+// MAXM bounds m: up to 64 a lane holds one member of B (position lane), above two (lane and
+// lane + 64); up to 32 the reductions stop at half the wave.  Every bound gives the same steps.
+template <int MAXM>
 __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double tol, double frac, int64_t max_inner_p,
                                                      int64_t max_iter, int m, double b_up, double b_low, int64_t t) {
+  constexpr bool TWO = MAXM > 64;
   const int lane = threadIdx.x & 63;
   const int p0 = lane, p1 = lane + 64;
-  const bool v0 = p0 < m, v1 = p1 < m;
+  const bool v0 = p0 < m, v1 = TWO && p1 < m;
   double f0 = v0 ? S.bf[p0] : 0.0, f1 = v1 ? S.bf[p1] : 0.0;
   double a0 = v0 ? S.ba[p0] : 0.0, a1 = v1 ? S.ba[p1] : 0.0;
   const int y0 = v0 ? S.by[p0] : 0, y1 = v1 ? S.by[p1] : 0;
@@ -435,13 +442,13 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double
   int inner = 0;
   for (; inner < max_inner; ++inner) {
     // this lane's best member of each side (positions l and l + 64)
-    const bool u0 = ws_in_up(y0, a0, C), u1 = ws_in_up(y1, a1, C);
-    const bool l0 = ws_in_low(y0, a0, C), l1 = ws_in_low(y1, a1, C);
+    const bool u0 = ws_in_up(y0, a0, C), u1 = TWO && ws_in_up(y1, a1, C);
+    const bool l0 = ws_in_low(y0, a0, C), l1 = TWO && ws_in_low(y1, a1, C);
     // position l + 64 wins a lane's side on a smaller (larger) f, or an equal f and a smaller
     // index (bitwise forms: no branches)
     const bool tie_i = (f1 == f0) & (i1 < i0);
-    const bool up1 = u1 & (!u0 | (f1 < f0) | tie_i);
-    const bool lo1 = l1 & (!l0 | (f1 > f0) | tie_i);
+    const bool up1 = TWO && (u1 & (!u0 | (f1 < f0) | tie_i));
+    const bool lo1 = TWO && (l1 & (!l0 | (f1 > f0) | tie_i));
     const double cu_v = up1 ? f1 : (u0 ? f0 : INFINITY);
     const int cu_i = up1 ? i1 : (u0 ? i0 : IBIG);
     const int cu_p = up1 ? p1 : (u0 ? p0 : -1);
@@ -450,7 +457,7 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double
     const int cl_p = lo1 ? p1 : (l0 ? p0 : -1);
     // wave extremes of both sides, then the smallest index among the lanes holding each
     double ru = cu_v, rl = cl_v;
-    wave_minmax(ru, rl);
+    wave_minmax<MAXM <= 32>(ru, rl);
     const unsigned long long tu = (unsigned long long)__ballot(cu_v == ru);
     const unsigned long long tw = (unsigned long long)__ballot(cl_v == rl);
     int lu = __ffsll(tu) - 1, ll = __ffsll(tw) - 1;
@@ -468,18 +475,22 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double
     if (pu < 0 || pl < 0) break;
     const double fu = readlane_d(cu_v, lu), fl = readlane_d(cl_v, ll);
     if (fl - fu <= tl) break;
-    const bool hu1 = pu >= 64, hl1 = pl >= 64;  // which of its two positions the winner holds
+    const bool hu1 = TWO && pu >= 64, hl1 = TWO && pl >= 64;  // which of its two positions the winner holds
     const double au = readlane_d(hu1 ? a1 : a0, lu), al = readlane_d(hl1 ? a1 : a0, ll);
-    const double yu = readlane_d(hu1 ? dy1 : dy0, lu), yl = readlane_d(hl1 ? dy1 : dy0, ll);
+    const double yu = (double)__builtin_amdgcn_readlane(hu1 ? y1 : y0, lu);
+    const double yl = (double)__builtin_amdgcn_readlane(hl1 ? y1 : y0, ll);
     const float *Ku = S.u.K + pu * WS_QMAX, *Kl = S.u.K + pl * WS_QMAX;
     const double kul = (double)Ku[pl];
-    const float ku0 = Ku[p0], kl0 = Kl[p0], ku1 = Ku[p1], kl1 = Kl[p1];
+    const float ku0 = Ku[p0], kl0 = Kl[p0];
     const PairStep ps = solve_pair(C, fu, fl, au, al, yu, yl, kul);
     const double cu = (ps.au - au) * yu, cl = (ps.al - al) * yl;
     f0 = f_update(f0, cu, ku0, cl, kl0);
-    f1 = f_update(f1, cu, ku1, cl, kl1);
     a0 = p0 == pu ? ps.au : (p0 == pl ? ps.al : a0);
-    a1 = p1 == pu ? ps.au : (p1 == pl ? ps.al : a1);
+    if (TWO) {
+      const float ku1 = Ku[p1], kl1 = Kl[p1];
+      f1 = f_update(f1, cu, ku1, cl, kl1);
+      a1 = p1 == pu ? ps.au : (p1 == pl ? ps.al : a1);
+    }
   }
   if (v0) S.bn[p0] = a0;
   if (v1) S.bn[p1] = a1;
@@ -1146,7 +1157,14 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         }
       }
       __syncthreads();
-      if (wave == 0) local_solve(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
+      if (wave == 0) {
+        if (m <= 32)
+          local_solve<32>(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
+        else if (m <= 64)
+          local_solve<64>(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
+        else
+          local_solve<WS_QMAX>(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
+      }
       __syncthreads();
       if (!solo) {
         // publish the new multipliers (two words each) and the step count
