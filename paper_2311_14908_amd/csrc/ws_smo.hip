@@ -991,8 +991,12 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       S.u.st.aux[side][v] = ws_aux(base + v, S.y[v]);
       S.u.st.ab[side][v] = (u64)__double_as_longlong(S.a[v]);
     }
+    if (wave == 2) {  // the I_low list, for wave 0
+      S.lk[2][lane] = k;
+      S.lv[2][lane] = v;
+    }
     __syncthreads();
-    // ---- 1d. the working set: the I_up list, then the I_low list without repeats
+    // ---- 1d. the working set (wave 0): the I_up list, then the I_low list without repeats
     if (wave == 0) {
       const bool ok = lane < h && k != KSENT;
       if (ok) {
@@ -1002,42 +1006,41 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         S.bf[lane] = key_f(k);
         S.ba[lane] = __longlong_as_double((long long)S.u.st.ab[0][v]);
       }
-      const int cnt = __popcll(__ballot(ok));  // every lane votes: outside the lane-0 branch
-      if (lane == 0) S.nu = cnt;
-    }
-    __syncthreads();
-    if (wave == 2) {
-      const int nu = S.nu;
-      const bool ok = lane < h && k != KSENT;
-      const unsigned aux = ok ? S.u.st.aux[1][v] : 0u;
-      const int idx = ok ? (int)(aux & 0x7fffffffu) : -1;
+      const int nu = __popcll(__ballot(ok));
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      const u64 kl = S.lk[2][lane];
+      const unsigned vl = S.lv[2][lane];
+      const bool okl = lane < h && kl != KSENT;
+      const unsigned aux = okl ? S.u.st.aux[1][vl] : 0u;
+      const int idx = okl ? (int)(aux & 0x7fffffffu) : -1;
       // is idx among the first nu entries of the I_up list?  Broadcast LDS reads, four indices
       // a read, over a bound known at compile time (nu <= h <= SEG): no loop, no lane reads.
-      const int nus = __builtin_amdgcn_readfirstlane(nu);
       bool dup = false;
 #pragma unroll
       for (int r = 0; r < SEG; r += 4) {
-        if (r < nus) {
+        if (r < nu) {
           const int4 w = *reinterpret_cast<const int4 *>(&S.bi[r]);
-          dup = dup || (w.x == idx) || (r + 1 < nus && w.y == idx) || (r + 2 < nus && w.z == idx) ||
-                (r + 3 < nus && w.w == idx);
+          dup = dup || (w.x == idx) || (r + 1 < nu && w.y == idx) || (r + 2 < nu && w.z == idx) ||
+                (r + 3 < nu && w.w == idx);
         }
       }
-      const bool keep = ok && !dup;
+      const bool keep = okl && !dup;
       const u64 mk = __ballot(keep);
-      const int nok = __popcll(__ballot(ok));
+      const int nok = __popcll(__ballot(okl));
       const int pos = nu + __popcll(mk & ((1ull << lane) - 1ull));
       if (keep) {
         S.bi[pos] = idx;
         S.by[pos] = (aux >> 31) ? -1 : 1;
-        S.bf[pos] = -key_f(k);
-        S.ba[pos] = __longlong_as_double((long long)S.u.st.ab[1][v]);
+        S.bf[pos] = -key_f(kl);
+        S.ba[pos] = __longlong_as_double((long long)S.u.st.ab[1][vl]);
       }
       if (lane == 0) {
+        S.nu = nu;
         S.m = nu + __popcll(mk);
         S.nl = nok;
-        S.il = ok ? idx : IBIG;
-        S.bl = ok ? -key_f(k) : -INFINITY;
+        S.il = okl ? idx : IBIG;
+        S.bl = okl ? -key_f(kl) : -INFINITY;
       }
     }
     __syncthreads();
@@ -1276,16 +1279,18 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
           double qa[WS_QUARTERS], qb[WS_QUARTERS];
 #pragma unroll
           for (int g = 0; g < WS_QUARTERS; ++g) qa[g] = qb[g] = 0.0;
+          // no branch inside, so the loads of the four quarters are issued together: a quarter
+          // shorter than qlen adds 0 * K (+0) for its missing last term, which leaves its sum
+          // unchanged (a sum that starts at +0 and adds products never becomes -0)
           for (int i = 0; i < qlen; ++i) {
 #pragma unroll
             for (int g = 0; g < WS_QUARTERS; ++g) {
-              const int r = qr0[g] + i;
-              if (r < qr1[g]) {
-                const double c = S.nzc[r];
-                const float *row = S.u.K + S.nzp[r] * len;
-                qa[g] = ws_acc(qa[g], c, row[pa]);
-                if (hb) qb[g] = ws_acc(qb[g], c, row[pb]);
-              }
+              const bool in = qr0[g] + i < qr1[g];
+              const int r = in ? qr0[g] + i : 0;
+              const double c = in ? S.nzc[r] : 0.0;
+              const float *row = S.u.K + S.nzp[r] * len;
+              qa[g] = ws_acc(qa[g], c, row[pa]);
+              qb[g] = ws_acc(qb[g], c, row[hb ? pb : pa]);
             }
           }
           S.f[pa] = S.f[pa] + (((qa[0] + qa[1]) + qa[2]) + qa[3]);
