@@ -170,12 +170,17 @@ def test_row_path_streamed_large_configuration():
 
 
 @pytest.mark.parametrize("mfma", MFMAS)
+@pytest.mark.parametrize("aligned", [False, True])
 @pytest.mark.parametrize("cid,n,d", [(0, 1000, 16), (2, 1300, 128), (1, 700, 784), (3, 3001, 32), (0, 333, 13),
                                      (0, 129, 5)])
-def test_gram_small(cid, n, d, mfma):
+def test_gram_small(cid, n, d, mfma, aligned):
+    """Every entry of the Gram against the oracle.  With a row pitch that is a multiple of 64 the
+    kernels store the mirrored tiles as float4s (and rows of up to 128 features take the
+    one-stage kernel); with n + 3 every mirrored entry is stored on its own."""
     wl = synth.workload(cid)
     X, _, _, _ = synth.generate(cid, n=n, m=1, d=d)
-    G = svmx.svm_gram(dev(X), wl.gamma, ld=n + 3, gram_mfma=mfma).cpu().numpy()[:, :n]
+    ld = (n + 63) // 64 * 64 if aligned else n + 3
+    G = svmx.svm_gram(dev(X), wl.gamma, ld=ld, gram_mfma=mfma).cpu().numpy()[:, :n]
     ref = oracle.kernel_rows(X, np.arange(n), wl.gamma)
     assert row_rel_err(G, ref) <= ROW_RTOL
     assert np.all(np.diag(G) == 1.0)
