@@ -264,19 +264,22 @@ __device__ void merge_lists(const u64 *words, int side, int first0, int first, i
       if (r * R + seg < nl) pending |= 1u << r;
     const uint64_t t0 = wall_clock64();
     while (pending) {
+      // every load of the sweep first (no test between them, so they are in flight together)
 #pragma unroll
       for (int r = 0; r < NR; ++r) {
+        const int i = r * R + seg;
+        const u64 *src = words + ((size_t)(first + i * step) * 2 + side) * 64 * CAND_WORDS + (size_t)e * CAND_WORDS;
         if (pending & (1u << r)) {
-          const int i = r * R + seg;
-          const u64 *src = words + ((size_t)(first + i * step) * 2 + side) * 64 * CAND_WORDS + (size_t)e * CAND_WORDS;
-          bool ok = true;
 #pragma unroll
-          for (int c = 0; c < CAND_WORDS; ++c) {
-            w[r][c] = ld_word(src + c);
-            ok = ok && cand_stamped(w[r][c], stamp);
-          }
-          if (ok) pending &= ~(1u << r);
+          for (int c = 0; c < CAND_WORDS; ++c) w[r][c] = ld_word(src + c);
         }
+      }
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        bool ok = true;
+#pragma unroll
+        for (int c = 0; c < CAND_WORDS; ++c) ok = ok && cand_stamped(w[r][c], stamp);
+        if (ok) pending &= ~(1u << r);
       }
       if (pending && wall_clock64() - t0 > spin_limit) {
         __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -316,6 +319,27 @@ __device__ void merge_lists(const u64 *words, int side, int first0, int first, i
       if (r + span < nr) seg_merge<SEG>(rk[r], rv[r], rk[r + span], rv[r + span]);
   k = rk[0];
   v = rv[0];
+}
+
+// Waits until words a and b both carry `stamp` (both loads in flight at once); returns their
+// 60-bit payloads.
+__device__ __forceinline__ void poll_word2(const u64 *a, const u64 *b, unsigned stamp, uint64_t spin_limit, int32_t *err,
+                                          int *abort_flag, u64 &pa, u64 &pb) {
+  const uint64_t t0 = wall_clock64();
+  for (;;) {
+    const u64 x = ld_word(a), y = ld_word(b);
+    if (cand_stamped(x, stamp) && cand_stamped(y, stamp)) {
+      pa = x & CAND_M60;
+      pb = y & CAND_M60;
+      return;
+    }
+    if (wall_clock64() - t0 > spin_limit) {
+      __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *abort_flag = 1;
+      pa = pb = 0;
+      return;
+    }
+  }
 }
 
 // Waits until word `w` carries `stamp`; returns its 60-bit payload.
@@ -1107,25 +1131,38 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       }
     }
     if (solver && (!GRAM || kdist)) {
-      // wait for every published entry of K_BB, WS_GATHER per thread at a time
+      // wait for every published entry of K_BB, WK_GATHER per thread at a time: each sweep
+      // issues all its loads before testing any, so they are in flight together
+      constexpr int WK_GATHER = 16;
       const int mm = m * m;
-      for (int e0 = 0; e0 < mm; e0 += WS_BS * WS_GATHER) {
+      const int dra = WS_BS / m, dcb = WS_BS - dra * m;  // slot e -> e + WS_BS in (row, column)
+      for (int e0 = 0; e0 < mm; e0 += WS_BS * WK_GATHER) {
+        int off[WK_GATHER];
         unsigned pending = 0;
+        {
+          int ra = (e0 + tid) / m, cb = (e0 + tid) - ra * m;
 #pragma unroll
-        for (int b = 0; b < WS_GATHER; ++b)
-          if (e0 + b * WS_BS + tid < mm) pending |= 1u << b;
+          for (int b = 0; b < WK_GATHER; ++b) {
+            off[b] = ra * WS_QMAX + cb;
+            if (e0 + b * WS_BS + tid < mm) pending |= 1u << b;
+            ra += dra;
+            cb += dcb;
+            if (cb >= m) {
+              cb -= m;
+              ++ra;
+            }
+          }
+        }
         const uint64_t t0 = wall_clock64();
         while (pending) {
+          u64 w[WK_GATHER];
 #pragma unroll
-          for (int b = 0; b < WS_GATHER; ++b) {
-            if (pending & (1u << b)) {
-              const int e = e0 + b * WS_BS + tid;
-              const int ra = e / m, cb = e - ra * m;
-              const u64 w = ld_word(kbuf + kpar + (size_t)ra * WS_QMAX + cb);
-              if ((unsigned)(w >> 32) == kstamp) {
-                S.u.K[ra * WS_QMAX + cb] = __uint_as_float((unsigned)w);
-                pending &= ~(1u << b);
-              }
+          for (int b = 0; b < WK_GATHER; ++b) w[b] = (pending & (1u << b)) ? ld_word(kbuf + kpar + off[b]) : 0ull;
+#pragma unroll
+          for (int b = 0; b < WK_GATHER; ++b) {
+            if ((pending & (1u << b)) && (unsigned)(w[b] >> 32) == kstamp) {
+              S.u.K[off[b]] = __uint_as_float((unsigned)w[b]);
+              pending &= ~(1u << b);
             }
           }
           if (pending && wall_clock64() - t0 > sp.spin_limit) {
@@ -1217,8 +1254,8 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       }
       const u64 *bw = bcast + par * WS_BCAST_PITCH;
       if (tid < m) {
-        const u64 lo = poll_word(bw + 1 + 2 * tid, stamp, sp.spin_limit, sp.error, &S.abort_flag);
-        const u64 hi = poll_word(bw + 2 + 2 * tid, stamp, sp.spin_limit, sp.error, &S.abort_flag);
+        u64 lo, hi;
+        poll_word2(bw + 1 + 2 * tid, bw + 2 + 2 * tid, stamp, sp.spin_limit, sp.error, &S.abort_flag, lo, hi);
         S.bn[tid] = __longlong_as_double((long long)((hi << 32) | lo));
       }
       if (tid == WS_BS - 1) S.steps = (int64_t)poll_word(bw, stamp, sp.spin_limit, sp.error, &S.abort_flag);
