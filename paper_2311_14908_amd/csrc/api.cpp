@@ -55,13 +55,16 @@ constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
 // working_set = SVM_WORKING_SET_AUTO: q = 128 for rows of 256 features or more, else 32; the
 // first WS_AUTO_PROBE_ROUNDS rounds decide.  The rounds go on when they took at least as many
 // pair steps per round as a round costs in pair steps (measured on MI355X: a round of q = 32
-// costs about 6 pair steps on the Gram path -- 32 us against 5.4 at 100,000 x 32, 26 against
-// 4.6 at 50,000 x 128 -- and about 7 on the row path -- 58 us against 8.3 at 100,000 x 32; one
-// of q = 128 about 23 on the Gram path -- 94 us against 4.1 at 20,000 x 784 -- and 13 on the
-// row path), else the pair solver takes over from the state the rounds reached.
+// costs 4.9 to 6.9 pair steps on the Gram path -- 26.7 us against 5.4 at 100,000 x 32, 23.2
+// against 4.65 at 50,000 x 128, 28.2 against 4.1 at 20,000 x 784 -- and 5.0 to 6.5 on the row
+// path -- 42.3 us against 8.4 at 100,000 x 32, 78.6 against 12.0 at 20,000 x 784; one of
+// q = 128 10.6 to 18.8 on the Gram path and 11.3 on the row path -- 77.1 us against 4.1 and
+// 135.7 against 12.0 at 20,000 x 784), else the pair solver takes over from the state the
+// rounds reached.  The thresholds sit above the break-even of the problems each q is chosen
+// for (q = 32: rows of fewer than 256 features, 4.9 to 5.0 on the Gram path).
 constexpr int64_t WS_AUTO_PROBE_ROUNDS = 128;
 double ws_auto_min_steps(int32_t q, bool gram) {
-  if (q >= 128) return gram ? 25.0 : 15.0;
+  if (q >= 128) return gram ? 20.0 : 12.5;
   return gram ? 6.5 : 7.0;
 }
 
