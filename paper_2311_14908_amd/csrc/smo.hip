@@ -220,7 +220,7 @@ __device__ R exchange(const Prob &P, int rank, unsigned stamp, const R &mine, Re
     if (wave == 0) {
       u64 *lv2 = P.slots2 + par * (size_t)P.ng * SLOT_WORDS;
       const int g = rank / P.g1;
-      if (rank % P.g1 == 0) {
+      if (rank == group_leader(P, g)) {
         const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
         const R gs = poll_reduce<R>(lv1, q0, q1, 64, stamp, spin_limit, err, abort_flag);
         put_record(lv2 + (size_t)g * SLOT_WORDS, stamp, gs);

@@ -60,6 +60,17 @@ struct Prob {
 
 constexpr int SLOT_WORDS = 16;  // 6 used; a record sits alone in one 128-byte line
 
+// Rank that reduces the records (or merges the lists) of first-level group g, whose members are
+// ranks g g1 .. min(nwg, g g1 + g1) - 1: the member whose workgroup runs on XCD g mod 8 (a launch
+// deals its workgroups to the eight XCDs in turn), so that the groups' work spreads over the
+// XCDs; the first rank of each group would put every one of them on one XCD whenever g1 and
+// wg0 are multiples of 8.  Which member it is does not change any value.
+__host__ __device__ __forceinline__ int32_t group_leader(const Prob &P, int32_t g) {
+  const int32_t q0 = g * P.g1, size = (P.nwg < q0 + P.g1 ? P.nwg : q0 + P.g1) - q0;
+  const int32_t off = ((g & 7) - ((P.wg0 + q0) & 7) + 8) & 7;
+  return q0 + (off < size ? off : 0);
+}
+
 // Launch-wide parameters of the persistent solver.
 struct SolveParams {
   const Prob *probs;

@@ -977,7 +977,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     }
     __syncthreads();  // lk/lv are rewritten below
     // ---- 1b. group lists (more than 16 owners): group leaders merge their group's lists
-    if (owner && P.g1 > 0 && rank % P.g1 == 0) {
+    if (owner && P.g1 > 0 && rank == group_leader(P, rank / P.g1)) {
       const int g = rank / P.g1;
       const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
       merge_lists<SEG>(P.slots + par * P.nwg * WS_LIST_WORDS, side, q0, q0 + half, q1, 2, h, stamp,
