@@ -460,7 +460,6 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double
   double a0 = v0 ? S.ba[p0] : 0.0, a1 = v1 ? S.ba[p1] : 0.0;
   const int y0 = v0 ? S.by[p0] : 0, y1 = v1 ? S.by[p1] : 0;
   const int i0 = v0 ? S.bi[p0] : IBIG, i1 = v1 ? S.bi[p1] : IBIG;
-  const double dy0 = (double)y0, dy1 = (double)y1;
   const double tl = fmax(tol, frac * (b_low - b_up));
   const int max_inner = (int)min<int64_t>(max_inner_p, max_iter - t);
   int inner = 0;
@@ -1300,13 +1299,25 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       const int ngrp = WS_BS / span;  // 4, 2 or 1 thread groups
       const int grp = tid / span;
       const int g0 = grp * (WS_QUARTERS / ngrp), g1 = g0 + WS_QUARTERS / ngrp;
-      int qr0[WS_QUARTERS], qr1[WS_QUARTERS];
-#pragma unroll
-      for (int g = 0; g < WS_QUARTERS; ++g) {
-        qr0[g] = g * nnz / WS_QUARTERS;
-        qr1[g] = (g + 1) * nnz / WS_QUARTERS;
-      }
       const int qlen = nnz - (WS_QUARTERS - 1) * nnz / WS_QUARTERS;  // the longest quarter (the last)
+      // The terms of the quarter chains as lane registers of every wave: term i of quarter g
+      // (change c and row offset in S.u.K) in lane (g QL + i) mod 64 of register (g QL) / 64,
+      // QL = SEG / 2 >= the longest quarter (m <= 2 SEG).  A term past its quarter's end is
+      // (0, row 0): it adds 0 * K = +0, which leaves the sum unchanged (a sum that starts at +0
+      // and adds products never becomes -0).  The loops read the terms with lane reads, so only
+      // the rows come from LDS and no row read waits on another LDS read.
+      constexpr int QL = SEG / 2, NSR = (WS_QUARTERS * QL + 63) / 64;
+      double tc[NSR];
+      int to[NSR];
+#pragma unroll
+      for (int r = 0; r < NSR; ++r) {
+        const int sl = r * 64 + lane, g = sl / QL, i = sl - g * QL;
+        const int idx = g * nnz / WS_QUARTERS + i;
+        const bool in = g < WS_QUARTERS && idx < (g + 1) * nnz / WS_QUARTERS;
+        const int ic = in ? idx : 0;
+        tc[r] = in ? S.nzc[ic] : 0.0;
+        to[r] = in ? S.nzp[ic] * len : 0;
+      }
       if (ngrp == 1 && rows_in_lds) {
         // every thread sums all four quarters of two of its samples in registers: the eight
         // chains advance together, each in its own order, so the sums are those written
@@ -1316,33 +1327,75 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
           double qa[WS_QUARTERS], qb[WS_QUARTERS];
 #pragma unroll
           for (int g = 0; g < WS_QUARTERS; ++g) qa[g] = qb[g] = 0.0;
-          // no branch inside, so the loads of the four quarters are issued together: a quarter
-          // shorter than qlen adds 0 * K (+0) for its missing last term, which leaves its sum
-          // unchanged (a sum that starts at +0 and adds products never becomes -0)
-          for (int i = 0; i < qlen; ++i) {
+          // no branch inside, so the row reads of the four quarters are issued together
+          const int pbx = hb ? pb : pa;
+          // two terms of each chain a batch (QL is even and at least qlen, so a batch stays inside
+          // the quarters' slots; terms past a quarter's end are (0, row 0))
+          for (int i0 = 0; i0 < qlen; i0 += 2) {
+            double c[2][WS_QUARTERS];
+            float ka[2][WS_QUARTERS], kb[2][WS_QUARTERS];
 #pragma unroll
-            for (int g = 0; g < WS_QUARTERS; ++g) {
-              const bool in = qr0[g] + i < qr1[g];
-              const int r = in ? qr0[g] + i : 0;
-              const double c = in ? S.nzc[r] : 0.0;
-              const float *row = S.u.K + S.nzp[r] * len;
-              qa[g] = ws_acc(qa[g], c, row[pa]);
-              qb[g] = ws_acc(qb[g], c, row[hb ? pb : pa]);
-            }
+            for (int d = 0; d < 2; ++d)
+#pragma unroll
+              for (int g = 0; g < WS_QUARTERS; ++g) {
+                const int sl = (g * QL) % 64 + i0 + d;
+                c[d][g] = readlane_d(tc[(g * QL) / 64], sl);
+                const float *row = S.u.K + __builtin_amdgcn_readlane(to[(g * QL) / 64], sl);
+                ka[d][g] = row[pa];
+                kb[d][g] = row[pbx];
+              }
+            // compiler barrier: the reads of the batch are issued before the first is used (left
+            // to itself the scheduler waits for each read before issuing the next)
+            __asm__ volatile("" ::: "memory");
+#pragma unroll
+            for (int d = 0; d < 2; ++d)
+#pragma unroll
+              for (int g = 0; g < WS_QUARTERS; ++g) {
+                qa[g] = ws_acc(qa[g], c[d][g], ka[d][g]);
+                qb[g] = ws_acc(qb[g], c[d][g], kb[d][g]);
+              }
           }
           S.f[pa] = S.f[pa] + (((qa[0] + qa[1]) + qa[2]) + qa[3]);
           if (hb) S.f[pb] = S.f[pb] + (((qb[0] + qb[1]) + qb[2]) + qb[3]);
         }
       } else if (rows_in_lds) {
         // each thread its one or two quarters (g0, g0 + 1) of one sample, the chains together
-        const int ra0 = g0 * nnz / WS_QUARTERS, la = (g0 + 1) * nnz / WS_QUARTERS - ra0;
-        const int rb0 = ra0 + la, lb = g1 - g0 == 2 ? (g0 + 2) * nnz / WS_QUARTERS - rb0 : 0;
+        // g0 is the same in the whole wave (span >= 64); quarter g0 + 1 only with two of them
+        const int la = (g0 + 1) * nnz / WS_QUARTERS - g0 * nnz / WS_QUARTERS;
+        const int lb = g1 - g0 == 2 ? (g0 + 2) * nnz / WS_QUARTERS - (g0 + 1) * nnz / WS_QUARTERS : 0;
         const int lm = max(la, lb);
+        const int la0 = __builtin_amdgcn_readfirstlane(g0 * QL), lb0 = la0 + QL;
+        auto term = [&](int sl, double &c, int &o) {  // slot sl < 4 QL, the same in the wave
+          if (NSR == 1 || sl < 64) {
+            c = readlane_d(tc[0], sl & 63);
+            o = __builtin_amdgcn_readlane(to[0], sl & 63);
+          } else {
+            c = readlane_d(tc[NSR - 1], sl & 63);
+            o = __builtin_amdgcn_readlane(to[NSR - 1], sl & 63);
+          }
+        };
         for (int pos = tid - grp * span; pos < len; pos += WS_BS) {
           double sa = 0.0, sb = 0.0;
-          for (int i = 0; i < lm; ++i) {
-            if (i < la) sa = ws_acc(sa, S.nzc[ra0 + i], S.u.K[S.nzp[ra0 + i] * len + pos]);
-            if (i < lb) sb = ws_acc(sb, S.nzc[rb0 + i], S.u.K[S.nzp[rb0 + i] * len + pos]);
+          // four terms of each chain a batch (QL is a multiple of four, so a batch stays inside
+          // its quarter's slots; terms past the quarter's end are (0, row 0))
+          for (int i0 = 0; i0 < lm; i0 += 4) {
+            double ca[4], cb[4];
+            float ka[4], kb[4];
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+              int oa, ob = 0;
+              term(la0 + i0 + d, ca[d], oa);
+              cb[d] = 0.0;
+              if (lb > 0) term(lb0 + i0 + d, cb[d], ob);
+              ka[d] = S.u.K[oa + pos];
+              kb[d] = S.u.K[ob + pos];
+            }
+            __asm__ volatile("" ::: "memory");  // the reads of the batch are issued together
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+              sa = ws_acc(sa, ca[d], ka[d]);
+              sb = ws_acc(sb, cb[d], kb[d]);
+            }
           }
           S.w.part[g0][pos] = sa;
           if (g1 - g0 == 2) S.w.part[g0 + 1][pos] = sb;
