@@ -410,9 +410,6 @@ __device__ __forceinline__ double dpp_full_d(double v) {  // every lane reads it
   return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-// HALF: lanes 32 .. 63 hold neutral values (+inf for a, -inf for b), so lane 31 holds the
-// result after the row_bcast:15 step and the last step is skipped.
-template <bool HALF = false>
 __device__ __forceinline__ void wave_minmax(double &a, double &b) {
 #define SVMX_MM_FULL(CTRL)                       \
   {                                              \
@@ -433,11 +430,28 @@ __device__ __forceinline__ void wave_minmax(double &a, double &b) {
   SVMX_MM_FULL(0x124)     // row_ror:4
   SVMX_MM_FULL(0x128)     // row_ror:8
   SVMX_MM_MASK(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
-  if (!HALF) SVMX_MM_MASK(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
+  SVMX_MM_MASK(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
 #undef SVMX_MM_FULL
 #undef SVMX_MM_MASK
-  a = readlane_d(a, HALF ? 31 : 63);
-  b = readlane_d(b, HALF ? 31 : 63);
+  a = readlane_d(a, 63);
+  b = readlane_d(b, 63);
+}
+
+// Min of a over each half of the wave (lanes 0 .. 31 and 32 .. 63), left in lanes 31 and 63:
+// the first five rounds of wave_minmax, the row-15 broadcast reaching rows 1 and 3 only.
+__device__ __forceinline__ void halves_min(double &a) {
+#define SVMX_HM_FULL(CTRL)                       \
+  {                                              \
+    const double oa = dpp_full_d<CTRL>(a);       \
+    a = oa < a ? oa : a;                         \
+  }
+  SVMX_HM_FULL(0xB1)   // quad_perm [1,0,3,2]
+  SVMX_HM_FULL(0x4E)   // quad_perm [2,3,0,1]
+  SVMX_HM_FULL(0x124)  // row_ror:4
+  SVMX_HM_FULL(0x128)  // row_ror:8
+#undef SVMX_HM_FULL
+  const double oa = dpp_mov_d<0x142, 0xA>(a);  // row_bcast:15 -> rows 1, 3
+  a = oa < a ? oa : a;
 }
 
 // The pair steps on B (wave 0 only; K_BB in S.u.K): S.bn receives the new multipliers,
@@ -448,7 +462,7 @@ __device__ __forceinline__ void wave_minmax(double &a, double &b) {
 // The parameters come as values: a reference to the kernel's parameter block would make the
 // kernel keep a copy of it in scratch memory and reload fields from there inside the round.
 // MAXM bounds m: up to 64 a lane holds one member of B (position lane), above two (lane and
-// lane + 64); up to 32 the reductions stop at half the wave.  Every bound gives the same steps.
+// lane + 64).  Every bound gives the same steps (and local_solve_halves those for m <= 32).
 template <int MAXM>
 __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double tol, double frac, int64_t max_inner_p,
                                                      int64_t max_iter, int m, double b_up, double b_low, int64_t t) {
@@ -480,7 +494,7 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double
     const int cl_p = lo1 ? p1 : (l0 ? p0 : -1);
     // wave extremes of both sides, then the smallest index among the lanes holding each
     double ru = cu_v, rl = cl_v;
-    wave_minmax<MAXM <= 32>(ru, rl);
+    wave_minmax(ru, rl);
     const unsigned long long tu = (unsigned long long)__ballot(cu_v == ru);
     const unsigned long long tw = (unsigned long long)__ballot(cl_v == rl);
     int lu = __ffsll(tu) - 1, ll = __ffsll(tw) - 1;
@@ -517,6 +531,66 @@ __device__ __attribute__((noinline)) void local_solve(WsLds &S, double C, double
   }
   if (v0) S.bn[p0] = a0;
   if (v1) S.bn[p1] = a1;
+  if (lane == 0) S.steps = inner;
+}
+
+// The pair steps on B for m <= 32, as local_solve: member p sits in lanes p and p + 32, the
+// lower half offering it to I_up by f, the upper half to I_low by -f, so one chain of wave
+// reductions finds both extremes (the smallest f in I_up and the largest in I_low, ties to the
+// smaller sample index: the choices of local_solve).  Both halves update their copy of every
+// member with the same arithmetic, so the copies stay equal and the steps are those of
+// local_solve.
+__device__ __attribute__((noinline)) void local_solve_halves(WsLds &S, double C, double tol, double frac,
+                                                            int64_t max_inner_p, int64_t max_iter, int m, double b_up,
+                                                            double b_low, int64_t t) {
+  const int lane = threadIdx.x & 63, p = lane & 31;
+  const bool low = lane >= 32;
+  const bool v = p < m;
+  double f = v ? S.bf[p] : 0.0;
+  double a = v ? S.ba[p] : 0.0;
+  const int y = v ? S.by[p] : 0;
+  const int i = v ? S.bi[p] : IBIG;
+  const double tl = fmax(tol, frac * (b_low - b_up));
+  const int max_inner = (int)min<int64_t>(max_inner_p, max_iter - t);
+  // membership as in ws_in_up / ws_in_low: I_up takes y > 0 with a < C or y < 0 with a > 0,
+  // I_low the reverse; which label goes with which test is fixed for the lane
+  const bool with_below_c = low ? y < 0 : y > 0, with_above_0 = low ? y > 0 : y < 0;
+  int inner = 0;
+  for (; inner < max_inner; ++inner) {
+    const bool mem = (with_below_c & (a < C)) | (with_above_0 & (a > 0.0));
+    const double cv = mem ? (low ? -f : f) : INFINITY;
+    double r = cv;
+    halves_min(r);
+    const double ru = readlane_d(r, 31), rl = readlane_d(r, 63);  // rl = -(largest f in I_low)
+    const bool tie = low ? cv == rl : cv == ru;
+    unsigned long long tu = (unsigned long long)__ballot(cv == ru) & 0xffffffffull;
+    unsigned long long tw = (unsigned long long)__ballot(cv == rl) & ~0xffffffffull;
+    if (__popcll(tu) > 1) {
+      const int best = wave_min_int(!low && tie ? i : IBIG);
+      tu = (unsigned long long)__ballot(!low && tie && i == best);
+    }
+    if (__popcll(tw) > 1) {
+      const int best = wave_min_int(low && tie ? i : IBIG);
+      tw = (unsigned long long)__ballot(low && tie && i == best);
+    }
+    const int lu = (__ffsll(tu) - 1) & 63, ll = (__ffsll(tw) - 1) & 63;
+    const int cp = mem ? p : -1;
+    const int pu = __builtin_amdgcn_readlane(cp, lu), pl = __builtin_amdgcn_readlane(cp, ll);
+    if (pu < 0 || pl < 0) break;
+    const double fu = readlane_d(f, lu), fl = readlane_d(f, ll);
+    if (fl - fu <= tl) break;
+    const double au = readlane_d(a, lu), al = readlane_d(a, ll);
+    const double yu = (double)__builtin_amdgcn_readlane(y, lu);
+    const double yl = (double)__builtin_amdgcn_readlane(y, ll);
+    const float *Ku = S.u.K + pu * WS_QMAX, *Kl = S.u.K + pl * WS_QMAX;
+    const double kul = (double)Ku[pl];
+    const float ku = Ku[p], kl = Kl[p];
+    const PairStep ps = solve_pair(C, fu, fl, au, al, yu, yl, kul);
+    const double cu = (ps.au - au) * yu, cl = (ps.al - al) * yl;
+    f = f_update(f, cu, ku, cl, kl);
+    a = p == pu ? ps.au : (p == pl ? ps.al : a);
+  }
+  if (!low && v) S.bn[p] = a;
   if (lane == 0) S.steps = inner;
 }
 
@@ -1198,7 +1272,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       __syncthreads();
       if (wave == 0) {
         if (m <= 32)
-          local_solve<32>(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
+          local_solve_halves(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
         else if (m <= 64)
           local_solve<64>(S, sp.C, sp.tol, p.frac, p.max_inner, sp.max_iter, m, b_up, b_low, t);
         else
