@@ -61,21 +61,23 @@ __device__ __forceinline__ bool kv_lt(u64 ka, unsigned va, u64 kb, unsigned vb) 
 }
 
 // Value of lane (lane ^ d) for d = 1, 2, 4, 8, 16, 32 without LDS traffic: DPP quad
-// permutes and row rotations inside rows of 16, and the gfx950 lane swaps across rows and
-// halves (permlane16_swap with both operands x returns x of lane l for even rows and of
-// lane l + 16 for odd ones in its first result, the reverse in its second; permlane32_swap
-// likewise for the two halves).  d is a constant after unrolling.
+// permutes and a row rotation inside rows of 16; for d = 4 a left shift by 4 into the lanes
+// 0-3 and 8-11 of each row and a right shift by 4 into the lanes 4-7 and 12-15 (two moves
+// under complementary bank masks, no select); the gfx950 lane swaps across rows and halves
+// (permlane16_swap with both operands x returns, in every lane, x of the pair's lane in the
+// even row in its first result and of the lane in the odd row in its second; permlane32_swap
+// likewise for the two halves).  The DPP moves take no old value (mov_dpp: every lane they
+// write has a source), so x needs no copy.  d is a constant after unrolling.
 __device__ __forceinline__ unsigned xor_lane(unsigned x, int d) {
   const int lane = threadIdx.x & 63;
   switch (d) {
-    case 1: return (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
-    case 2: return (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+    case 1: return (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+    case 2: return (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
     case 4: {
-      const unsigned a = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x124, 0xF, 0xF, false);  // row_ror:4
-      const unsigned b = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x12C, 0xF, 0xF, false);  // row_ror:12
-      return (lane & 4) ? a : b;
+      const int t = __builtin_amdgcn_mov_dpp((int)x, 0x104, 0xF, 0x5, false);            // row_shl:4, banks 0, 2
+      return (unsigned)__builtin_amdgcn_update_dpp(t, (int)x, 0x114, 0xF, 0xA, false);  // row_shr:4, banks 1, 3
     }
-    case 8: return (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x128, 0xF, 0xF, false);  // row_ror:8
+    case 8: return (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0x128, 0xF, 0xF, false);  // row_ror:8
     case 16: {
       const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
       return (lane & 16) ? r[0] : r[1];
@@ -91,10 +93,24 @@ __device__ __forceinline__ u64 xor_lane64(u64 x, int d) {
   return ((u64)xor_lane((unsigned)(x >> 32), d) << 32) | xor_lane((unsigned)x, d);
 }
 
+// Both entries of the pair (lane & ~d, lane | d), d = 16 or 32, in every lane: lo from the
+// lane with bit d clear, hi from the one with it set (the two results of one lane swap).
+__device__ __forceinline__ void pair_lanes(unsigned x, int d, unsigned &lo, unsigned &hi) {
+  if (d == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    lo = r[0];
+    hi = r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    lo = r[0];
+    hi = r[1];
+  }
+}
+
 // Value of lane 63 - lane: the mirror inside each row of 16 (DPP row_mirror), then rows
 // exchanged by xor 48.
 __device__ __forceinline__ unsigned rev_lane(unsigned x) {
-  const unsigned m = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x140, 0xF, 0xF, false);  // row_mirror
+  const unsigned m = (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0x140, 0xF, 0xF, false);  // row_mirror
   return xor_lane(xor_lane(m, 16), 32);
 }
 
@@ -102,11 +118,24 @@ __device__ __forceinline__ unsigned rev_lane(unsigned x) {
 // smaller element, in a descending pair the larger one.  The entries of a list are distinct
 // except empty ones, which are equal and interchangeable, so one comparison decides both lanes:
 // a lane takes its partner's entry when "the partner's comes first" equals "keep the smaller".
+// For d = 16 and 32 every lane holds both entries of its pair after the lane swaps, so it takes
+// the pair's smaller or larger one directly: the same outcome without selecting the partner.
 __device__ __forceinline__ void kv_cx(u64 &k, unsigned &v, int d, bool asc) {
   const int lane = threadIdx.x & 63;
+  const bool keep_min = ((lane & d) == 0) == asc;
+  if (d >= 16) {
+    unsigned khl, khh, kll, klh, vl, vh;
+    pair_lanes((unsigned)(k >> 32), d, khl, khh);
+    pair_lanes((unsigned)k, d, kll, klh);
+    pair_lanes(v, d, vl, vh);
+    const u64 lo = ((u64)khl << 32) | kll, hi = ((u64)khh << 32) | klh;
+    const bool take_hi = kv_lt(hi, vh, lo, vl) == keep_min;  // the pair's smaller entry, or its larger one
+    k = take_hi ? hi : lo;
+    v = take_hi ? vh : vl;
+    return;
+  }
   const u64 ok = xor_lane64(k, d);
   const unsigned ov = xor_lane(v, d);
-  const bool keep_min = ((lane & d) == 0) == asc;
   if (kv_lt(ok, ov, k, v) == keep_min) {
     k = ok;
     v = ov;
@@ -138,7 +167,7 @@ __device__ __forceinline__ void wave_merge64(u64 &k, unsigned &v, u64 bk, unsign
 // row_mirror, then the lane swaps across rows and halves).
 template <int M>
 __device__ __forceinline__ unsigned mirror_lane(unsigned x) {
-  const unsigned m = (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x140, 0xF, 0xF, false);  // row_mirror
+  const unsigned m = (unsigned)__builtin_amdgcn_mov_dpp((int)x, 0x140, 0xF, 0xF, false);  // row_mirror
   if (M == 16) return m;
   const unsigned m2 = xor_lane(m, 16);
   return M == 32 ? m2 : xor_lane(m2, 32);
