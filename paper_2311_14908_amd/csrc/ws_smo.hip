@@ -136,10 +136,9 @@ __device__ __forceinline__ void kv_cx(u64 &k, unsigned &v, int d, bool asc) {
   }
   const u64 ok = xor_lane64(k, d);
   const unsigned ov = xor_lane(v, d);
-  if (kv_lt(ok, ov, k, v) == keep_min) {
-    k = ok;
-    v = ov;
-  }
+  const bool take = kv_lt(ok, ov, k, v) == keep_min;  // selects, not a branch
+  k = take ? ok : k;
+  v = take ? ov : v;
 }
 
 __device__ __forceinline__ void wave_sort64(u64 &k, unsigned &v) {
@@ -155,10 +154,9 @@ __device__ __forceinline__ void wave_sort64(u64 &k, unsigned &v) {
 __device__ __forceinline__ void wave_merge64(u64 &k, unsigned &v, u64 bk, unsigned bv) {
   const u64 rk = ((u64)rev_lane((unsigned)(bk >> 32)) << 32) | rev_lane((unsigned)bk);
   const unsigned rv = rev_lane(bv);
-  if (kv_lt(rk, rv, k, v)) {
-    k = rk;
-    v = rv;
-  }
+  const bool take = kv_lt(rk, rv, k, v);
+  k = take ? rk : k;
+  v = take ? rv : v;
 #pragma unroll
   for (int d = 32; d > 0; d >>= 1) kv_cx(k, v, d, true);
 }
@@ -199,10 +197,9 @@ __device__ __forceinline__ void seg_level(u64 &k, unsigned &v) {
   u64 ok;
   unsigned ov;
   kv_mirror<M>(k, v, ok, ov);
-  if (kv_lt(ok, ov, k, v)) {
-    k = ok;
-    v = ov;
-  }
+  const bool take = kv_lt(ok, ov, k, v);
+  k = take ? ok : k;
+  v = take ? ov : v;
   seg_clean<SEG>(k, v);
 }
 
@@ -220,10 +217,9 @@ __device__ __forceinline__ void seg_merge(u64 &k, unsigned &v, u64 bk, unsigned 
   u64 rk;
   unsigned rv;
   kv_mirror<SEG>(bk, bv, rk, rv);
-  if (kv_lt(rk, rv, k, v)) {
-    k = rk;
-    v = rv;
-  }
+  const bool take = kv_lt(rk, rv, k, v);
+  k = take ? rk : k;
+  v = take ? rv : v;
   seg_clean<SEG>(k, v);
 }
 
@@ -256,6 +252,12 @@ __device__ __forceinline__ int ws_label(const Prob &P, int64_t j) {
   return P.y ? gp(P.y)[ws_gmap(P, j)] : (j < P.len0 ? 1 : -1);
 }
 
+// A list entry: sort key and position (see the list comments above).
+struct KV {
+  u64 k;
+  unsigned v;
+};
+
 // Lane `lane` of the calling wave publishes entry `lane` of a list: the three words of the
 // candidate (key, aux, multiplier bits) or of an empty entry.
 __device__ __forceinline__ void put_cand(u64 *list, int lane, u64 key, unsigned aux, u64 abits, unsigned stamp) {
@@ -267,15 +269,18 @@ __device__ __forceinline__ void put_cand(u64 *list, int lane, u64 key, unsigned 
 }
 
 // Wave-level: merge lists first, first + step, ... below last (side `side`, h <= SEG entries
-// each; at most WS_MAXL lists) of the words at `words` into (k, v): afterwards lanes 0 .. h - 1
-// hold the h smallest, ascending (every segment of SEG lanes holds the same list).  A register
-// takes 64 / SEG lists, list i of register r in segment i; v = (list - first0) * 64 + entry
-// indexes the staging arrays, which receive each taken candidate's aux word and multiplier
-// bits.  Every lane waits for its entries of all lists at once, so the round trips overlap.
+// each; at most WS_MAXL lists) of the words at `words`: afterwards lanes 0 .. h - 1 of the
+// result hold the h smallest, ascending (every segment of SEG lanes holds the same list).  A
+// register takes 64 / SEG lists, list i of register r in segment i; v = (list - first0) * 64 +
+// entry indexes the staging arrays, which receive each taken candidate's aux word and
+// multiplier bits.  Every lane waits for its entries of all lists at once, so the round trips
+// overlap.  Not inlined, and the result comes back by value: inside the kernel the compiler
+// turned each compare-exchange into a branch with register copies (about twice the
+// instructions of the selects it emits here).
 template <int SEG>
-__device__ void merge_lists(const u64 *words, int side, int first0, int first, int last, int step, int h,
-                            unsigned stamp, unsigned *st_aux, u64 *st_ab, u64 &k, unsigned &v, uint64_t spin_limit,
-                            int32_t *err, int *abort_flag) {
+__device__ __forceinline__ KV merge_lists(const u64 *words, int side, int first0, int first, int last,
+                                                    int step, int h, unsigned stamp, unsigned *st_aux, u64 *st_ab,
+                                                    uint64_t spin_limit, int32_t *err, int *abort_flag) {
   constexpr int R = 64 / SEG;         // lists per register
   constexpr int NR = WS_MAXL / R;     // registers
   const int lane = threadIdx.x & 63;
@@ -346,8 +351,7 @@ __device__ void merge_lists(const u64 *words, int side, int first0, int first, i
 #pragma unroll
     for (int r = 0; r + span < NR; r += 2 * span)
       if (r + span < nr) seg_merge<SEG>(rk[r], rv[r], rk[r + span], rv[r + span]);
-  k = rk[0];
-  v = rv[0];
+  return KV{rk[0], rv[0]};
 }
 
 // Waits until words a and b both carry `stamp` (both loads in flight at once); returns their
@@ -895,10 +899,6 @@ __device__ __forceinline__ void wave_sort_first(u64 &k, unsigned &v) {
 // no member of the wave's best h exceeds.  Only the members at or below it are gathered in LDS
 // and sorted (over 16, 32 or 64 lanes, as many as they need), 64 at a time, the threshold
 // tightening to the list's h-th entry after each batch.
-struct KV {
-  u64 k;
-  unsigned v;
-};
 
 constexpr int WS_OWN_CHUNKS = WS_SLICE_MAX / 128;  // chunks of 64 samples one wave takes
 
@@ -1082,8 +1082,10 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     if (owner && P.g1 > 0 && rank == group_leader(P, rank / P.g1)) {
       const int g = rank / P.g1;
       const int q0 = g * P.g1, q1 = min(P.nwg, q0 + P.g1);
-      merge_lists<SEG>(P.slots + par * P.nwg * WS_LIST_WORDS, side, q0, q0 + half, q1, 2, h, stamp,
-                       S.u.st.aux[side], S.u.st.ab[side], k, v, sp.spin_limit, sp.error, &S.abort_flag);
+      const KV r = merge_lists<SEG>(P.slots + par * P.nwg * WS_LIST_WORDS, side, q0, q0 + half, q1, 2, h, stamp,
+                                    S.u.st.aux[side], S.u.st.ab[side], sp.spin_limit, sp.error, &S.abort_flag);
+      k = r.k;
+      v = r.v;
       if (half == 1) {
         S.lk[wave][lane] = k;
         S.lv[wave][lane] = v;
@@ -1104,8 +1106,10 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       const bool two = P.g1 > 0;
       const u64 *words = two ? P.slots2 + par * P.ng * WS_LIST_WORDS : P.slots + par * P.nwg * WS_LIST_WORDS;
       const int nls = two ? P.ng : P.nwg;
-      merge_lists<SEG>(words, side, 0, half, nls, 2, h, stamp, S.u.st.aux[side], S.u.st.ab[side], k, v,
-                       sp.spin_limit, sp.error, &S.abort_flag);
+      const KV r = merge_lists<SEG>(words, side, 0, half, nls, 2, h, stamp, S.u.st.aux[side], S.u.st.ab[side],
+                                    sp.spin_limit, sp.error, &S.abort_flag);
+      k = r.k;
+      v = r.v;
       if (half == 1) {
         S.lk[wave][lane] = k;
         S.lv[wave][lane] = v;
