@@ -36,25 +36,72 @@ __device__ __forceinline__ double dpp_mov_d(double v) {
   return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
+template <int CTRL>
+__device__ __forceinline__ double dpp_full_d(double v) {  // every lane reads its source lane
+  const long long b = __double_as_longlong(v);
+  const unsigned hi = (unsigned)__builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xF, 0xF, false);
+  const unsigned lo = (unsigned)__builtin_amdgcn_mov_dpp((int)b, CTRL, 0xF, 0xF, false);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
 // Wave-wide min (MAX = false) or max (MAX = true) of v, returned to every lane.  DPP row
 // operations (xor 1 and 2 inside quads, rotations by 4 and 8 inside rows of 16, then the
 // row-15 and row-31 broadcasts) leave the result in lane 63.  Lanes outside a broadcast's row
-// mask keep their own value, which min/max leaves unchanged.
+// mask keep their own value, which min/max leaves unchanged.  Compare and select: the values
+// are finite or +-inf, so fmin/fmax's quieting of NaN inputs is not needed (either zero may
+// come out of -0 against +0; callers compare with ==, for which they are equal).
 template <bool MAX>
 __device__ __forceinline__ double wave_extreme(double v) {
-#define SVMX_EXT_ROUND(CTRL, RM)                      \
+#define SVMX_EXT_FULL(CTRL)                           \
+  {                                                   \
+    const double o = dpp_full_d<CTRL>(v);             \
+    v = MAX ? (o > v ? o : v) : (o < v ? o : v);      \
+  }
+#define SVMX_EXT_MASK(CTRL, RM)                       \
   {                                                   \
     const double o = dpp_mov_d<CTRL, RM>(v);          \
-    v = MAX ? fmax(v, o) : fmin(v, o);                \
+    v = MAX ? (o > v ? o : v) : (o < v ? o : v);      \
   }
-  SVMX_EXT_ROUND(0xB1, 0xF)   // quad_perm [1,0,3,2]
-  SVMX_EXT_ROUND(0x4E, 0xF)   // quad_perm [2,3,0,1]
-  SVMX_EXT_ROUND(0x124, 0xF)  // row_ror:4
-  SVMX_EXT_ROUND(0x128, 0xF)  // row_ror:8
-  SVMX_EXT_ROUND(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
-  SVMX_EXT_ROUND(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
-#undef SVMX_EXT_ROUND
+  SVMX_EXT_FULL(0xB1)         // quad_perm [1,0,3,2]
+  SVMX_EXT_FULL(0x4E)         // quad_perm [2,3,0,1]
+  SVMX_EXT_FULL(0x124)        // row_ror:4
+  SVMX_EXT_FULL(0x128)        // row_ror:8
+  SVMX_EXT_MASK(0x142, 0xA)   // row_bcast:15 -> rows 1, 3
+  SVMX_EXT_MASK(0x143, 0xC)   // row_bcast:31 -> rows 2, 3
+#undef SVMX_EXT_FULL
+#undef SVMX_EXT_MASK
   return readlane_d(v, 63);
+}
+
+// Wave-wide min of a and max of b, returned to every lane: the DPP pattern of wave_extreme
+// (quad permutes, row rotations, then the row-15 and row-31 broadcasts into lane 63) with
+// compare-and-select (the values are finite or +-inf, so no NaN canonicalization) and the
+// two chains interleaved round by round.
+__device__ __forceinline__ void wave_minmax(double &a, double &b) {
+#define SVMX_MM_FULL(CTRL)                       \
+  {                                              \
+    const double oa = dpp_full_d<CTRL>(a);       \
+    const double ob = dpp_full_d<CTRL>(b);       \
+    a = oa < a ? oa : a;                         \
+    b = ob > b ? ob : b;                         \
+  }
+#define SVMX_MM_MASK(CTRL, RM)                   \
+  {                                              \
+    const double oa = dpp_mov_d<CTRL, RM>(a);    \
+    const double ob = dpp_mov_d<CTRL, RM>(b);    \
+    a = oa < a ? oa : a;                         \
+    b = ob > b ? ob : b;                         \
+  }
+  SVMX_MM_FULL(0xB1)      // quad_perm [1,0,3,2]
+  SVMX_MM_FULL(0x4E)      // quad_perm [2,3,0,1]
+  SVMX_MM_FULL(0x124)     // row_ror:4
+  SVMX_MM_FULL(0x128)     // row_ror:8
+  SVMX_MM_MASK(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
+  SVMX_MM_MASK(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
+#undef SVMX_MM_FULL
+#undef SVMX_MM_MASK
+  a = readlane_d(a, 63);
+  b = readlane_d(b, 63);
 }
 
 // Wave-wide min of an int, returned to every lane (same DPP pattern).
@@ -68,37 +115,21 @@ __device__ __forceinline__ int wave_min_int(int v) {
   return __builtin_amdgcn_readlane(v, 63);
 }
 
+// Lane of the winner among the lanes with `hit` (those holding the extreme value): the one with
+// the smallest index i; an index reduction runs only when several lanes tie.
+__device__ __forceinline__ int tie_lane(bool hit, int i) {
+  const unsigned long long tie = (unsigned long long)__ballot(hit);
+  if (__popcll(tie) == 1) return __ffsll(tie) - 1;
+  const int best = wave_min_int(hit ? i : IBIG);
+  return __ffsll((unsigned long long)__ballot(hit && i == best)) - 1;
+}
+
 // Lane holding the winner of one side: the extreme value, then the smallest index among the
-// lanes holding it (an index reduction runs only when several lanes tie).  This is the (value,
-// index) lexicographic order: -0 and +0 compare equal.
+// lanes holding it.  This is the (value, index) lexicographic order: -0 and +0 compare equal.
 template <bool MAX>
 __device__ __forceinline__ int winner_lane(double v, int i) {
   const double rv = wave_extreme<MAX>(v);
-  const unsigned long long tie = (unsigned long long)__ballot(v == rv);
-  if (__popcll(tie) == 1) return __ffsll(tie) - 1;
-  const int best = wave_min_int(v == rv ? i : IBIG);
-  return __ffsll((unsigned long long)__ballot(v == rv && i == best)) - 1;
-}
-
-// Winner of one side: the extreme value, then the smallest index among the lanes holding it
-// (an index reduction runs only when several lanes tie), then value, index, multiplier and label
-// read from that lane.  This is the (value, index) lexicographic order: -0 and +0 compare equal.
-template <bool MAX>
-__device__ __forceinline__ void side_winner(double v, int i, double a, int y, double &rv, int &ri, double &ra,
-                                            int &ry) {
-  rv = wave_extreme<MAX>(v);
-  const unsigned long long tie = (unsigned long long)__ballot(v == rv);
-  int lane;
-  if (__popcll(tie) == 1) {
-    lane = __ffsll(tie) - 1;
-  } else {
-    const int best = wave_min_int(v == rv ? i : IBIG);
-    lane = __ffsll((unsigned long long)__ballot(v == rv && i == best)) - 1;
-  }
-  rv = readlane_d(v, lane);  // the winner's own value (its sign of zero included)
-  ri = __builtin_amdgcn_readlane(i, lane);
-  ra = readlane_d(a, lane);
-  ry = __builtin_amdgcn_readlane(y, lane);
+  return tie_lane(v == rv, i);
 }
 
 __device__ __forceinline__ void st_word(u64 *p, u64 v) {

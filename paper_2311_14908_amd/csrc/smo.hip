@@ -63,10 +63,22 @@ __device__ __forceinline__ void sel_merge(Sel &s, const Sel &o) {
 }
 
 // Wave-wide selection, returned to every lane.  Must be called by all 64 lanes of the wave.
+// Each side's winner: its extreme value, then the smallest index among the lanes holding it
+// (the (value, index) lexicographic order; -0 and +0 compare equal), with value, index,
+// multiplier and label read from that lane.  The two sides' reductions run interleaved.
 __device__ __forceinline__ Sel sel_wave(const Sel &mine) {
+  double ru = mine.vu, rl = mine.vl;
+  wave_minmax(ru, rl);
+  const int lu = tie_lane(mine.vu == ru, mine.iu), ll = tie_lane(mine.vl == rl, mine.il);
   Sel r;
-  side_winner<false>(mine.vu, mine.iu, mine.au, mine.yu, r.vu, r.iu, r.au, r.yu);
-  side_winner<true>(mine.vl, mine.il, mine.al, mine.yl, r.vl, r.il, r.al, r.yl);
+  r.vu = readlane_d(mine.vu, lu);  // the winner's own value (its sign of zero included)
+  r.iu = __builtin_amdgcn_readlane(mine.iu, lu);
+  r.au = readlane_d(mine.au, lu);
+  r.yu = __builtin_amdgcn_readlane(mine.yu, lu);
+  r.vl = readlane_d(mine.vl, ll);
+  r.il = __builtin_amdgcn_readlane(mine.il, ll);
+  r.al = readlane_d(mine.al, ll);
+  r.yl = __builtin_amdgcn_readlane(mine.yl, ll);
   return r;
 }
 

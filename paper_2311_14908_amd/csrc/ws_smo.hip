@@ -431,45 +431,6 @@ struct WsLds {
   int64_t steps;
 };
 
-// Wave-wide min of a and max of b, returned to every lane: the DPP pattern of wave_extreme
-// (quad permutes, row rotations, then the row-15 and row-31 broadcasts into lane 63) with
-// compare-and-select (the values are finite or +-inf, so no NaN canonicalization) and the
-// two chains interleaved round by round.
-template <int CTRL>
-__device__ __forceinline__ double dpp_full_d(double v) {  // every lane reads its source lane
-  const long long b = __double_as_longlong(v);
-  const unsigned hi = (unsigned)__builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xF, 0xF, false);
-  const unsigned lo = (unsigned)__builtin_amdgcn_mov_dpp((int)b, CTRL, 0xF, 0xF, false);
-  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-}
-
-__device__ __forceinline__ void wave_minmax(double &a, double &b) {
-#define SVMX_MM_FULL(CTRL)                       \
-  {                                              \
-    const double oa = dpp_full_d<CTRL>(a);       \
-    const double ob = dpp_full_d<CTRL>(b);       \
-    a = oa < a ? oa : a;                         \
-    b = ob > b ? ob : b;                         \
-  }
-#define SVMX_MM_MASK(CTRL, RM)                   \
-  {                                              \
-    const double oa = dpp_mov_d<CTRL, RM>(a);    \
-    const double ob = dpp_mov_d<CTRL, RM>(b);    \
-    a = oa < a ? oa : a;                         \
-    b = ob > b ? ob : b;                         \
-  }
-  SVMX_MM_FULL(0xB1)      // quad_perm [1,0,3,2]
-  SVMX_MM_FULL(0x4E)      // quad_perm [2,3,0,1]
-  SVMX_MM_FULL(0x124)     // row_ror:4
-  SVMX_MM_FULL(0x128)     // row_ror:8
-  SVMX_MM_MASK(0x142, 0xA)  // row_bcast:15 -> rows 1, 3
-  SVMX_MM_MASK(0x143, 0xC)  // row_bcast:31 -> rows 2, 3
-#undef SVMX_MM_FULL
-#undef SVMX_MM_MASK
-  a = readlane_d(a, 63);
-  b = readlane_d(b, 63);
-}
-
 // Min of a over each half of the wave (lanes 0 .. 31 and 32 .. 63), left in lanes 31 and 63:
 // the first five rounds of wave_minmax, the row-15 broadcast reaching rows 1 and 3 only.
 __device__ __forceinline__ void halves_min(double &a) {
