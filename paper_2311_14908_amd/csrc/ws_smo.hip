@@ -394,6 +394,7 @@ __device__ __forceinline__ u64 poll_word(const u64 *w, unsigned stamp, uint64_t 
 struct WsLds {
   double f[WS_SLICE_MAX], a[WS_SLICE_MAX];
   signed char y[WS_SLICE_MAX];
+  u64 key[2][WS_SLICE_MAX];  // sort keys of the I_up (by f) and I_low (by -f) sides, KSENT if not a member
   u64 lk[WS_NW][64];
   unsigned lv[WS_NW][64];
   u64 pk[WS_NW][64];  // own lists: each wave's members below its threshold, 64 at a time
@@ -833,13 +834,16 @@ __device__ __attribute__((noinline)) void owner_rows(WsLds &S, SplitX X, float c
   }
 }
 
-// Key of sample pos for a side (0: I_up by f, 1: I_low by -f), or KSENT if it is not a member.
-__device__ __forceinline__ u64 side_key(const WsLds &S, int side, int pos, int len, double C) {
-  if (pos >= len) return KSENT;
-  const double fj = S.f[pos], aj = S.a[pos];
-  const int yj = S.y[pos];
-  if (!(side == 0 ? ws_in_up(yj, aj, C) : ws_in_low(yj, aj, C))) return KSENT;
-  return f_key(side == 0 ? fj : -fj);
+// Keys of sample pos for both sides (0: I_up by f, 1: I_low by -f; KSENT where it is not a
+// member), written wherever f or a of the sample is set, so that the lists read them ready-made.
+__device__ __forceinline__ void put_keys(WsLds &S, int pos, double f, double a, int y, double C) {
+  S.key[0][pos] = ws_in_up(y, a, C) ? f_key(f) : KSENT;
+  S.key[1][pos] = ws_in_low(y, a, C) ? f_key(-f) : KSENT;
+}
+
+// Key of sample pos for a side, or KSENT if it is not a member or past the slice.
+__device__ __forceinline__ u64 side_key(const WsLds &S, int side, int pos, int len) {
+  return pos < len ? S.key[side][pos] : KSENT;
 }
 
 // Bitonic sort of the first S lanes (S = 16, 32, 64): lanes S .. 63 must hold empty entries,
@@ -864,14 +868,14 @@ __device__ __forceinline__ void wave_sort_first(u64 &k, unsigned &v) {
 constexpr int WS_OWN_CHUNKS = WS_SLICE_MAX / 128;  // chunks of 64 samples one wave takes
 
 template <int SEG>
-__device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, int len, int h, double C) {
+__device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, int len, int h) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = (len + 63) / 64;
   u64 k = KSENT;
   unsigned v = VSENT;
   if (nch - half <= 2) {  // at most one chunk for this wave
     if (half < nch) {
-      u64 ck = side_key(S, side, half * 64 + lane, len, C);
+      u64 ck = side_key(S, side, half * 64 + lane, len);
       unsigned cv = ck != KSENT ? (unsigned)(half * 64 + lane) : VSENT;
       if (__ballot(ck != KSENT) != 0) wave_sort64(ck, cv);
       k = ck;
@@ -883,13 +887,18 @@ __device__ __attribute__((noinline)) KV own_list(WsLds &S, int side, int half, i
   u64 tk = KSENT;
   unsigned tv = VSENT;
 #pragma unroll
+  for (int i = 0; i < WS_OWN_CHUNKS; ++i) {  // every read first (addresses clamped into the slice)
+    const int pos = (half + 2 * i) * 64 + lane;
+    ck[i] = S.key[side][pos < len ? pos : 0];
+  }
+  __asm__ volatile("" ::: "memory");  // the reads are issued before the first is used
+#pragma unroll
   for (int i = 0; i < WS_OWN_CHUNKS; ++i) {
     const int pos = (half + 2 * i) * 64 + lane;
-    ck[i] = side_key(S, side, pos, len, C);  // empty past len
-    if (ck[i] != KSENT && kv_lt(ck[i], (unsigned)pos, tk, tv)) {
-      tk = ck[i];
-      tv = (unsigned)pos;
-    }
+    if (pos >= len) ck[i] = KSENT;  // empty past len
+    const bool better = ck[i] != KSENT && kv_lt(ck[i], (unsigned)pos, tk, tv);
+    tk = better ? ck[i] : tk;
+    tv = better ? (unsigned)pos : tv;
   }
   // minimum over groups of G lanes, then the maximum over the 64 / G >= SEG >= h groups
   constexpr int G = 64 / SEG;
@@ -994,9 +1003,12 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
   u64 *kbuf = bcast + 2 * WS_BCAST_PITCH;
 
   for (int j = tid; j < len; j += WS_BS) {
-    S.f[j] = gp(P.f)[base + j];
-    S.a[j] = gp(P.alpha)[base + j];
-    S.y[j] = (signed char)ws_label(P, base + j);
+    const double fj = gp(P.f)[base + j], aj = gp(P.alpha)[base + j];
+    const int yj = ws_label(P, base + j);
+    S.f[j] = fj;
+    S.a[j] = aj;
+    S.y[j] = (signed char)yj;
+    put_keys(S, j, fj, aj, yj, C);
   }
   if (tid == 0) S.abort_flag = 0;
   int64_t t = ctl->t;
@@ -1016,7 +1028,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     u64 k = KSENT;
     unsigned v = VSENT;
     if (owner) {
-      const KV r = own_list<SEG>(S, side, half, len, h, C);
+      const KV r = own_list<SEG>(S, side, half, len, h);
       k = r.k;
       v = r.v;
     }
@@ -1355,11 +1367,13 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         const int nnz = __popcll(m0) + __popcll(m1);
         if (lane == 0) S.nnz = nnz;
       }
-      __syncthreads();
+      // the new multipliers of the own members of B, before the barrier: the keys written with
+      // the new f below read them
       for (int q = tid; q < m; q += WS_BS) {
         const int64_t j = S.bi[q] - base;
         if (j >= 0 && j < len) S.a[j] = S.bn[q];
       }
+      __syncthreads();
       // threads as (sample, quarters): span samples by 256 / span thread groups, span a power
       // of two that divides the workgroup, so every thread's group is below ngrp
       const int nnz = S.nnz;
@@ -1423,8 +1437,14 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
                 qb[g] = ws_acc(qb[g], c[d][g], kb[d][g]);
               }
           }
-          S.f[pa] = S.f[pa] + (((qa[0] + qa[1]) + qa[2]) + qa[3]);
-          if (hb) S.f[pb] = S.f[pb] + (((qb[0] + qb[1]) + qb[2]) + qb[3]);
+          const double fa = S.f[pa] + (((qa[0] + qa[1]) + qa[2]) + qa[3]);
+          S.f[pa] = fa;
+          put_keys(S, pa, fa, S.a[pa], S.y[pa], C);
+          if (hb) {
+            const double fb = S.f[pb] + (((qb[0] + qb[1]) + qb[2]) + qb[3]);
+            S.f[pb] = fb;
+            put_keys(S, pb, fb, S.a[pb], S.y[pb], C);
+          }
         }
       } else if (rows_in_lds) {
         // each thread its one or two quarters (g0, g0 + 1) of one sample, the chains together
@@ -1471,7 +1491,9 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         __syncthreads();
         for (int pos = tid; pos < len; pos += WS_BS) {
           const double s = ((S.w.part[0][pos] + S.w.part[1][pos]) + S.w.part[2][pos]) + S.w.part[3][pos];
-          S.f[pos] = S.f[pos] + s;
+          const double fp = S.f[pos] + s;
+          S.f[pos] = fp;
+          put_keys(S, pos, fp, S.a[pos], S.y[pos], C);
         }
       } else {
       // the rows of B do not fit in LDS next to the slice: read them from the Gram
@@ -1494,7 +1516,9 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       __syncthreads();
       for (int pos = tid; pos < len; pos += WS_BS) {
         const double s = ((S.w.part[0][pos] + S.w.part[1][pos]) + S.w.part[2][pos]) + S.w.part[3][pos];
-        S.f[pos] = S.f[pos] + s;
+        const double fp = S.f[pos] + s;
+        S.f[pos] = fp;
+        put_keys(S, pos, fp, S.a[pos], S.y[pos], C);
       }
       }
     }
