@@ -55,17 +55,18 @@ constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
 // working_set = SVM_WORKING_SET_AUTO: q = 128 for rows of 256 features or more, else 32; the
 // first WS_AUTO_PROBE_ROUNDS rounds decide.  The rounds go on when they took at least as many
 // pair steps per round as a round costs in pair steps (measured on MI355X: a round of q = 32
-// costs 4.9 to 6.9 pair steps on the Gram path -- 26.7 us against 5.4 at 100,000 x 32, 23.2
-// against 4.65 at 50,000 x 128, 28.2 against 4.1 at 20,000 x 784 -- and 5.0 to 6.5 on the row
-// path -- 42.3 us against 8.4 at 100,000 x 32, 78.6 against 12.0 at 20,000 x 784; one of
-// q = 128 10.6 to 18.8 on the Gram path and 11.3 on the row path -- 77.1 us against 4.1 and
-// 135.7 against 12.0 at 20,000 x 784), else the pair solver takes over from the state the
-// rounds reached.  The thresholds sit above the break-even of the problems each q is chosen
-// for (q = 32: rows of fewer than 256 features, 4.9 to 5.0 on the Gram path).
+// costs 4.4 to 6.2 pair steps on the Gram path -- 23.0 us against 5.22 at 100,000 x 32, 20.4
+// against 4.61 at 50,000 x 128, 25.1 against 4.05 at 20,000 x 784 -- and 4.7 on the row path
+// -- 38.7 us against 8.25 at 100,000 x 32; one of q = 128 9.9 to 18.1 on the Gram path -- 45.8
+// us against 4.61 at 50,000 x 128, 65.1 against 5.22 at 100,000 x 32, 73.4 against 4.05 at
+// 20,000 x 784 -- and about 11.4 on the row path, 135 us against 11.8 at 20,000 x 784), else
+// the pair solver takes over from the state the rounds reached.  The thresholds sit above the
+// break-even of the problems each q is chosen for (q = 32: rows of fewer than 256 features,
+// 4.4 on the Gram path; q = 128: 18.1).
 constexpr int64_t WS_AUTO_PROBE_ROUNDS = 128;
 double ws_auto_min_steps(int32_t q, bool gram) {
   if (q >= 128) return gram ? 20.0 : 12.5;
-  return gram ? 6.5 : 7.0;
+  return gram ? 5.0 : 5.5;
 }
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
