@@ -129,6 +129,18 @@ typedef struct {
                                 on it. */
   int32_t selection;         /* svm_selection (binary and one-vs-one training) */
   int32_t reserved;          /* must be 0 */
+  const double *alpha_init;  /* binary training: device [n] multipliers to start from instead of 0
+                                (a warm start, e.g. to resume a call stopped by max_iter), or NULL.
+                                Must be finite with 0 <= a_i <= C and |sum a_i y_i| <= 1e-9 C n
+                                (the equality constraint), else SVM_EINVAL.  The buffer may be the
+                                alpha argument itself; it is read before the call writes alpha.
+                                svm_train_ovo rejects it (SVM_EINVAL). */
+  const double *f_init;      /* with alpha_init: device [n] values f_i = sum_j a_j y_j K_ij - y_i
+                                that go with it (a previous call's f_out), or NULL: recomputed on
+                                the device from alpha_init -- from the Gram on the Gram path, from X
+                                with the exact fp64 kernel otherwise.  With the f_out of a call
+                                stopped by max_iter, the resumed call takes the steps the
+                                uninterrupted one would have taken.  Must be finite. */
 } svm_options;
 
 typedef struct {

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build", "svmx")
-SOURCES = ["api.cpp", "smo.hip", "ws_smo.hip", "gram.hip", "gram_split.hip", "predict.hip"]
+SOURCES = ["api.cpp", "smo.hip", "ws_smo.hip", "gram.hip", "gram_split.hip", "predict.hip", "warm.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",

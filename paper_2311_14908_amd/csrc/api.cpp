@@ -19,6 +19,7 @@
 #include <vector>
 
 #include "common.hpp"
+#include "warm.hpp"
 #include "svmx.h"
 
 using namespace svmx;
@@ -90,6 +91,8 @@ struct Opts {
   int32_t working_set;
   int32_t resident_rows;
   int32_t selection;
+  const double *alpha_init;
+  const double *f_init;
 };
 
 bool resolve(const svm_options *o, int64_t n, Opts *r) {
@@ -113,6 +116,8 @@ bool resolve(const svm_options *o, int64_t n, Opts *r) {
   r->working_set = o->working_set;
   r->resident_rows = o->resident_rows;
   r->selection = o->selection;
+  r->alpha_init = o->alpha_init;
+  r->f_init = o->f_init;
   if (o->reserved != 0 || (r->selection != SVM_SELECT_MVP && r->selection != SVM_SELECT_SECOND_ORDER)) return false;
   if (r->selection == SVM_SELECT_SECOND_ORDER && r->working_set > 0) return false;
   const bool ws_ok = r->working_set == 0 || r->working_set == SVM_WORKING_SET_AUTO ||
@@ -226,7 +231,7 @@ struct TrainPlan {
   Shape pair_shape;      // the pair solver's shape, for a switch
   int32_t cache_cap;
   int64_t off_f, off_gram, off_split, off_sqn, off_cache, off_tags, off_ctl, off_prob, off_wgp, off_slots, off_slots2,
-      off_tul, off_tb, off_fin, off_err, off_rounds;
+      off_tul, off_tb, off_fin, off_err, off_rounds, off_warm;
   int64_t slot_words, slot2_words;
   int64_t total;
 };
@@ -301,6 +306,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o_in, TrainPlan *p) {
   p->off_fin = L.add(8 * 4);
   p->off_err = L.add(16);
   p->off_rounds = L.add(8);
+  p->off_warm = o.alpha_init ? L.add(12LL * n) : -1;  // warm start: support-vector list (coefs, indices)
   p->total = round_up(L.total, ALIGN);
   return SVM_OK;
 }
@@ -617,6 +623,37 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
   hipStream_t stream = r.stream;
   s0 = check_labels_pm1(y, n, stream);
   if (s0 != SVM_OK) return s0;
+  // warm start: the given multipliers (and f) read to the host before anything writes alpha,
+  // checked, and their support vectors listed for the device
+  std::vector<double> warm_a, warm_f, warm_coef;
+  std::vector<int32_t> warm_y, warm_sv;
+  if (r.f_init && !r.alpha_init) return fail(SVM_EINVAL, "f_init needs alpha_init");
+  if (r.alpha_init) {
+    warm_a.resize(n);
+    warm_y.resize(n);
+    HIPCHK(hipMemcpyAsync(warm_a.data(), r.alpha_init, 8 * n, hipMemcpyDeviceToHost, stream));
+    HIPCHK(hipMemcpyAsync(warm_y.data(), y, 4 * n, hipMemcpyDeviceToHost, stream));
+    if (r.f_init) {
+      warm_f.resize(n);
+      HIPCHK(hipMemcpyAsync(warm_f.data(), r.f_init, 8 * n, hipMemcpyDeviceToHost, stream));
+    }
+    HIPCHK(hipStreamSynchronize(stream));
+    double sum_ay = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+      const double a = warm_a[i];
+      if (!(std::isfinite(a) && a >= 0.0 && a <= C))
+        return fail(SVM_EINVAL, "alpha_init[%lld] = %g is outside [0, C]", (long long)i, a);
+      sum_ay += a * (double)warm_y[i];
+      if (a > 0.0) {
+        warm_sv.push_back((int32_t)i);
+        warm_coef.push_back(a * (double)warm_y[i]);
+      }
+    }
+    if (!(std::fabs(sum_ay) <= 1e-9 * C * (double)n))
+      return fail(SVM_EINVAL, "alpha_init breaks the equality constraint: sum a_i y_i = %g", sum_ay);
+    for (int64_t i = 0; i < (int64_t)warm_f.size(); ++i)
+      if (!std::isfinite(warm_f[i])) return fail(SVM_EINVAL, "f_init[%lld] is not finite", (long long)i);
+  }
 
   char *ws = static_cast<char *>(workspace);
   double *f = reinterpret_cast<double *>(ws + p.off_f);
@@ -677,6 +714,21 @@ static svm_status train_impl(const float *X, const int32_t *y, int64_t n, int64_
 
   HIPCHK(ts.start(stream));
   HIPCHK(launch_solver_init(dprob, 1, n, stream));
+  if (r.alpha_init) {
+    HIPCHK(hipMemcpyAsync(alpha, warm_a.data(), 8 * n, hipMemcpyHostToDevice, stream));
+    if (r.f_init) {
+      HIPCHK(hipMemcpyAsync(f, warm_f.data(), 8 * n, hipMemcpyHostToDevice, stream));
+    } else {
+      const int64_t nsv = (int64_t)warm_sv.size();
+      double *dcoef = reinterpret_cast<double *>(ws + p.off_warm);
+      int32_t *dsv = reinterpret_cast<int32_t *>(ws + p.off_warm + 8 * n);
+      if (nsv > 0) {
+        HIPCHK(hipMemcpyAsync(dcoef, warm_coef.data(), 8 * nsv, hipMemcpyHostToDevice, stream));
+        HIPCHK(hipMemcpyAsync(dsv, warm_sv.data(), 4 * nsv, hipMemcpyHostToDevice, stream));
+      }
+      HIPCHK(launch_f_from_alpha(dsv, dcoef, nsv, y, n, G, p.ld, X, d, gamma, f, stream));
+    }
+  }
   SolveParams sp{};
   sp.probs = dprob;
   sp.wg_prob = wgp;
@@ -898,6 +950,7 @@ svm_status svm_train_ovo(const float *X, const int32_t *label, int64_t n, int64_
     return fail(SVM_EINVAL, "C, gamma and tol must be finite and > 0");
   Opts r;
   if (!resolve(o, n, &r)) return fail(SVM_EINVAL, "bad options");
+  if (r.alpha_init || r.f_init) return fail(SVM_EINVAL, "alpha_init / f_init: binary training only");
   OvoPlan p;
   svm_status s0 = plan_ovo(n, d, k, r, &p);
   if (s0 != SVM_OK) return s0;

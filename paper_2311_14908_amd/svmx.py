@@ -37,7 +37,8 @@ class svm_options(C.Structure):
                 ("trace_len", C.c_int32), ("trace_ws", C.POINTER(C.c_int32)), ("trace_b", C.POINTER(C.c_double)),
                 ("f_out", C.c_void_p), ("stream", C.c_void_p), ("workgroups", C.c_int32),
                 ("exchange_levels", C.c_int32), ("gram_mfma", C.c_int32), ("working_set", C.c_int32),
-                ("resident_rows", C.c_int32), ("selection", C.c_int32), ("reserved", C.c_int32)]
+                ("resident_rows", C.c_int32), ("selection", C.c_int32), ("reserved", C.c_int32),
+                ("alpha_init", C.c_void_p), ("f_init", C.c_void_p)]
 
 
 class svm_stats(C.Structure):
@@ -115,7 +116,8 @@ def _dev(t: torch.Tensor, dtype, name):
 
 def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, check_every=0, trace_len=0,
             workgroups=0, exchange_levels=0, gram_mfma=0, working_set=0, resident_rows=0, selection=0,
-            f_out: torch.Tensor | None = None, stream=None):
+            f_out: torch.Tensor | None = None, stream=None, alpha_init: torch.Tensor | None = None,
+            f_init: torch.Tensor | None = None):
     o = svm_options()
     load().svm_default_options(C.byref(o))
     o.gram = gram
@@ -132,6 +134,8 @@ def options(gram=GRAM_AUTO, gram_budget_bytes=0, row_cache_bytes=0, max_iter=0, 
     o.resident_rows = resident_rows
     o.selection = selection
     o.f_out = None if f_out is None else f_out.data_ptr()
+    o.alpha_init = None if alpha_init is None else _dev(alpha_init, torch.float64, "alpha_init").data_ptr()
+    o.f_init = None if f_init is None else _dev(f_init, torch.float64, "f_init").data_ptr()
     s = stream if stream is not None else torch.cuda.current_stream()
     o.stream = s.cuda_stream
     return o

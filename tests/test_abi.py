@@ -37,8 +37,9 @@ def test_struct_layouts_match_header():
     lib = svmx.load()
     o = svmx.svm_options()
     lib.svm_default_options(C.byref(o))
-    assert o.struct_size == C.sizeof(svmx.svm_options) == 104
+    assert o.struct_size == C.sizeof(svmx.svm_options) == 120
     assert o.selection == svmx.SELECT_MVP and o.reserved == 0
+    assert o.alpha_init is None and o.f_init is None  # no warm start by default
     assert o.check_every == 65536 and o.gram == svmx.GRAM_AUTO
     assert C.sizeof(svmx.svm_stats) == 120
 
