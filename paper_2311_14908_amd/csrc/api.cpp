@@ -61,13 +61,15 @@ constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
 // -- 38.7 us against 8.25 at 100,000 x 32; one of q = 128 9.9 to 18.1 on the Gram path -- 45.8
 // us against 4.61 at 50,000 x 128, 65.1 against 5.22 at 100,000 x 32, 73.4 against 4.05 at
 // 20,000 x 784 -- and about 11.4 on the row path, 135 us against 11.8 at 20,000 x 784), else
-// the pair solver takes over from the state the rounds reached.  The thresholds sit above the
-// break-even of the problems each q is chosen for (q = 32: rows of fewer than 256 features,
-// 4.4 on the Gram path; q = 128: 18.1).
+// the pair solver takes over from the state the rounds reached.  Steps a round rise over a
+// training (at 100,000 x 32 from 6.5 in the first 128 rounds to 8.6 over all; on the
+// 50,000 x 128 mixture from 4.3 to 4.8), so the q = 32 thresholds sit a little under the
+// break-even of the problems that q is chosen for (rows of fewer than 256 features: 4.4 on the
+// Gram path, 4.7 on the row path); q = 128 keeps a margin above its 18.1.
 constexpr int64_t WS_AUTO_PROBE_ROUNDS = 128;
 double ws_auto_min_steps(int32_t q, bool gram) {
   if (q >= 128) return gram ? 20.0 : 12.5;
-  return gram ? 5.0 : 5.5;
+  return gram ? 4.25 : 4.5;
 }
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
