@@ -18,7 +18,8 @@
 //      collects it into LDS, runs the pair steps on B in one wave until the gap on B is at most
 //      max(tol, frac * gap of the round) or the round's step cap is reached, and publishes the
 //      new multipliers of B; meanwhile every owner loads the Gram rows of B over its own
-//      samples into LDS;
+//      samples into LDS (over as many of them as 16,384 entries hold; the rest of the slice
+//      reads them from the Gram in step 4);
 //   4. every owner adds sum_p c_p K(B_p, j) to f_j of its own samples (c_p the change of a y
 //      at B_p, in a fixed grouping of B's order) and stores the new multipliers of its
 //      members of B.
@@ -1172,8 +1173,11 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
     // Gram path: the owners fetch K_BB from the Gram between them and publish it, then load the
     // Gram rows of B over their own samples while the pair steps run.  Row path: every owner
     // evaluates K(B, own samples) and publishes the columns of K_BB of its own members of B.
-    // The solving workgroup collects K_BB.
-    const bool rows_in_lds = GRAM ? owner && !solo && m * len <= WS_QMAX * WS_QMAX : owner;
+    // The solving workgroup collects K_BB.  On the Gram path the rows of B over the first lcap
+    // own samples fit in LDS (over all of them while m len <= WS_QMAX^2); the f update reads the
+    // rest of the slice from the Gram.
+    const int lcap = !GRAM || m * len <= WS_QMAX * WS_QMAX ? len : (WS_QMAX * WS_QMAX) / m;
+    const bool rows_in_lds = GRAM ? owner && !solo : owner;
     const size_t kpar = par * (size_t)(WS_QMAX * WS_QMAX);
     const unsigned kstamp = (unsigned)(round + 1);
     if (tid < m) {
@@ -1315,13 +1319,13 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
       }
       // owners: the Gram rows of B over the own samples into LDS while the pair steps run
       if (GRAM && rows_in_lds) {
-        const int ml = m * len;
+        const int ml = m * lcap;
         for (int e0 = 0; e0 < ml; e0 += WS_BS * WS_GATHER) {
           float kv[WS_GATHER];
 #pragma unroll
           for (int b = 0; b < WS_GATHER; ++b) {
             const int e = min(e0 + b * WS_BS + tid, ml - 1);
-            const int ra = e / len, pos = e - ra * len;
+            const int ra = e / lcap, pos = e - ra * lcap;
             kv[b] = gp(sp.gram)[S.roff[ra] + ws_gmap(P, base + pos)];
           }
 #pragma unroll
@@ -1398,14 +1402,14 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
         const bool in = g < WS_QUARTERS && idx < (g + 1) * nnz / WS_QUARTERS;
         const int ic = in ? idx : 0;
         tc[r] = in ? S.nzc[ic] : 0.0;
-        to[r] = in ? S.nzp[ic] * len : 0;
+        to[r] = in ? S.nzp[ic] * lcap : 0;
       }
       if (ngrp == 1 && rows_in_lds) {
         // every thread sums all four quarters of two of its samples in registers: the eight
         // chains advance together, each in its own order, so the sums are those written
-        for (int pa = tid; pa < len; pa += 2 * WS_BS) {
+        for (int pa = tid; pa < lcap; pa += 2 * WS_BS) {
           const int pb = pa + WS_BS;
-          const bool hb = pb < len;
+          const bool hb = pb < lcap;
           double qa[WS_QUARTERS], qb[WS_QUARTERS];
 #pragma unroll
           for (int g = 0; g < WS_QUARTERS; ++g) qa[g] = qb[g] = 0.0;
@@ -1444,6 +1448,47 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
             const double fb = S.f[pb] + (((qb[0] + qb[1]) + qb[2]) + qb[3]);
             S.f[pb] = fb;
             put_keys(S, pb, fb, S.a[pb], S.y[pb], C);
+          }
+        }
+        // the samples past lcap: the same four chains with the rows read from the Gram (term
+        // slots as above, with the Gram row offset; 0, the first row, past a quarter's end),
+        // eight terms of each a batch, all 32 reads issued before the first is used (QL is a
+        // multiple of eight and at least qlen, so a batch stays inside the quarters' slots)
+        if (lcap < len) {
+          int64_t tg[NSR];
+#pragma unroll
+          for (int r = 0; r < NSR; ++r) {
+            const int sl = r * 64 + lane, g = sl / QL, i = sl - g * QL;
+            const int idx = g * nnz / WS_QUARTERS + i;
+            const bool in = g < WS_QUARTERS && idx < (g + 1) * nnz / WS_QUARTERS;
+            tg[r] = in ? S.nzoff[in ? idx : 0] : 0;
+          }
+          for (int pos = lcap + tid; pos < len; pos += WS_BS) {
+            const int64_t gj = ws_gmap(P, base + pos);
+            double qs[WS_QUARTERS];
+#pragma unroll
+            for (int g = 0; g < WS_QUARTERS; ++g) qs[g] = 0.0;
+            for (int i0 = 0; i0 < qlen; i0 += 8) {
+              double c[8][WS_QUARTERS];
+              float kk[8][WS_QUARTERS];
+#pragma unroll
+              for (int d = 0; d < 8; ++d)
+#pragma unroll
+                for (int g = 0; g < WS_QUARTERS; ++g) {
+                  const int sl = (g * QL) % 64 + i0 + d;
+                  c[d][g] = readlane_d(tc[(g * QL) / 64], sl);
+                  const int64_t ro = (int64_t)readlane64((u64)tg[(g * QL) / 64], sl);
+                  kk[d][g] = gp(sp.gram)[ro + gj];
+                }
+              __asm__ volatile("" ::: "memory");
+#pragma unroll
+              for (int d = 0; d < 8; ++d)
+#pragma unroll
+                for (int g = 0; g < WS_QUARTERS; ++g) qs[g] = ws_acc(qs[g], c[d][g], kk[d][g]);
+            }
+            const double fp = S.f[pos] + (((qs[0] + qs[1]) + qs[2]) + qs[3]);
+            S.f[pos] = fp;
+            put_keys(S, pos, fp, S.a[pos], S.y[pos], C);
           }
         }
       } else if (rows_in_lds) {
@@ -1496,7 +1541,7 @@ __global__ void __launch_bounds__(WS_BS) ws_solve(WsParams p) {
           put_keys(S, pos, fp, S.a[pos], S.y[pos], C);
         }
       } else {
-      // the rows of B do not fit in LDS next to the slice: read them from the Gram
+      // one workgroup alone (LDS holds K_BB): the rows of B read from the Gram
       for (int pos = tid - grp * span; pos < len; pos += WS_BS) {
         const int64_t gj = ws_gmap(P, base + pos);
         for (int g = g0; g < g1; ++g) {

@@ -112,8 +112,9 @@ def test_ws_c0_against_oracle(c0, q):
                                      (20000, 128, 0)])
 def test_ws_sizes_and_levels(n, q, wgs):
     """One workgroup, one merge level (up to 16 workgroups) and two levels (above 16), ragged
-    slices (150 and 149 samples: the f update's thread mapping for slices of 129..192 samples,
-    with the Gram rows of B read from HBM and from LDS), working sets larger than the problem:
+    slices (150 and 149 samples: the f update's thread mapping for slices of 129..192 samples;
+    at q = 128 the Gram rows of B over the first 128 samples of a slice come from LDS and the
+    rest from HBM), working sets larger than the problem:
     the rounds up to the first near tie against
     the oracle, the optimum, feasibility and decisions.  tol = 1e-5: past a near tie the two
     solvers stop at different points of the tol-optimal set, whose decisions may differ by about
@@ -135,11 +136,15 @@ def test_ws_sizes_and_levels(n, q, wgs):
     check_decisions(d_gpu, oracle.decision(X, y, ref.alpha, ref.b, T, 0.3))
 
 
-def test_ws_configurations_agree():
-    """Workgroup counts (one merge level and two) and host check cadences change nothing."""
+@pytest.mark.parametrize("q", [64, 32])
+def test_ws_configurations_agree(q):
+    """Workgroup counts (one merge level and two) and host check cadences change nothing: with 9
+    workgroups a slice holds 1,000 samples, so the f update reads the Gram rows of B over the
+    first 16,384 / q of them (256 at q = 64, 512 at q = 32) from LDS and over the rest from HBM;
+    with 64 or more every row comes from LDS."""
     X, y = synth.two_blobs(9000, 8, seed=17)
     Xd, yd = dev(X), dev(y)
-    kw = dict(working_set=64, trace_len=500)
+    kw = dict(working_set=q, trace_len=500)
     base = svmx.svm_train(Xd, yd, 1.0, 0.3, 1e-3, workgroups=9, **kw)
     for wgs, ce in [(16, 0), (17, 0), (64, 0), (141, 0), (0, 0), (0, 1), (0, 500)]:
         out = svmx.svm_train(Xd, yd, 1.0, 0.3, 1e-3, workgroups=wgs, check_every=ce, **kw)
