@@ -214,3 +214,31 @@ def test_auto_full_size(cid, gram, schedule):
     assert abs(float(a @ y)) <= 1e-9 * wl.C * len(y)
     f = oracle.f_from_alpha(X, y, a, wl.gamma)
     kkt_and_gap(f, y, a, out.b, wl.C, wl.tol, slack=1e-4)
+
+
+def test_rounds_past_the_lds_rows():
+    """140,000 samples of the 100,000 x 32 recipe with the Gram and working_set = AUTO: the 255
+    owners hold slices of 549-550 samples, more than the 16,384 / 32 = 512 whose Gram rows of B
+    fit in LDS, so every round's f update also reads the rest of each slice from the Gram.  The
+    schedule stays on rounds and the solution passes feasibility, tol-KKT and the duality gap on
+    every row with f recomputed by the oracle from the GPU's alpha."""
+    wl = synth.workload(3)
+    n = 140_000
+    assert -(-n // 255) > 16_384 // 32
+    X, y, _, _ = synth.generate(3, n=n, m=1)
+    Xd, yd = dev(X), dev(y)
+    out = svmx.svm_train(Xd, yd, wl.C, wl.gamma, wl.tol, gram=svmx.GRAM_ON, working_set=svmx.WORKING_SET_AUTO)
+    assert out.status == svmx.SVM_OK
+    st = out.stats
+    print(f"\nn={n}: schedule {st['schedule']}, {st['rounds']} rounds, {st['iterations']} pair steps, "
+          f"W={st['dual_obj']:.9f}")
+    assert st["schedule"] == 1
+    a = out.alpha.cpu().numpy()
+    b = out.b
+    del out, Xd, yd
+    torch.cuda.empty_cache()
+    assert np.all(a >= 0) and np.all(a <= wl.C)
+    assert abs(float(a @ y)) <= 1e-9 * wl.C * n
+    f = oracle.f_from_alpha(X, y, a, wl.gamma)
+    gap, W = kkt_and_gap(f, y, a, b, wl.C, wl.tol, slack=1e-4)
+    assert abs(W - st["dual_obj"]) <= 1e-6 * abs(W)
