@@ -224,12 +224,16 @@ __global__ void __launch_bounds__(SBS) gram_rbf_f16x3(SplitX s, int64_t n, float
   }
 }
 
-// Rows of up to 128 features (at most four k stages): the build is bound by its stores, not by
-// the MFMA, and what limits the stores is how many a CU keeps in flight.  One LDS stage (32 KB,
-// loaded, then multiplied, no register prefetch) instead of two, so four workgroups share a CU
-// instead of two; a diagonal tile writes each upper value to both of its places instead of
-// mirroring through LDS.  Same products in the same order, so the same values.  Measured:
-// 13.9 -> 11.3-11.7 ms at 100,000 x 32 (40 GB), 3.5 -> 3.3 ms at 50,000 x 128.
+// One LDS stage (32 KB, loaded, then multiplied, no register prefetch) instead of two, so four
+// workgroups share a CU instead of two; a diagonal tile writes each upper value to both of its
+// places instead of mirroring through LDS.  Same products in the same order, so the same
+// values.  Short rows are bound by the stores, and four workgroups a CU keep twice as many in
+// flight: 13.9 -> 11.3-11.7 ms at 100,000 x 32 (40 GB), 3.5 -> 3.3 ms at 50,000 x 128.  Long
+// rows are bound by the stage loads and the MFMA schedule, and there the other workgroups'
+// products cover each one's loads better than one stage of register prefetch in two:
+// 1.34 -> 1.12 ms at 20,000 x 784, 10.95 -> 9.73 ms at 60,000 x 784, 0.66 -> 0.53 ms at
+// 20,000 x 256.  The two-stage kernel remains for a Gram whose row pitch or base does not
+// allow float4 stores.
 __global__ void __launch_bounds__(SBS, 4) gram_rbf_f16x3_lds1(SplitX s, int64_t n, float c, float *__restrict__ G,
                                                              int64_t ld, int64_t nt, int64_t ntiles) {
   __shared__ SplitStage S[1];
@@ -332,14 +336,11 @@ hipError_t launch_gram_split(const float *X, int64_t n, int64_t d, float gamma, 
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
   const float c = -gamma * 1.4426950408889634f;
   const bool st4 = (ld % 4 == 0) && ((reinterpret_cast<uintptr_t>(G) & 15) == 0);
-  if (st4 && s.dp <= 4 * SKS) {
+  if (st4) {
     hipLaunchKernelGGL(gram_rbf_f16x3_lds1, dim3((unsigned)grid), dim3(SBS), 0, st, s, n, c, G, ld, nt, ntiles);
     return hipGetLastError();
   }
-  if (st4)
-    hipLaunchKernelGGL((gram_rbf_f16x3<true>), dim3((unsigned)grid), dim3(SBS), 0, st, s, n, c, G, ld, nt, ntiles);
-  else
-    hipLaunchKernelGGL((gram_rbf_f16x3<false>), dim3((unsigned)grid), dim3(SBS), 0, st, s, n, c, G, ld, nt, ntiles);
+  hipLaunchKernelGGL((gram_rbf_f16x3<false>), dim3((unsigned)grid), dim3(SBS), 0, st, s, n, c, G, ld, nt, ntiles);
   return hipGetLastError();
 }
 
