@@ -11,10 +11,13 @@ namespace svmx {
 // to its right (each row-major; the last one may be narrower).  A run of consecutive indices
 // (what the workgroups of one XCD hold at once) therefore reads SUPER row slabs and SUPER column
 // slabs, which stay in that XCD's L2, instead of one row slab and a different column slab per
-// tile.  Bijective onto the upper triangle for every nt >= 1.
+// tile.  Bijective onto the upper triangle for every nt >= 1 and SUPER >= 1.  SUPER = 8 suits
+// long rows, whose slabs are the traffic; short rows are bound by the tile stores, which a
+// wider super-tile (32) keeps on fewer rows of the Gram at a time.
 constexpr int64_t SUPER = 8;
 
-__host__ __device__ inline void upper_tile_super(int64_t lin, int64_t nt, int64_t &ti, int64_t &tj) {
+__host__ __device__ inline void upper_tile_super(int64_t lin, int64_t nt, int64_t &ti, int64_t &tj,
+                                                 const int64_t SUPER = svmx::SUPER) {
   int64_t I = 0, base = 0, r = 0, right = 0;
   for (;;) {
     r = nt - SUPER * I < SUPER ? nt - SUPER * I : SUPER;
