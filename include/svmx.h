@@ -106,10 +106,11 @@ typedef struct {
   int32_t working_set;       /* 0 = one maximal violating pair per step with f updated every step
                                 (Section III.B).  SVM_WORKING_SET_AUTO (-1): binary training with
                                 the first-order rule, no trace and automatic workgroups, n > 4096:
-                                rounds of q = 128 (rows of 256 features or more) or 32 for the first
-                                128 rounds, continued if they took at least as many pair steps per
-                                round as a round costs (Gram path: 20 at q = 128, 4.25 at 32; row
-                                path: 12.5 and 4.5, measured on MI355X), else the per-step solver
+                                rounds of q = 64 with a Gram and 128 without (rows of 256 features
+                                or more), else 32, for the first 128 rounds, continued if they took
+                                at least as many pair steps per round as a round costs (Gram path:
+                                10 at q = 64, 4.25 at 32; row path: 12.5 at q = 128, 4.5 at 32,
+                                measured on MI355X), else the per-step solver
                                 takes over from their state (svm_stats.schedule says which); every
                                 other case per-step.  Deterministic: the rule reads the state after
                                 a fixed number of rounds, not the host check cadence.

@@ -53,8 +53,9 @@ constexpr int64_t LDS_BYTES = 160 * 1024;
 constexpr int32_t MAX_CLASSES = 64;
 constexpr double WS_FRAC = 0.5;           // working-set rounds stop at max(tol, 0.5 x the round's gap)
 constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
-// working_set = SVM_WORKING_SET_AUTO: q = 128 for rows of 256 features or more, else 32; the
-// first WS_AUTO_PROBE_ROUNDS rounds decide.  The rounds go on when they took at least as many
+// working_set = SVM_WORKING_SET_AUTO: for rows of 256 features or more q = 64 with a Gram (47.0
+// ms against 49.4 with q = 128 at 20,000 x 784) and 128 without (88.5 ms against 109.5 with
+// q = 64), else 32; the first WS_AUTO_PROBE_ROUNDS rounds decide.  The rounds go on when they took at least as many
 // pair steps per round as a round costs in pair steps (measured on MI355X: a round of q = 32
 // costs 4.4 to 6.2 pair steps on the Gram path -- 23.0 us against 5.22 at 100,000 x 32, 20.4
 // against 4.61 at 50,000 x 128, 25.1 against 4.05 at 20,000 x 784 -- and 4.7 on the row path
@@ -69,6 +70,7 @@ constexpr int32_t WS_INNER_PER_Q = 100;   // and take at most 100 q pair steps
 constexpr int64_t WS_AUTO_PROBE_ROUNDS = 128;
 double ws_auto_min_steps(int32_t q, bool gram) {
   if (q >= 128) return gram ? 20.0 : 12.5;
+  if (q >= 64) return gram ? 10.0 : 8.0;  // break-evens 9.75 (39.5 us against 4.05 at 20,000 x 784), 7.8
   return gram ? 4.25 : 4.5;
 }
 
@@ -261,7 +263,7 @@ svm_status plan_train(int64_t n, int64_t d, const Opts &o_in, TrainPlan *p) {
     // rounds only where a problem spreads over several workgroups, with the first-order rule,
     // no trace (a trace records pair steps) and the automatic workgroup count
     o.working_set = 0;
-    const int32_t q = d >= 256 ? 128 : 32;
+    const int32_t q = d >= 256 ? (p->gram ? 64 : 128) : 32;
     Shape ws;
     if (o.selection == SVM_SELECT_MVP && o.trace_len == 0 && o.workgroups == 0 && n > 4096 &&
         choose_ws_shape(n, 0, q, p->gram, &ws) && ws.nwg > 1) {
